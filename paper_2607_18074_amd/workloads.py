@@ -1,0 +1,173 @@
+"""Seeded synthetic workloads: graphs, edge vectors, radial features and tensors.
+
+This module holds input generation only, none of the convolution's
+arithmetic; the float64 oracle and the HIP library both consume what it makes.
+
+The five named workloads follow the benchmark configurations: the paper's own
+position sets and graphs are not published (§5.1 builds radius graphs on one
+unstated position set), so each is a uniform random stand-in with the stated
+node count, mean degree and cutoff.
+
+* ``tiny``: 64 nodes, 1024 directed edges; receiver uniform over nodes, sender
+  uniform over the other 63 (duplicates allowed); direction uniform on the
+  sphere, length uniform in [0.5, 5.0].
+* ``small`` / ``medium`` / ``wide`` / ``stress``: positions uniform in a cube
+  [0, L]^3 (non-periodic) whose side L solves (N-1) F(r_c/L) = target degree,
+  F the distance CDF of two uniform points in the unit cube; edges are all
+  ordered pairs closer than r_c; evec = p_sender - p_receiver.
+
+Edges are sorted by (receiver, sender, generation index), giving the
+receiver-sorted CSR (rowptr, sender).  Radial features are K Bessel functions
+with the DimeNet polynomial envelope (p = 6) at cutoff r_c, evaluated in
+float64 and cast to float32.  Node features and output cotangents are N(0, 1);
+weights are N(0, col_std^2) with the per-column standard deviation given by
+the caller (it depends on the path table, which is the method's business).
+Seeds: ``SeedSequence(seed).spawn(6)`` for {positions/edges,
+lengths/directions, x, W, m_bar, cotangents}.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+CONFIGS = {
+    "tiny": dict(index=0, kind="tiny", N=64, E=1024, r_c=5.0, K=8,
+                 irreps_in="8x0e+8x1o", lmax=1, irreps_out="8x0e+8x1o",
+                 passes=("fwd",)),
+    "small": dict(index=1, kind="cube", N=2000, degree=32.0, r_c=5.0, K=8,
+                  irreps_in="32x0e+32x1o+32x2e", lmax=2, irreps_out="32x0e+32x1o+32x2e",
+                  passes=("fwd", "bwd")),
+    "medium": dict(index=2, kind="cube", N=20000, degree=50.0, r_c=5.0, K=16,
+                   irreps_in="64x0e+64x1o+64x1e+64x2e", lmax=3,
+                   irreps_out="64x0e+64x1o+64x1e+64x2e", passes=("fwd", "bwd", "dbwd")),
+    "wide": dict(index=3, kind="cube", N=50000, degree=40.0, r_c=5.0, K=16,
+                 irreps_in="128x0e+128x1o+128x2e+64x3o", lmax=3,
+                 irreps_out="128x0e+128x1o+128x2e+64x3o", passes=("fwd", "bwd")),
+    "stress": dict(index=4, kind="cube", N=200000, degree=80.0, r_c=6.0, K=8,
+                   irreps_in="32x0e+32x1o+32x2e", lmax=2, irreps_out="32x0e+32x1o+32x2e",
+                   passes=("fwd", "bwd", "dbwd")),
+}
+
+
+def cube_distance_cdf(s):
+    """P(|p - q| < s) for p, q uniform in the unit cube, valid for s <= 1."""
+    return (4 * np.pi / 3) * s ** 3 - (3 * np.pi / 2) * s ** 4 + (8 / 5) * s ** 5 - s ** 6 / 6
+
+
+def cube_side(N, degree, r_c):
+    """Side L with (N - 1) F(r_c / L) = degree, by bisection."""
+    lo, hi = r_c, r_c * 1e4
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if (N - 1) * cube_distance_cdf(r_c / mid) > degree:
+            lo = mid
+        else:
+            hi = mid
+    return 0.5 * (lo + hi)
+
+
+def bessel_basis(d, K, r_c, p=6):
+    """phi[e, n] = sqrt(2/r_c) sin(n pi d / r_c) / d * u(d / r_c), n = 1..K."""
+    d = np.asarray(d, dtype=np.float64)
+    t = d / r_c
+    u = 1 - (p + 1) * (p + 2) / 2 * t ** p + p * (p + 2) * t ** (p + 1) - p * (p + 1) / 2 * t ** (p + 2)
+    u = np.where(t < 1.0, u, 0.0)
+    n = np.arange(1, K + 1, dtype=np.float64)
+    return np.sqrt(2.0 / r_c) * np.sin(n[None, :] * np.pi * d[:, None] / r_c) / d[:, None] * u[:, None]
+
+
+@dataclass
+class Graph:
+    N: int
+    rowptr: np.ndarray   # int32 [N+1]
+    sender: np.ndarray   # int32 [E]
+    evec: np.ndarray     # float32 [E, 3]
+    phi: np.ndarray      # float32 [E, K]
+
+    @property
+    def E(self):
+        return int(self.sender.shape[0])
+
+
+def _csr(N, recv, send, evec):
+    order = np.lexsort((np.arange(len(recv)), send, recv))
+    recv, send, evec = recv[order], send[order], evec[order]
+    rowptr = np.zeros(N + 1, dtype=np.int64)
+    np.add.at(rowptr, recv + 1, 1)
+    rowptr = np.cumsum(rowptr)
+    return rowptr.astype(np.int32), send.astype(np.int32), evec
+
+
+def random_graph(N, E, seed, len_lo=0.5, len_hi=5.0, K=8, r_c=5.0):
+    """Receiver uniform, sender uniform over the other nodes, random edge vectors."""
+    ss = np.random.SeedSequence(seed).spawn(6)
+    rg, rd = np.random.default_rng(ss[0]), np.random.default_rng(ss[1])
+    recv = rg.integers(0, N, size=E)
+    send = (recv + 1 + rg.integers(0, max(N - 1, 1), size=E)) % N if N > 1 else recv.copy()
+    dirs = rd.normal(size=(E, 3))
+    dirs /= np.linalg.norm(dirs, axis=1, keepdims=True)
+    lens = rd.uniform(len_lo, len_hi, size=E)
+    evec = dirs * lens[:, None]
+    rowptr, send, evec = _csr(N, recv, send, evec)
+    d = np.linalg.norm(evec, axis=1)
+    return Graph(N, rowptr, send, evec.astype(np.float32), bessel_basis(d, K, r_c).astype(np.float32))
+
+
+def cube_graph(N, degree, r_c, seed, K):
+    """All ordered pairs within r_c of N uniform points in a cube sized for `degree`."""
+    from scipy.spatial import cKDTree
+
+    ss = np.random.SeedSequence(seed).spawn(6)
+    L = cube_side(N, degree, r_c)
+    pos = np.random.default_rng(ss[0]).uniform(0.0, L, size=(N, 3))
+    pairs = cKDTree(pos).query_pairs(r_c, output_type="ndarray").astype(np.int64)
+    recv = np.concatenate([pairs[:, 0], pairs[:, 1]])
+    send = np.concatenate([pairs[:, 1], pairs[:, 0]])
+    evec = pos[send] - pos[recv]
+    rowptr, send, evec = _csr(N, recv, send, evec)
+    d = np.linalg.norm(evec, axis=1)
+    return Graph(N, rowptr, send, evec.astype(np.float32), bessel_basis(d, K, r_c).astype(np.float32))
+
+
+def config_graph(name):
+    c = CONFIGS[name]
+    if c["kind"] == "tiny":
+        return random_graph(c["N"], c["E"], c["index"], K=c["K"], r_c=c["r_c"])
+    return cube_graph(c["N"], c["degree"], c["r_c"], c["index"], c["K"])
+
+
+def node_features(N, dim, seed, stream=2):
+    rng = np.random.default_rng(np.random.SeedSequence(seed).spawn(6)[stream])
+    return rng.normal(size=(N, dim)).astype(np.float32)
+
+
+def weights(K, col_std, seed):
+    """W[K, N_w] ~ N(0, col_std[col]^2)."""
+    col_std = np.asarray(col_std, dtype=np.float64)
+    rng = np.random.default_rng(np.random.SeedSequence(seed).spawn(6)[3])
+    return (rng.normal(size=(K, col_std.shape[0])) * col_std[None, :]).astype(np.float32)
+
+
+def out_cotangent(N, dim, seed):
+    return node_features(N, dim, seed, stream=4)
+
+
+def cotangents(N, E, K, dim_in, n_w, seed, which=("x", "evec", "phi", "W")):
+    """N(0,1) cotangents for the backward outputs (x_bar, evec_bar, phi_bar, A_bar)."""
+    rng = np.random.default_rng(np.random.SeedSequence(seed).spawn(6)[5])
+    out = {}
+    shapes = dict(x=(N, dim_in), evec=(E, 3), phi=(E, K), W=(K, n_w))
+    for k in ("x", "evec", "phi", "W"):
+        a = rng.normal(size=shapes[k]).astype(np.float32)
+        out[k] = a if k in which else None
+    return out
+
+
+def round_bf16(a):
+    """Round float32 values to the nearest bfloat16 (ties to even), kept as float32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    b = a.view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return (b.astype(np.uint32) << 16).view(np.float32)
