@@ -1,0 +1,175 @@
+/*
+ * sobek.h -- C ABI of libsobek_hip: the edge-conditioned Clebsch-Gordan
+ * tensor-product convolution with fully connected (uvw) multiplicity mixing,
+ * forward, backward and double backward, on AMD Instinct MI355X (gfx950).
+ *
+ * Operator (arXiv 2607.18074, Section 2.4, eqs. standard_tpconv_background
+ * and radial_projection_background): for every receiver i of a directed graph,
+ *
+ *   m_i = sum_{e = (j -> i)} sum_{paths pi} sum_{u, w}
+ *           ( sum_q phi[e, q] W[q, off_pi + u C_out + w] )
+ *           * sum_{m_i, m_y} c^pi[m_i, m_y, m_o] x_j[u, m_i] Y_e[m_y]
+ *
+ * where Y_e are real spherical harmonics of the edge vector evec[e]
+ * (component normalised, m = -l..l, Y_1 = sqrt3 (y, z, x)) and c^pi is the
+ * real-basis Clebsch-Gordan tensor of the path (Section 4.2, eq.
+ * angular_path_contraction) times the path normalisation.  The library
+ * evaluates it in the receiver-factorised streaming order of Sections 4.2-4.4
+ * (eqs. receiver_state, receiver_matrix_product, receiver_adjoint,
+ * receiver_double_adjoint): per-edge weights W_e = phi_e A, per-edge messages
+ * and per-edge weight adjoints are never written to device memory.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Status: every function returns 0 (SOBEK_OK) or a negative sobek_status.
+ *   sobek_last_error() returns a message for the last failure on the calling
+ *   thread; the pointer stays valid until the next sobek_* call on that thread.
+ * Memory: every device pointer is caller-owned.  conv_* calls never allocate
+ *   device memory; their scratch is the caller's workspace (ws, ws_bytes).
+ *   Plans own small device tables allocated in sobek_plan_create.
+ * Streams: conv_* calls enqueue work on the given stream and return without
+ *   synchronising.  They overwrite their outputs (no accumulation).
+ * Determinism: for identical inputs, plan, graph and workspace size the
+ *   results are bitwise identical (fixed reduction orders, no float atomics).
+ * Validation: shapes, null pointers, alignment and workspace size are checked
+ *   on the host.  Graph contents are validated by sobek_graph_prepare.
+ *   Zero-length edge vectors are a precondition violation (undefined result).
+ * Layouts (row-major, fp32):
+ *   x, gx      [N][dim_in]   irrep blocks in descriptor order; within a block
+ *              of multiplicity C and order l, element (u, m) sits at
+ *              off + m*C + u  (SOBEK_LAYOUT_IR_MUL) or off + u*(2l+1) + m
+ *              (SOBEK_LAYOUT_MUL_IR).
+ *   out, gout  [N][dim_out]  same convention with the output irreps.
+ *   evec       [E][3]        r_sender - r_receiver, receiver-sorted edge order.
+ *   phi        [E][K]        radial / invariant edge features, same order.
+ *   W          [K][n_weights] path-major in path order, then u, then w.
+ */
+#ifndef SOBEK_H_
+#define SOBEK_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sobek_status {
+  SOBEK_OK = 0,
+  SOBEK_E_INVALID = -1,     /* bad argument value or descriptor */
+  SOBEK_E_UNSUPPORTED = -2, /* valid request the library does not implement (e.g. l > 3) */
+  SOBEK_E_SHAPE = -3,       /* sizes inconsistent with the plan or graph */
+  SOBEK_E_ALIGN = -4,       /* a pointer is not 16-byte aligned */
+  SOBEK_E_WORKSPACE = -5,   /* workspace missing or smaller than the minimum */
+  SOBEK_E_HIP = -6,         /* a HIP runtime call failed (message has the HIP error) */
+  SOBEK_E_INTERNAL = -7,    /* internal invariant violated */
+  SOBEK_E_COMPILE = -8      /* kernel generation or hipRTC compilation failed */
+} sobek_status;
+
+enum { SOBEK_LAYOUT_IR_MUL = 0, SOBEK_LAYOUT_MUL_IR = 1 };
+enum { SOBEK_DTYPE_F32 = 0 };
+enum { SOBEK_NORM_NONE = 0, SOBEK_NORM_FAN_IN = 1 };
+enum { SOBEK_PASS_FWD = 0, SOBEK_PASS_BWD = 1, SOBEK_PASS_DBWD = 2 };
+
+/* One irreducible representation: multiplicity, order l >= 0, parity +1 ('e') or -1 ('o'). */
+typedef struct sobek_irrep {
+  int32_t mul, l, parity;
+} sobek_irrep;
+
+typedef struct sobek_plan_s *sobek_plan;   /* opaque; owns device tables and compiled kernels */
+typedef struct sobek_graph_s *sobek_graph; /* opaque; host metadata + views into a caller buffer */
+
+const char *sobek_last_error(void);
+int sobek_version(void);
+
+/* Plan: paths, tables and kernels for one operator signature.
+ *   in[n_in], out[n_out]: input and output irreps (mul >= 1, 0 <= l <= 3).
+ *   lmax: spherical harmonics 1x0e + 1x1o + ... up to lmax (<= 3), parity (-1)^l.
+ *   K: radial width (1..64).  layout: SOBEK_LAYOUT_*.  dtype: SOBEK_DTYPE_F32.
+ *   path_norm: SOBEK_NORM_NONE (alpha = 1) or SOBEK_NORM_FAN_IN
+ *   (alpha = 1/sqrt(sum of C_in over the paths into the same output irrep)).
+ * Paths are every (input, SH, output) triple allowed by the selection rules
+ * of Section 2.2 (eq. cg_selection_rules), in lexicographic index order; each
+ * owns C_in*C_out weights (eq. num_weights).  Kernels are generated for the
+ * signature and compiled with hipRTC for gfx950 (cached on disk).  The plan
+ * must be destroyed with sobek_plan_destroy. */
+int sobek_plan_create(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out,
+                      int K, int layout, int dtype, int path_norm, sobek_plan *plan);
+int sobek_plan_destroy(sobek_plan plan);
+/* Generate and compile (hipRTC, gfx950) the kernels of a signature into the
+ * on-disk code-object cache without touching a GPU; arguments as in
+ * sobek_plan_create.  Lets a build step prepare kernels ahead of a GPU run. */
+int sobek_jit_compile(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out, int K,
+                      int layout, int dtype, int path_norm);
+/* Full HIP source generated for a signature (prelude + plan code), NUL-terminated
+ * into buf when buf_bytes allows; *needed gets the size including the NUL. */
+int sobek_plan_source(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out, int K,
+                      int layout, int dtype, int path_norm, char *buf, size_t buf_bytes, size_t *needed);
+/* Sizes of the plan; any output pointer may be NULL. */
+int sobek_plan_info(sobek_plan plan, int64_t *n_paths, int64_t *n_weights, int64_t *dim_in,
+                    int64_t *dim_out, int64_t *dim_sh);
+/* Path table (host arrays of n_paths entries; any may be NULL). */
+int sobek_plan_paths(sobek_plan plan, int32_t *i_in, int32_t *i_sh, int32_t *i_out, int64_t *w_offset);
+/* Dense copy of c^pi for path `path` into the host array
+ * coeff[(2l_in+1)*(2l_sh+1)*(2l_out+1)], index (m_i, m_y, m_o) row-major. */
+int sobek_plan_cg(sobek_plan plan, int path, double *coeff);
+/* Generator's real coupling tensor Q for (l1, l2, l3) (no path normalisation) into the host array
+ * coeff[(2l1+1)*(2l2+1)*(2l3+1)], index (a, b, c) row-major.  Needs no GPU. */
+int sobek_cg_table(int l1, int l2, int l3, double *coeff);
+/* Spherical-harmonic table of the generator: Y_lm(u) = sum_t coeff[t] ux^p[t][0] uy^p[t][1] uz^p[t][2]
+ * on the unit sphere.  Writes at most max_terms terms; *n_terms gets the count. */
+int sobek_sh_table(int l, int m, int32_t *n_terms, double *coeff, int32_t *powers, int max_terms);
+
+/* Graph preparation (outside any timed region).  Inputs are the
+ * receiver-sorted CSR on the device: recv_rowptr[N+1] (int32, non-decreasing,
+ * recv_rowptr[0] = 0, recv_rowptr[N] = E) and sender[E] (int32 in [0, N)).
+ * The call validates them, builds the stable sender-sorted view (Section 4.3:
+ * one fixed reduction order per source row) into the caller's device buffer
+ * buf (at least sobek_graph_prepare_size bytes, 16-byte aligned) and keeps a
+ * host copy of recv_rowptr.  It synchronises the stream.  The CSR arrays and
+ * buf must outlive the graph handle. */
+int sobek_graph_prepare_size(int64_t N, int64_t E, size_t *bytes);
+int sobek_graph_prepare(const int32_t *recv_rowptr, const int32_t *sender, int64_t N, int64_t E,
+                        void *buf, size_t bytes, sobek_graph *graph, hipStream_t stream);
+int sobek_graph_destroy(sobek_graph graph);
+/* Number of nodes and edges of a prepared graph (either pointer may be NULL). */
+int sobek_graph_info(sobek_graph graph, int64_t *N, int64_t *E);
+
+/* Workspace for one pass: the smallest size that allows receiver chunks of at
+ * least one receiver, grown up to `budget` bytes (budget 0 = the default of
+ * 1 GiB).  The bytes never scale with E * n_weights or E * dim_out: receiver
+ * state is bounded by the chunk size, per-edge x-gradient contributions by the
+ * chunk's edges.  conv_* derive their chunking from ws_bytes. */
+int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t budget, size_t *bytes);
+
+/* Forward (Section 4.2): out[N][dim_out] = conv(x, evec, phi, W). */
+int sobek_conv_fwd(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                   const float *phi, const float *W, float *out, void *ws, size_t ws_bytes,
+                   hipStream_t stream);
+
+/* Backward (Sections 3.2 and 4.3): gradients of <gout, conv(...)> with respect
+ * to x [N][dim_in], evec [E][3], phi [E][K] and W [K][n_weights].  Any output
+ * may be NULL when not needed. */
+int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                   const float *phi, const float *W, const float *gout, float *gx, float *gevec,
+                   float *gphi, float *gW, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Double backward (Sections 3.3 and 4.4): vector-Jacobian product of the
+ * backward map (gout, x, evec, phi, W) -> (gx, gevec, gphi, gW) with
+ * cotangents t_gx [N][dim_in], t_gevec [E][3], t_gphi [E][K], t_gW [K][n_weights]
+ * (NULL = zero).  Outputs: g_gout [N][dim_out] (the tangent output),
+ * g_x, g_evec, g_phi, g_W; any may be NULL.  g_evec includes the
+ * spherical-harmonic Hessian term sum_m Ybar_m Hess(Y_m) t_gevec. */
+int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                    const float *phi, const float *W, const float *gout, const float *t_gx,
+                    const float *t_gevec, const float *t_gphi, const float *t_gW, float *g_gout,
+                    float *g_x, float *g_evec, float *g_phi, float *g_W, void *ws, size_t ws_bytes,
+                    hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOBEK_H_ */

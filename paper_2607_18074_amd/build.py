@@ -1,0 +1,63 @@
+"""Build libsobek_hip.so in-tree.
+
+1. Embed csrc/device/prelude.hip (hand-written device code) into the library as
+   a string; the library prepends it to every generated plan and compiles the
+   result with hipRTC for gfx950.
+2. Compile the host runtime (C ABI, plan builder, kernel generator, hipRTC
+   driver) into paper_2607_18074_amd/libsobek_hip.so.
+3. Optionally pre-compile the kernels of the given operator signatures into the
+   on-disk code-object cache (paper_2607_18074_amd/_jitcache/), so a GPU process
+   loads them instead of compiling.  This needs no GPU.
+"""
+
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+LIB = os.path.join(HERE, "libsobek_hip.so")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+SOURCES = ["api.cpp", "plan.cpp", "tables.cpp", "jit.cpp"]
+
+
+def embed_prelude():
+    src = os.path.join(CSRC, "device", "prelude.hip")
+    with open(src) as f:
+        text = f.read()
+    delim = "SOBEKPRELUDE"
+    assert f"){delim}\"" not in text
+    out = os.path.join(CSRC, "prelude_embed.inc")
+    content = f'R"{delim}(\n{text}\n){delim}"\n'
+    if not os.path.exists(out) or open(out).read() != content:
+        with open(out, "w") as f:
+            f.write(content)
+
+
+def build_library(verbose=False):
+    embed_prelude()
+    cmd = ["g++", "-O2", "-g", "-std=c++17", "-fPIC", "-shared", "-D__HIP_PLATFORM_AMD__",
+           f"-I{ROCM}/include", f"-I{os.path.join(ROOT, 'include')}", "-Wall", "-Wno-unused-function",
+           *[os.path.join(CSRC, s) for s in SOURCES],
+           f"-L{ROCM}/lib", "-lamdhip64", "-lhiprtc", f"-Wl,-rpath,{ROCM}/lib", "-o", LIB + ".tmp"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+def prewarm(signatures):
+    """JIT-compile kernels for (irreps_in, lmax, irreps_out, K[, layout, norm]) signatures."""
+    sys.path.insert(0, ROOT)
+    from paper_2607_18074_amd import _lib
+    for sig in signatures:
+        _lib.jit_compile(*sig)
+
+
+if __name__ == "__main__":
+    build_library(verbose=True)
+    print("built", LIB)

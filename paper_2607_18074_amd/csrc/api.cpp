@@ -1,0 +1,734 @@
+// C ABI of libsobek_hip and the host runtime that sequences the generated
+// kernels over bounded receiver chunks (Section 4, Appendix B.2).
+//
+// Receiver-factorised program per chunk of receivers [r0, r0 + n):
+//   forward  (Section 4.2):  S = sum_e phi_e (x) C(x_j, Y_e)   [sobek_fwd_S]
+//                            m_g = S_g A_g                      [sobek_gemm_sa, per output group]
+//   backward (Section 4.3):  Sbar_g = mbar_g A_g^T              [sobek_gemm_sbar]
+//                            A_bar_g += S_g^T mbar_g            [sobek_gemm_ga + sobek_ga_reduce]
+//                            phi_bar, evec_bar, per-edge x contributions   [sobek_bwd_E]
+//                            x_bar via the sender-sorted view   [sobek_sender_reduce]
+//   double backward (Section 4.4, eq. receiver_double_adjoint with d mbar = 0):
+//                            dS (directional state)             [sobek_fwd_dS]
+//                            m_dot = dS A + S dA                [sobek_gemm_sa x2]
+//                            Sbar = mbar A^T, Sbar' = mbar dA^T [sobek_gemm_sbar x2]
+//                            g_A = dS^T mbar                    [sobek_gemm_ga]
+//                            edge-local second adjoints         [sobek_dbwd_E]
+//                            g_x via the sender-sorted view     [sobek_sender_reduce]
+// Every reduction has a fixed order (CSR order, split order, chunk order), so
+// results are bitwise reproducible for a given workspace size.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <memory>
+#include <stdexcept>
+#include <string>
+#include <vector>
+
+#include "../../include/sobek.h"
+#include "jit.h"
+#include "plan.h"
+#include "tables.h"
+
+using sobek::Plan;
+
+struct sobek_plan_s {
+  Plan p;
+};
+
+struct sobek_graph_s {
+  int64_t N = 0, E = 0;
+  const int32_t* rowptr = nullptr;
+  const int32_t* sender = nullptr;
+  int32_t* send_rowptr = nullptr;
+  int32_t* send_perm = nullptr;
+  std::vector<int32_t> h_rowptr;
+  int64_t max_deg = 0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[2048];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIPCHK(call)                                                                          \
+  do {                                                                                        \
+    hipError_t e_ = (call);                                                                   \
+    if (e_ != hipSuccess) return fail(SOBEK_E_HIP, "%s: %s", #call, hipGetErrorString(e_));  \
+  } while (0)
+
+template <typename... Args>
+hipError_t launch(hipFunction_t f, unsigned gx, unsigned gy, unsigned gz, hipStream_t s, Args... args) {
+  if (gx == 0 || gy == 0 || gz == 0) return hipSuccess;
+  void* ptrs[] = {(void*)&args...};
+  return hipModuleLaunchKernel(f, gx, gy, gz, 256, 1, 1, 0, s, ptrs, nullptr);
+}
+
+#define LAUNCH(...) HIPCHK(launch(__VA_ARGS__))
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+int validate_irreps(const sobek_irrep* v, int n, std::vector<sobek::Irrep>& out, const char* what) {
+  if (n <= 0 || !v) return fail(SOBEK_E_INVALID, "%s irreps: empty or NULL", what);
+  for (int i = 0; i < n; ++i) {
+    if (v[i].mul < 1) return fail(SOBEK_E_INVALID, "%s irrep %d: multiplicity %d < 1", what, i, v[i].mul);
+    if (v[i].l < 0) return fail(SOBEK_E_INVALID, "%s irrep %d: negative order", what, i);
+    if (v[i].l > 3) return fail(SOBEK_E_UNSUPPORTED, "%s irrep %d: order %d > 3 not supported", what, i, v[i].l);
+    if (v[i].parity != 1 && v[i].parity != -1)
+      return fail(SOBEK_E_INVALID, "%s irrep %d: parity must be +1 or -1", what, i);
+    out.push_back({v[i].mul, v[i].l, v[i].parity, 0});
+  }
+  return SOBEK_OK;
+}
+
+int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
+                    int dtype, int norm, Plan& p) {
+  int rc;
+  if ((rc = validate_irreps(in, n_in, p.in, "input")) != SOBEK_OK) return rc;
+  if ((rc = validate_irreps(out, n_out, p.out, "output")) != SOBEK_OK) return rc;
+  if (lmax < 0) return fail(SOBEK_E_INVALID, "lmax < 0");
+  if (lmax > 3) return fail(SOBEK_E_UNSUPPORTED, "lmax %d > 3 not supported", lmax);
+  if (K < 1 || K > 64) return fail(SOBEK_E_INVALID, "K = %d outside [1, 64]", K);
+  if (layout != SOBEK_LAYOUT_IR_MUL && layout != SOBEK_LAYOUT_MUL_IR) return fail(SOBEK_E_INVALID, "bad layout");
+  if (dtype != SOBEK_DTYPE_F32) return fail(SOBEK_E_UNSUPPORTED, "only SOBEK_DTYPE_F32 is implemented");
+  if (norm != SOBEK_NORM_NONE && norm != SOBEK_NORM_FAN_IN) return fail(SOBEK_E_INVALID, "bad path normalisation");
+  p.lmax = lmax; p.K = K; p.layout = layout; p.dtype = dtype; p.norm = norm;
+  try {
+    sobek::build_plan(p);
+  } catch (const std::exception& ex) {
+    return fail(SOBEK_E_UNSUPPORTED, "plan: %s", ex.what());
+  }
+  if (p.paths.empty()) return fail(SOBEK_E_INVALID, "no path satisfies the selection rules");
+  int64_t maxD = 0;
+  for (auto& g : p.groups) maxD = std::max(maxD, g.D);
+  if (p.n_w * (int64_t)K >= (1ll << 31) || maxD >= (1ll << 31))
+    return fail(SOBEK_E_UNSUPPORTED, "weight tensor too large for 32-bit indexing");
+  p.source = sobek::generate_source(p);
+  return SOBEK_OK;
+}
+
+// ----------------------------------------------------------------------------
+// workspace planning
+// ----------------------------------------------------------------------------
+struct Chunk {
+  int r0, n;
+  int64_t e0, e1;
+};
+
+struct WsPlan {
+  // byte offsets
+  size_t off_x = 0, off_gout = 0, off_tgx = 0, off_out = 0, off_gx = 0, off_P = 0, off_state = 0, off_contrib = 0;
+  size_t fixed = 0;
+  int nstate = 0;
+  int64_t ncap = 0, ecap = 0;
+  size_t total = 0;
+  std::vector<Chunk> chunks;
+};
+
+int gemm_bn(int C) { return C <= 16 ? 16 : (C <= 32 ? 32 : 64); }
+int bn_index(int bn) { return bn == 16 ? 0 : (bn == 32 ? 1 : 2); }
+
+int nsplit_for(const sobek::Group& g, int64_t nrows) {
+  int bn = gemm_bn(g.C);
+  int64_t tiles = (int64_t)cdiv(g.D, 64) * cdiv(g.C, bn);
+  int64_t ns = (512 + tiles - 1) / tiles;
+  ns = std::max<int64_t>(1, std::min<int64_t>(ns, 64));
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, nrows / 64));
+  return (int)ns;
+}
+
+size_t partial_floats(const Plan& p, int64_t ncap) {
+  size_t m = 0;
+  for (auto& g : p.groups) m = std::max(m, (size_t)nsplit_for(g, ncap * g.d) * g.D * g.C);
+  return m;
+}
+
+// fixed part + per-receiver + per-edge bytes of a pass
+void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, WsPlan& w, size_t& per_recv, size_t& per_edge) {
+  const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes); return at; };
+  const size_t nx = (size_t)G.N * p.dim_in * 4, no = (size_t)G.N * p.dim_out * 4;
+  if (mulir) {
+    w.off_x = take(nx);
+    w.off_out = take(no);
+    if (pass >= SOBEK_PASS_BWD) { w.off_gout = take(no); w.off_gx = take(nx); }
+    if (pass == SOBEK_PASS_DBWD) w.off_tgx = take(nx);
+  }
+  w.off_P = o;  // partials, sized once the chunk capacity is known
+  w.fixed = o;
+  w.nstate = pass == SOBEK_PASS_FWD ? 1 : (pass == SOBEK_PASS_BWD ? 2 : 4);
+  per_recv = (size_t)w.nstate * p.srow * 4;
+  per_edge = pass == SOBEK_PASS_FWD ? 0 : (size_t)p.dim_in * 4;
+}
+
+size_t layout_total(const Plan& p, WsPlan& w, int pass) {
+  size_t o = w.fixed;
+  if (pass != SOBEK_PASS_FWD) o = align_up(o + partial_floats(p, w.ncap) * 4);
+  w.off_state = o;
+  o = align_up(o + (size_t)w.nstate * w.ncap * p.srow * 4);
+  w.off_contrib = o;
+  if (pass != SOBEK_PASS_FWD) o = align_up(o + (size_t)w.ecap * p.dim_in * 4);
+  return o;
+}
+
+int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_bytes, WsPlan& w, bool sizing_only) {
+  size_t per_recv, per_edge;
+  pass_costs(p, G, pass, w, per_recv, per_edge);
+  const int64_t N = G.N, E = G.E;
+  // try a single chunk, else split the remaining bytes between state and contributions
+  w.ncap = std::max<int64_t>(1, N);
+  w.ecap = std::max<int64_t>(G.max_deg, E);
+  size_t need = layout_total(p, w, pass);
+  if (need > ws_bytes) {
+    size_t partial_max = align_up(partial_floats(p, std::max<int64_t>(1, N)) * 4) + 2 * kAlign;
+    if (ws_bytes <= w.fixed + partial_max) {
+      w.ncap = 1;
+      w.ecap = std::max<int64_t>(1, G.max_deg);
+    } else {
+      size_t rem = ws_bytes - w.fixed - partial_max - 2 * kAlign;
+      double wr = (double)N * per_recv, we = (double)E * per_edge;
+      double frac = (wr + we) > 0 ? wr / (wr + we) : 1.0;
+      w.ncap = std::max<int64_t>(1, (int64_t)(rem * frac / std::max<size_t>(per_recv, 1)));
+      w.ncap = std::min<int64_t>(w.ncap, std::max<int64_t>(1, N));
+      if (per_edge) {
+        w.ecap = (int64_t)((rem - std::min(rem, (size_t)w.ncap * per_recv)) / per_edge);
+        if (w.ecap < G.max_deg) {
+          w.ecap = std::max<int64_t>(1, G.max_deg);
+          size_t left = rem > (size_t)w.ecap * per_edge ? rem - (size_t)w.ecap * per_edge : 0;
+          w.ncap = std::max<int64_t>(1, std::min<int64_t>(w.ncap, (int64_t)(left / std::max<size_t>(per_recv, 1))));
+        }
+      } else {
+        w.ecap = std::max<int64_t>(1, G.max_deg);
+      }
+    }
+    need = layout_total(p, w, pass);
+  }
+  w.total = need;
+  if (sizing_only) return SOBEK_OK;
+  if (need > ws_bytes)
+    return fail(SOBEK_E_WORKSPACE, "workspace of %zu bytes is below the minimum %zu for this pass", ws_bytes, need);
+  // greedy receiver chunks under both capacities
+  w.chunks.clear();
+  int64_t r = 0;
+  while (r < N) {
+    int64_t n = 0, e0 = G.h_rowptr[r];
+    while (r + n < N && n < w.ncap) {
+      int64_t e_next = G.h_rowptr[r + n + 1];
+      if (per_edge && n > 0 && e_next - e0 > w.ecap) break;
+      ++n;
+    }
+    w.chunks.push_back({(int)r, (int)n, e0, (int64_t)G.h_rowptr[r + n]});
+    r += n;
+  }
+  return SOBEK_OK;
+}
+
+size_t default_budget() { return (size_t)1 << 30; }
+
+struct Ctx {
+  const Plan& p;
+  const sobek_graph_s& G;
+  hipStream_t s;
+};
+
+int fill_zero(const Plan& p, float* buf, int64_t n, hipStream_t s) {
+  if (!buf || n <= 0) return SOBEK_OK;
+  long long nn = n;
+  LAUNCH(p.k.zero, cdiv(n, 256), 1, 1, s, buf, nn);
+  return SOBEK_OK;
+}
+
+int transpose(const Plan& p, const float* src, float* dst, int64_t N, bool input_side, int dir, hipStream_t s) {
+  const int CX = input_side ? p.dim_in : p.dim_out;
+  const int nb = input_side ? (int)p.in.size() : (int)p.out.size();
+  const int32_t* base = input_side ? p.d_in_blocks : p.d_out_blocks;
+  int n = (int)N;
+  LAUNCH(p.k.transpose, cdiv(N * CX, 256), 1, 1, s, src, dst, n, CX, (const int*)base, (const int*)(base + nb),
+         (const int*)(base + 2 * nb), nb, dir);
+  return SOBEK_OK;
+}
+
+int zero_dead_out(const Plan& p, float* out, int64_t N, hipStream_t s) {
+  for (int c : p.dead_out) {
+    int n = (int)N, CX = p.dim_out, off = p.out[c].off, width = p.out[c].dim();
+    LAUNCH(p.k.fill_cols, cdiv(N * width, 256), 1, 1, s, out, n, CX, off, width);
+  }
+  return SOBEK_OK;
+}
+
+float* state_ptr(const WsPlan& w, void* ws, const Plan& p, int which) {
+  return (float*)((char*)ws + w.off_state) + (size_t)which * w.ncap * p.srow;
+}
+
+// S (or dS) for the chunk
+int run_state(const Plan& p, const sobek_graph_s& G, const Chunk& c, const WsPlan& w, float* S, bool tangent,
+              const float* x, const float* evec, const float* phi, const float* xdot, const float* evdot,
+              const float* phidot, int flags, hipStream_t s) {
+  const int NU = (int)p.fwd_units.size();
+  long long ncap = w.ncap;
+  int r0 = c.r0, n = c.n;
+  LAUNCH(tangent ? p.k.fwd_dS : p.k.fwd_S, cdiv((int64_t)n * NU, 4), 1, 1, s, (const int*)G.rowptr,
+         (const int*)G.sender, evec, phi, x, S, r0, n, ncap, xdot, evdot, phidot, flags);
+  return SOBEK_OK;
+}
+
+// out(i, m_o, w) (+)= S_g A_g for every group
+int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, const float* S, const float* W, float* out, int acc,
+            hipStream_t s) {
+  for (auto& g : p.groups) {
+    const float* Sg = S + (size_t)w.ncap * g.s_off;
+    int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
+    int bn = gemm_bn(g.C);
+    LAUNCH(p.k.gemm_sa[bn_index(bn)], cdiv(nrows, 64), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
+           (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
+  }
+  return SOBEK_OK;
+}
+
+// Sbar_g = mbar_g A_g^T for every group
+int run_sbar(const Plan& p, const Chunk& c, const WsPlan& w, const float* M, const float* W, float* Sbar,
+             hipStream_t s) {
+  for (auto& g : p.groups) {
+    float* Sg = Sbar + (size_t)w.ncap * g.s_off;
+    int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
+    LAUNCH(p.k.gemm_sbar[2], cdiv(nrows, 64), cdiv(D, 64), 1, s, M, nrows, D, W,
+           (const int*)(p.d_ktab + g.ktab_off), Sg, dg, Cg, off, CX, r0);
+  }
+  return SOBEK_OK;
+}
+
+// gW (first ? = : +=) S_g^T mbar_g, deterministic split reduction
+int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float* S, const float* M, float* gW,
+           int first, hipStream_t s) {
+  float* P = (float*)((char*)ws + w.off_P);
+  for (auto& g : p.groups) {
+    const float* Sg = S + (size_t)w.ncap * g.s_off;
+    int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
+    int ns = nsplit_for(g, (int64_t)w.ncap * g.d);
+    int rps = (int)(((int64_t)cdiv(nrows, ns) + 15) / 16 * 16);
+    int bn = gemm_bn(g.C);
+    LAUNCH(p.k.gemm_ga[bn_index(bn)], cdiv(D, 64), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0, rps);
+    LAUNCH(p.k.ga_reduce, cdiv((int64_t)D * Cg, 256), 1, 1, s, (const float*)P, ns, D, Cg,
+           (const int*)(p.d_ktab + g.ktab_off), gW, first);
+  }
+  return SOBEK_OK;
+}
+
+int run_sender_reduce(const Plan& p, const sobek_graph_s& G, const Chunk& c, const float* contrib, float* gx,
+                      int first, hipStream_t s) {
+  int N = (int)G.N, CX = p.dim_in, e0 = (int)c.e0, e1 = (int)c.e1;
+  LAUNCH(p.k.sender_reduce, cdiv(G.N, 4), 1, 1, s, (const int*)G.send_rowptr, (const int*)G.send_perm, contrib, gx,
+         N, CX, e0, e1, first);
+  return SOBEK_OK;
+}
+
+int check_common(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                 const float* W, void* ws, size_t ws_bytes) {
+  if (!plan || !graph) return fail(SOBEK_E_INVALID, "NULL plan or graph");
+  if (graph->N > 0 && !x) return fail(SOBEK_E_INVALID, "x is NULL");
+  if (graph->E > 0 && (!evec || !phi)) return fail(SOBEK_E_INVALID, "evec or phi is NULL");
+  if (!W) return fail(SOBEK_E_INVALID, "W is NULL");
+  if (!ws && ws_bytes) return fail(SOBEK_E_WORKSPACE, "workspace pointer is NULL");
+  for (const void* q : {(const void*)x, (const void*)evec, (const void*)phi, (const void*)W, (const void*)ws})
+    if (q && !aligned16(q)) return fail(SOBEK_E_ALIGN, "pointer %p is not 16-byte aligned", q);
+  if (graph->N >= (1ll << 31) || graph->E >= (1ll << 31)) return fail(SOBEK_E_UNSUPPORTED, "graph too large");
+  if (graph->N * (int64_t)std::max(plan->p.dim_in, plan->p.dim_out) >= (1ll << 31) * 64ll)
+    return fail(SOBEK_E_UNSUPPORTED, "feature tensor too large");
+  return SOBEK_OK;
+}
+
+}  // namespace
+
+// ============================================================================
+extern "C" {
+
+const char* sobek_last_error(void) { return g_err.c_str(); }
+int sobek_version(void) { return 1; }
+
+int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
+                      int dtype, int path_norm, sobek_plan* plan) {
+  if (!plan) return fail(SOBEK_E_INVALID, "plan output pointer is NULL");
+  *plan = nullptr;
+  std::unique_ptr<sobek_plan_s> h(new sobek_plan_s());
+  Plan& p = h->p;
+  int rc = build_signature(in, n_in, lmax, out, n_out, K, layout, dtype, path_norm, p);
+  if (rc != SOBEK_OK) return rc;
+  std::vector<char> code;
+  try {
+    code = sobek::jit_compile(p.source);
+  } catch (const std::exception& ex) {
+    return fail(SOBEK_E_COMPILE, "%s", ex.what());
+  }
+  HIPCHK(hipModuleLoadData(&p.k.module, code.data()));
+  auto get = [&](hipFunction_t& f, const char* name) -> int {
+    hipError_t e = hipModuleGetFunction(&f, p.k.module, name);
+    if (e != hipSuccess) return fail(SOBEK_E_INTERNAL, "kernel %s missing: %s", name, hipGetErrorString(e));
+    return SOBEK_OK;
+  };
+  const char* bns[3] = {"16", "32", "64"};
+  if ((rc = get(p.k.fwd_S, "sobek_fwd_S")) || (rc = get(p.k.fwd_dS, "sobek_fwd_dS")) ||
+      (rc = get(p.k.bwd_E, "sobek_bwd_E")) || (rc = get(p.k.dbwd_E, "sobek_dbwd_E")) ||
+      (rc = get(p.k.ga_reduce, "sobek_ga_reduce")) || (rc = get(p.k.sender_reduce, "sobek_sender_reduce")) ||
+      (rc = get(p.k.transpose, "sobek_transpose")) || (rc = get(p.k.fill_cols, "sobek_fill_cols")) ||
+      (rc = get(p.k.zero, "sobek_zero")))
+    return rc;
+  for (int b = 0; b < 3; ++b) {
+    std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
+                ga = std::string("sobek_gemm_ga_") + bns[b];
+    if ((rc = get(p.k.gemm_sa[b], sa.c_str())) || (rc = get(p.k.gemm_sbar[b], sb.c_str())) ||
+        (rc = get(p.k.gemm_ga[b], ga.c_str())))
+      return rc;
+  }
+  HIPCHK(hipMalloc(&p.d_ktab, std::max<size_t>(4, p.ktab.size() * 4)));
+  HIPCHK(hipMemcpy(p.d_ktab, p.ktab.data(), p.ktab.size() * 4, hipMemcpyHostToDevice));
+  auto blocks = [](const std::vector<sobek::Irrep>& v) {
+    std::vector<int32_t> b(3 * v.size());
+    for (size_t i = 0; i < v.size(); ++i) {
+      b[i] = v[i].off;
+      b[v.size() + i] = v[i].mul;
+      b[2 * v.size() + i] = 2 * v[i].l + 1;
+    }
+    return b;
+  };
+  auto bi = blocks(p.in), bo = blocks(p.out);
+  HIPCHK(hipMalloc(&p.d_in_blocks, bi.size() * 4));
+  HIPCHK(hipMemcpy(p.d_in_blocks, bi.data(), bi.size() * 4, hipMemcpyHostToDevice));
+  HIPCHK(hipMalloc(&p.d_out_blocks, bo.size() * 4));
+  HIPCHK(hipMemcpy(p.d_out_blocks, bo.data(), bo.size() * 4, hipMemcpyHostToDevice));
+  *plan = h.release();
+  return SOBEK_OK;
+}
+
+int sobek_jit_compile(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
+                      int dtype, int path_norm) {
+  Plan p;
+  int rc = build_signature(in, n_in, lmax, out, n_out, K, layout, dtype, path_norm, p);
+  if (rc != SOBEK_OK) return rc;
+  try {
+    sobek::jit_compile(p.source);
+  } catch (const std::exception& ex) {
+    return fail(SOBEK_E_COMPILE, "%s", ex.what());
+  }
+  return SOBEK_OK;
+}
+
+int sobek_plan_source(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
+                      int dtype, int path_norm, char* buf, size_t buf_bytes, size_t* needed) {
+  Plan p;
+  int rc = build_signature(in, n_in, lmax, out, n_out, K, layout, dtype, path_norm, p);
+  if (rc != SOBEK_OK) return rc;
+  std::string s = sobek::full_source(p.source);
+  if (needed) *needed = s.size() + 1;
+  if (buf && buf_bytes) {
+    size_t n = std::min(buf_bytes - 1, s.size());
+    std::memcpy(buf, s.data(), n);
+    buf[n] = 0;
+  }
+  return SOBEK_OK;
+}
+
+int sobek_plan_destroy(sobek_plan plan) {
+  if (!plan) return SOBEK_OK;
+  Plan& p = plan->p;
+  if (p.d_ktab) (void)hipFree(p.d_ktab);
+  if (p.d_in_blocks) (void)hipFree(p.d_in_blocks);
+  if (p.d_out_blocks) (void)hipFree(p.d_out_blocks);
+  if (p.k.module) (void)hipModuleUnload(p.k.module);
+  delete plan;
+  return SOBEK_OK;
+}
+
+int sobek_plan_info(sobek_plan plan, int64_t* n_paths, int64_t* n_weights, int64_t* dim_in, int64_t* dim_out,
+                    int64_t* dim_sh) {
+  if (!plan) return fail(SOBEK_E_INVALID, "NULL plan");
+  const Plan& p = plan->p;
+  if (n_paths) *n_paths = (int64_t)p.paths.size();
+  if (n_weights) *n_weights = p.n_w;
+  if (dim_in) *dim_in = p.dim_in;
+  if (dim_out) *dim_out = p.dim_out;
+  if (dim_sh) *dim_sh = p.nsh;
+  return SOBEK_OK;
+}
+
+int sobek_plan_paths(sobek_plan plan, int32_t* i_in, int32_t* i_sh, int32_t* i_out, int64_t* w_offset) {
+  if (!plan) return fail(SOBEK_E_INVALID, "NULL plan");
+  const Plan& p = plan->p;
+  for (size_t t = 0; t < p.paths.size(); ++t) {
+    if (i_in) i_in[t] = p.paths[t].i_in;
+    if (i_sh) i_sh[t] = p.paths[t].i_sh;
+    if (i_out) i_out[t] = p.paths[t].i_out;
+    if (w_offset) w_offset[t] = p.paths[t].w_off;
+  }
+  return SOBEK_OK;
+}
+
+int sobek_plan_cg(sobek_plan plan, int path, double* coeff) {
+  if (!plan || !coeff) return fail(SOBEK_E_INVALID, "NULL argument");
+  const Plan& p = plan->p;
+  if (path < 0 || path >= (int)p.paths.size()) return fail(SOBEK_E_INVALID, "path index out of range");
+  const auto& c = p.paths[path].cg;
+  std::copy(c.begin(), c.end(), coeff);
+  return SOBEK_OK;
+}
+
+int sobek_cg_table(int l1, int l2, int l3, double* coeff) {
+  if (!coeff) return fail(SOBEK_E_INVALID, "NULL coeff");
+  if (l1 < 0 || l2 < 0 || l3 < 0 || l1 > 8 || l2 > 8 || l3 > 8) return fail(SOBEK_E_INVALID, "bad orders");
+  if (l3 < std::abs(l1 - l2) || l3 > l1 + l2) return fail(SOBEK_E_INVALID, "triangle rule violated");
+  const auto& Q = sobek::real_cg(l1, l2, l3);
+  std::copy(Q.begin(), Q.end(), coeff);
+  return SOBEK_OK;
+}
+
+int sobek_sh_table(int l, int m, int32_t* n_terms, double* coeff, int32_t* powers, int max_terms) {
+  if (l < 0 || l > 8 || m < -l || m > l) return fail(SOBEK_E_INVALID, "bad (l, m)");
+  const auto& P = sobek::sh_poly(l, m);
+  if (n_terms) *n_terms = (int32_t)P.size();
+  for (int t = 0; t < (int)P.size() && t < max_terms; ++t) {
+    if (coeff) coeff[t] = P[t].c;
+    if (powers) {
+      powers[3 * t] = P[t].px;
+      powers[3 * t + 1] = P[t].py;
+      powers[3 * t + 2] = P[t].pz;
+    }
+  }
+  return SOBEK_OK;
+}
+
+int sobek_graph_prepare_size(int64_t N, int64_t E, size_t* bytes) {
+  if (!bytes) return fail(SOBEK_E_INVALID, "NULL bytes");
+  if (N < 0 || E < 0) return fail(SOBEK_E_INVALID, "negative size");
+  *bytes = align_up((size_t)(N + 1) * 4) + align_up((size_t)std::max<int64_t>(E, 1) * 4);
+  return SOBEK_OK;
+}
+
+int sobek_graph_prepare(const int32_t* recv_rowptr, const int32_t* sender, int64_t N, int64_t E, void* buf,
+                        size_t bytes, sobek_graph* graph, hipStream_t stream) {
+  if (!graph) return fail(SOBEK_E_INVALID, "graph output pointer is NULL");
+  *graph = nullptr;
+  if (N < 0 || E < 0) return fail(SOBEK_E_INVALID, "negative size");
+  if (N >= (1ll << 31) || E >= (1ll << 31)) return fail(SOBEK_E_UNSUPPORTED, "graph too large for int32 indices");
+  if (!recv_rowptr || (E > 0 && !sender)) return fail(SOBEK_E_INVALID, "NULL CSR array");
+  size_t need;
+  sobek_graph_prepare_size(N, E, &need);
+  if (!buf || bytes < need) return fail(SOBEK_E_WORKSPACE, "graph buffer needs %zu bytes", need);
+  if (!aligned16(buf)) return fail(SOBEK_E_ALIGN, "graph buffer is not 16-byte aligned");
+  std::unique_ptr<sobek_graph_s> g(new sobek_graph_s());
+  g->N = N; g->E = E; g->rowptr = recv_rowptr; g->sender = sender;
+  g->h_rowptr.resize(N + 1);
+  std::vector<int32_t> hs(E);
+  HIPCHK(hipMemcpyAsync(g->h_rowptr.data(), recv_rowptr, (N + 1) * 4, hipMemcpyDeviceToHost, stream));
+  if (E) HIPCHK(hipMemcpyAsync(hs.data(), sender, E * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  if (g->h_rowptr[0] != 0 || g->h_rowptr[N] != E) return fail(SOBEK_E_INVALID, "rowptr must start at 0 and end at E");
+  for (int64_t i = 0; i < N; ++i) {
+    int64_t d = (int64_t)g->h_rowptr[i + 1] - g->h_rowptr[i];
+    if (d < 0) return fail(SOBEK_E_INVALID, "rowptr decreases at %lld", (long long)i);
+    g->max_deg = std::max(g->max_deg, d);
+  }
+  // stable counting sort by sender: inside one sender, edges keep receiver order
+  std::vector<int32_t> srow(N + 1, 0), perm(E);
+  for (int64_t e = 0; e < E; ++e) {
+    if (hs[e] < 0 || hs[e] >= N) return fail(SOBEK_E_INVALID, "sender[%lld] = %d out of range", (long long)e, hs[e]);
+    srow[hs[e] + 1]++;
+  }
+  for (int64_t i = 0; i < N; ++i) srow[i + 1] += srow[i];
+  std::vector<int32_t> pos(srow.begin(), srow.end() - 1);
+  for (int64_t e = 0; e < E; ++e) perm[pos[hs[e]]++] = (int32_t)e;
+  g->send_rowptr = (int32_t*)buf;
+  g->send_perm = (int32_t*)((char*)buf + align_up((size_t)(N + 1) * 4));
+  HIPCHK(hipMemcpyAsync(g->send_rowptr, srow.data(), (N + 1) * 4, hipMemcpyHostToDevice, stream));
+  if (E) HIPCHK(hipMemcpyAsync(g->send_perm, perm.data(), E * 4, hipMemcpyHostToDevice, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  *graph = g.release();
+  return SOBEK_OK;
+}
+
+int sobek_graph_destroy(sobek_graph graph) {
+  delete graph;
+  return SOBEK_OK;
+}
+
+int sobek_graph_info(sobek_graph graph, int64_t* N, int64_t* E) {
+  if (!graph) return fail(SOBEK_E_INVALID, "NULL graph");
+  if (N) *N = graph->N;
+  if (E) *E = graph->E;
+  return SOBEK_OK;
+}
+
+int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t budget, size_t* bytes) {
+  if (!plan || !graph || !bytes) return fail(SOBEK_E_INVALID, "NULL argument");
+  if (pass < SOBEK_PASS_FWD || pass > SOBEK_PASS_DBWD) return fail(SOBEK_E_INVALID, "bad pass");
+  WsPlan w;
+  plan_workspace(plan->p, *graph, pass, budget ? budget : default_budget(), w, true);
+  *bytes = w.total;
+  return SOBEK_OK;
+}
+
+int sobek_conv_fwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                   const float* W, float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
+  if (rc) return rc;
+  if (!out && graph->N) return fail(SOBEK_E_INVALID, "out is NULL");
+  if (out && !aligned16(out)) return fail(SOBEK_E_ALIGN, "out is not 16-byte aligned");
+  const Plan& p = plan->p;
+  const sobek_graph_s& G = *graph;
+  WsPlan w;
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_FWD, ws_bytes, w, false))) return rc;
+  if (G.N == 0) return SOBEK_OK;
+  const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
+  const float* xk = x;
+  float* ok = out;
+  if (mulir) {
+    xk = (const float*)((char*)ws + w.off_x);
+    ok = (float*)((char*)ws + w.off_out);
+    if ((rc = transpose(p, x, (float*)xk, G.N, true, 0, stream))) return rc;
+  }
+  float* S = state_ptr(w, ws, p, 0);
+  for (auto& c : w.chunks) {
+    if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
+    if ((rc = run_mix(p, c, w, S, W, ok, 0, stream))) return rc;
+  }
+  if ((rc = zero_dead_out(p, ok, G.N, stream))) return rc;
+  if (mulir && (rc = transpose(p, ok, out, G.N, false, 1, stream))) return rc;
+  return SOBEK_OK;
+}
+
+int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                   const float* W, const float* gout, float* gx, float* gevec, float* gphi, float* gW, void* ws,
+                   size_t ws_bytes, hipStream_t stream) {
+  int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
+  if (rc) return rc;
+  if (!gout && graph->N) return fail(SOBEK_E_INVALID, "gout is NULL");
+  for (const void* q : {(const void*)gout, (const void*)gx, (const void*)gevec, (const void*)gphi, (const void*)gW})
+    if (q && !aligned16(q)) return fail(SOBEK_E_ALIGN, "pointer %p is not 16-byte aligned", q);
+  const Plan& p = plan->p;
+  const sobek_graph_s& G = *graph;
+  WsPlan w;
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false))) return rc;
+  if (gW) { if ((rc = fill_zero(p, gW, (int64_t)p.K * p.n_w, stream))) return rc; }
+  if (G.N == 0) return SOBEK_OK;
+  const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
+  const float* xk = x;
+  const float* gk = gout;
+  float* gxk = gx;
+  if (mulir) {
+    xk = (const float*)((char*)ws + w.off_x);
+    gk = (const float*)((char*)ws + w.off_gout);
+    if (gx) gxk = (float*)((char*)ws + w.off_gx);
+    if ((rc = transpose(p, x, (float*)xk, G.N, true, 0, stream))) return rc;
+    if ((rc = transpose(p, gout, (float*)gk, G.N, false, 0, stream))) return rc;
+  }
+  float* S = state_ptr(w, ws, p, 0);
+  float* Sb = state_ptr(w, ws, p, 1);
+  float* contrib = gx ? (float*)((char*)ws + w.off_contrib) : nullptr;
+  const bool edge = gx || gevec || gphi;
+  for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
+    const Chunk& c = w.chunks[ci];
+    if (gW) {
+      if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
+      if ((rc = run_ga(p, c, w, ws, S, gk, gW, 0, stream))) return rc;
+    }
+    if (edge) {
+      if ((rc = run_sbar(p, c, w, gk, W, Sb, stream))) return rc;
+      int r0 = c.r0, n = c.n, e0 = (int)c.e0, flags = 0;
+      long long ncap = w.ncap;
+      LAUNCH(p.k.bwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
+             (const float*)Sb, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
+             (const float*)nullptr, gphi, gevec, contrib, r0, n, ncap, e0, flags);
+      if (gx && (rc = run_sender_reduce(p, G, c, contrib, gxk, ci == 0, stream))) return rc;
+    }
+  }
+  if (mulir && gx && (rc = transpose(p, gxk, gx, G.N, true, 1, stream))) return rc;
+  return SOBEK_OK;
+}
+
+int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                    const float* W, const float* gout, const float* t_gx, const float* t_gevec, const float* t_gphi,
+                    const float* t_gW, float* g_gout, float* g_x, float* g_evec, float* g_phi, float* g_W, void* ws,
+                    size_t ws_bytes, hipStream_t stream) {
+  int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
+  if (rc) return rc;
+  if (!gout && graph->N) return fail(SOBEK_E_INVALID, "gout is NULL");
+  for (const void* q : {(const void*)gout, (const void*)t_gx, (const void*)t_gevec, (const void*)t_gphi,
+                        (const void*)t_gW, (const void*)g_gout, (const void*)g_x, (const void*)g_evec,
+                        (const void*)g_phi, (const void*)g_W})
+    if (q && !aligned16(q)) return fail(SOBEK_E_ALIGN, "pointer %p is not 16-byte aligned", q);
+  const Plan& p = plan->p;
+  const sobek_graph_s& G = *graph;
+  WsPlan w;
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_DBWD, ws_bytes, w, false))) return rc;
+  const int flags = (t_gphi ? 1 : 0) | (t_gx ? 2 : 0) | (t_gevec ? 4 : 0) | (t_gW ? 8 : 0);
+  const bool tan = flags & 7;
+  if (g_W) { if ((rc = fill_zero(p, g_W, (int64_t)p.K * p.n_w, stream))) return rc; }
+  if (G.N == 0) return SOBEK_OK;
+  const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
+  const float *xk = x, *gk = gout, *txk = t_gx;
+  float *ggk = g_gout, *gxk = g_x;
+  if (mulir) {
+    xk = (const float*)((char*)ws + w.off_x);
+    gk = (const float*)((char*)ws + w.off_gout);
+    if ((rc = transpose(p, x, (float*)xk, G.N, true, 0, stream))) return rc;
+    if ((rc = transpose(p, gout, (float*)gk, G.N, false, 0, stream))) return rc;
+    if (t_gx) {
+      txk = (const float*)((char*)ws + w.off_tgx);
+      if ((rc = transpose(p, t_gx, (float*)txk, G.N, true, 0, stream))) return rc;
+    }
+    if (g_gout) ggk = (float*)((char*)ws + w.off_out);
+    if (g_x) gxk = (float*)((char*)ws + w.off_gx);
+  }
+  if (g_gout && !tan && !t_gW) { if ((rc = fill_zero(p, ggk, G.N * p.dim_out, stream))) return rc; }
+  float* dS = state_ptr(w, ws, p, 0);
+  float* S = state_ptr(w, ws, p, 1);
+  float* Sb = state_ptr(w, ws, p, 2);
+  float* Sb2 = state_ptr(w, ws, p, 3);
+  float* contrib = g_x ? (float*)((char*)ws + w.off_contrib) : nullptr;
+  const bool edge = g_x || g_evec || g_phi;
+  for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
+    const Chunk& c = w.chunks[ci];
+    if (tan && (g_gout || g_W))
+      if ((rc = run_state(p, G, c, w, dS, true, xk, evec, phi, txk, t_gevec, t_gphi, flags & 7, stream))) return rc;
+    if (t_gW && g_gout)
+      if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
+    if (g_gout) {
+      if (tan && (rc = run_mix(p, c, w, dS, W, ggk, 0, stream))) return rc;
+      if (t_gW && (rc = run_mix(p, c, w, S, t_gW, ggk, tan ? 1 : 0, stream))) return rc;
+    }
+    if (g_W && tan && (rc = run_ga(p, c, w, ws, dS, gk, g_W, 0, stream))) return rc;
+    if (edge) {
+      if ((rc = run_sbar(p, c, w, gk, W, Sb, stream))) return rc;
+      if (t_gW && (rc = run_sbar(p, c, w, gk, t_gW, Sb2, stream))) return rc;
+      int r0 = c.r0, n = c.n, e0 = (int)c.e0;
+      long long ncap = w.ncap;
+      int fl = flags;
+      LAUNCH(p.k.dbwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
+             (const float*)Sb, (const float*)Sb2, txk, t_gevec, t_gphi, g_phi, g_evec, contrib, r0, n, ncap, e0, fl);
+      if (g_x && (rc = run_sender_reduce(p, G, c, contrib, gxk, ci == 0, stream))) return rc;
+    }
+  }
+  if (g_gout && (rc = zero_dead_out(p, ggk, G.N, stream))) return rc;
+  if (mulir) {
+    if (g_gout && (rc = transpose(p, ggk, g_gout, G.N, false, 1, stream))) return rc;
+    if (g_x && (rc = transpose(p, gxk, g_x, G.N, true, 1, stream))) return rc;
+  }
+  return SOBEK_OK;
+}
+
+}  // extern "C"

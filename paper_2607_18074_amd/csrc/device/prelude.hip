@@ -1,0 +1,264 @@
+// Device code shared by every generated plan.  The plan generator prepends its
+// constants and specialised edge kernels to this file and compiles the result
+// with hipRTC for gfx950 (wave64, fp32 MFMA, packed-FP32 disabled).
+//
+// Contents
+//   * channel GEMMs on fp32 MFMA (v_mfma_f32_16x16x4_f32), per output group g
+//     of the receiver-factorised program (Section 4.2 eq. receiver_matrix_product,
+//     Section 4.3 eq. receiver_adjoint, Section 4.4 eq. receiver_double_adjoint):
+//       sobek_gemm_sa    out(i, m_o, w)  (+)= sum_k S_g[(i,m_o), k] A_g[k, w]
+//       sobek_gemm_sbar  Sbar_g[(i,m_o), k] = sum_w mbar(i, m_o, w) A_g[k, w]
+//       sobek_gemm_ga    P[split, k, w]   = sum_{(i,m_o) in split} S_g[(i,m_o), k] mbar(i, m_o, w)
+//     A_g[k, w] is read in place from W: row k of group g lives at W + ktab[k]
+//     (ktab[k] = q*N_w + off_pi + u*C_out for k = koff_pi + q*C_in + u).
+//   * sobek_ga_reduce: fixed-order sum of the split partials into W's layout.
+//   * sobek_sender_reduce: deterministic x-gradient gather over the sender-sorted
+//     view (Section 4.3: one fixed reduction order per source row).
+//   * layout transposes (ir_mul <-> mul_ir, Section 4.5) and a column fill.
+//
+// MFMA 16x16x4 fp32 operand layout (lane l of the wave):
+//   A[i][k] in lane i + 16k,  B[k][j] in lane j + 16k,
+//   D[4g + r][j] in accumulator register r of lane j + 16g.
+
+typedef float sb_f4 __attribute__((ext_vector_type(4)));
+typedef long long sb_i64;
+
+#define SB_DEV __device__ __forceinline__
+
+SB_DEV sb_f4 sb_mfma(float a, float b, sb_f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// GEMM tiles: 256 threads = 4 waves; block tile BM=64 rows x BN columns, BK=16.
+// Wave w owns rows [16w, 16w+16) and all BN columns (BN/16 MFMA tiles).
+// ---------------------------------------------------------------------------
+#define SB_BM 64
+#define SB_BK 16
+
+// out row r of group g -> address of (receiver r0 + r / dg, component r % dg) block.
+SB_DEV sb_i64 sb_row_addr(int r, int dg, int Cg, int off, int CX, int r0) {
+  return (sb_i64)(r0 + r / dg) * CX + off + (r % dg) * Cg;
+}
+
+template <int BN>
+SB_DEV void sb_gemm_sa(const float* __restrict__ S, int nrows, int D, const float* __restrict__ W,
+                       const int* __restrict__ ktab, float* __restrict__ out, int dg, int Cg, int off,
+                       int CX, int r0, int accumulate) {
+  __shared__ float sA[SB_BK][SB_BM + 4];
+  __shared__ float sB[SB_BK][BN + 4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int rb = blockIdx.x * SB_BM, cb = blockIdx.y * BN;
+  sb_f4 acc[BN / 16];
+#pragma unroll
+  for (int t = 0; t < BN / 16; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < D; k0 += SB_BK) {
+    for (int idx = tid; idx < SB_BM * SB_BK; idx += 256) {
+      int row = idx / SB_BK, kk = idx % SB_BK;
+      int gr = rb + row, gk = k0 + kk;
+      sA[kk][row] = (gr < nrows && gk < D) ? S[(sb_i64)gr * D + gk] : 0.f;
+    }
+    for (int idx = tid; idx < SB_BK * BN; idx += 256) {
+      int kk = idx / BN, c = idx % BN;
+      int gk = k0 + kk, gc = cb + c;
+      sB[kk][c] = (gk < D && gc < Cg) ? W[(sb_i64)ktab[gk] + gc] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < SB_BK; kk += 4) {
+      float a = sA[kk + (lane >> 4)][16 * wave + (lane & 15)];
+#pragma unroll
+      for (int t = 0; t < BN / 16; ++t) acc[t] = sb_mfma(a, sB[kk + (lane >> 4)][16 * t + (lane & 15)], acc[t]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      int row = rb + 16 * wave + 4 * (lane >> 4) + r;
+      int col = cb + 16 * t + (lane & 15);
+      if (row < nrows && col < Cg) {
+        float* o = out + sb_row_addr(row, dg, Cg, off, CX, r0) + col;
+        *o = accumulate ? (*o + acc[t][r]) : acc[t][r];
+      }
+    }
+}
+
+template <int BN>
+SB_DEV void sb_gemm_sbar(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
+                         const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int Cg, int off,
+                         int CX, int r0) {
+  __shared__ float sA[SB_BK][SB_BM + 4];
+  __shared__ float sB[SB_BK][BN + 4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int rb = blockIdx.x * SB_BM, kb = blockIdx.y * BN;
+  sb_f4 acc[BN / 16];
+#pragma unroll
+  for (int t = 0; t < BN / 16; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  for (int w0 = 0; w0 < Cg; w0 += SB_BK) {
+    for (int idx = tid; idx < SB_BM * SB_BK; idx += 256) {
+      int row = idx / SB_BK, ww = idx % SB_BK;
+      int gr = rb + row, gw = w0 + ww;
+      sA[ww][row] = (gr < nrows && gw < Cg) ? M[sb_row_addr(gr, dg, Cg, off, CX, r0) + gw] : 0.f;
+    }
+    for (int idx = tid; idx < SB_BK * BN; idx += 256) {
+      int kc = idx / SB_BK, ww = idx % SB_BK;
+      int gk = kb + kc, gw = w0 + ww;
+      sB[ww][kc] = (gk < D && gw < Cg) ? W[(sb_i64)ktab[gk] + gw] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < SB_BK; kk += 4) {
+      float a = sA[kk + (lane >> 4)][16 * wave + (lane & 15)];
+#pragma unroll
+      for (int t = 0; t < BN / 16; ++t) acc[t] = sb_mfma(a, sB[kk + (lane >> 4)][16 * t + (lane & 15)], acc[t]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      int row = rb + 16 * wave + 4 * (lane >> 4) + r;
+      int col = kb + 16 * t + (lane & 15);
+      if (row < nrows && col < D) Sbar[(sb_i64)row * D + col] = acc[t][r];
+    }
+}
+
+template <int BN>
+SB_DEV void sb_gemm_ga(const float* __restrict__ S, int nrows, int D, const float* __restrict__ M,
+                       float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split) {
+  __shared__ float sA[SB_BK][SB_BM + 4];
+  __shared__ float sB[SB_BK][BN + 4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int kb = blockIdx.x * SB_BM, cb = blockIdx.y * BN, split = blockIdx.z;
+  const int rbeg = split * rows_per_split;
+  const int rend = min(nrows, rbeg + rows_per_split);
+  sb_f4 acc[BN / 16];
+#pragma unroll
+  for (int t = 0; t < BN / 16; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  for (int r0b = rbeg; r0b < rend; r0b += SB_BK) {
+    for (int idx = tid; idx < SB_BK * SB_BM; idx += 256) {
+      int rr = idx / SB_BM, kk = idx % SB_BM;
+      int gr = r0b + rr, gk = kb + kk;
+      sA[rr][kk] = (gr < rend && gk < D) ? S[(sb_i64)gr * D + gk] : 0.f;
+    }
+    for (int idx = tid; idx < SB_BK * BN; idx += 256) {
+      int rr = idx / BN, c = idx % BN;
+      int gr = r0b + rr, gc = cb + c;
+      sB[rr][c] = (gr < rend && gc < Cg) ? M[sb_row_addr(gr, dg, Cg, off, CX, r0) + gc] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < SB_BK; kk += 4) {
+      float a = sA[kk + (lane >> 4)][16 * wave + (lane & 15)];
+#pragma unroll
+      for (int t = 0; t < BN / 16; ++t) acc[t] = sb_mfma(a, sB[kk + (lane >> 4)][16 * t + (lane & 15)], acc[t]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      int k = kb + 16 * wave + 4 * (lane >> 4) + r;
+      int col = cb + 16 * t + (lane & 15);
+      if (k < D && col < Cg) P[((sb_i64)split * D + k) * Cg + col] = acc[t][r];
+    }
+}
+
+#define SB_GEMM_ENTRY(BN)                                                                           \
+  extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sa_##BN(                            \
+      const float* S, int nrows, int D, const float* W, const int* ktab, float* out, int dg,       \
+      int Cg, int off, int CX, int r0, int accumulate) {                                           \
+    sb_gemm_sa<BN>(S, nrows, D, W, ktab, out, dg, Cg, off, CX, r0, accumulate);                    \
+  }                                                                                                \
+  extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sbar_##BN(                          \
+      const float* M, int nrows, int D, const float* W, const int* ktab, float* Sbar, int dg,      \
+      int Cg, int off, int CX, int r0) {                                                           \
+    sb_gemm_sbar<BN>(M, nrows, D, W, ktab, Sbar, dg, Cg, off, CX, r0);                             \
+  }                                                                                                \
+  extern "C" __global__ __launch_bounds__(256) void sobek_gemm_ga_##BN(                            \
+      const float* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \
+      int r0, int rows_per_split) {                                                                \
+    sb_gemm_ga<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split);                        \
+  }
+
+SB_GEMM_ENTRY(16)
+SB_GEMM_ENTRY(32)
+SB_GEMM_ENTRY(64)
+
+// gW[ktab[k] + w] = (first ? 0 : gW[..]) + sum_{s < nsplit} P[s, k, w]   (fixed split order)
+extern "C" __global__ __launch_bounds__(256) void sobek_ga_reduce(const float* P, int nsplit, int D, int Cg,
+                                                                  const int* ktab, float* gW, int first) {
+  sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (sb_i64)D * Cg) return;
+  int k = (int)(t / Cg), w = (int)(t % Cg);
+  float s = 0.f;
+  for (int p = 0; p < nsplit; ++p) s += P[((sb_i64)p * D + k) * Cg + w];
+  float* o = gW + (sb_i64)ktab[k] + w;
+  *o = first ? s : (*o + s);
+}
+
+// One wave per sender j: x-gradient rows are the sum, in sender-CSR order, of the
+// per-edge contribution rows of its out-edges inside the receiver chunk [e0, e1)
+// (contributions are stored at row e - e0).  first: chunk 0 overwrites every row.
+extern "C" __global__ __launch_bounds__(256) void sobek_sender_reduce(const int* send_rowptr, const int* send_perm,
+                                                                      const float* contrib, float* gx, int N,
+                                                                      int CX, int e0, int e1, int first) {
+  int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  int lane = threadIdx.x & 63;
+  if (j >= N) return;
+  int b = send_rowptr[j], e = send_rowptr[j + 1];
+  int lo = b, hi = e;
+  while (lo < hi) {  // first position with edge id >= e0
+    int mid = (lo + hi) >> 1;
+    if (send_perm[mid] < e0) lo = mid + 1; else hi = mid;
+  }
+  int start = lo;
+  hi = e;
+  while (lo < hi) {  // first position with edge id >= e1
+    int mid = (lo + hi) >> 1;
+    if (send_perm[mid] < e1) lo = mid + 1; else hi = mid;
+  }
+  int stop = lo;
+  if (!first && start == stop) return;
+  for (int c = lane; c < CX; c += 64) {
+    float s = first ? 0.f : gx[(sb_i64)j * CX + c];
+    for (int p = start; p < stop; ++p) s += contrib[(sb_i64)(send_perm[p] - e0) * CX + c];
+    gx[(sb_i64)j * CX + c] = s;
+  }
+}
+
+// Layout transpose of one irrep block per launch row: for node n and block
+// (off, C, d): ir_mul index off + m*C + u  <->  mul_ir index off + u*d + m.
+// dir = 0: mul_ir -> ir_mul, dir = 1: ir_mul -> mul_ir.
+extern "C" __global__ __launch_bounds__(256) void sobek_transpose(const float* src, float* dst, int N, int CX,
+                                                                  const int* boff, const int* bmul,
+                                                                  const int* bdim, int nblocks, int dir) {
+  sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (sb_i64)N * CX) return;
+  int n = (int)(t / CX), col = (int)(t % CX);
+  int b = 0;
+  while (b + 1 < nblocks && boff[b + 1] <= col) ++b;
+  int C = bmul[b], d = bdim[b], r = col - boff[b];
+  int m = r / C, u = r % C;  // col read as ir_mul (m, u)
+  int other = boff[b] + u * d + m;
+  if (dir == 0) dst[(sb_i64)n * CX + col] = src[(sb_i64)n * CX + other];
+  else dst[(sb_i64)n * CX + other] = src[(sb_i64)n * CX + col];
+}
+
+// out[n][off + c] = 0 for c < width (output irreps no path reaches).
+extern "C" __global__ __launch_bounds__(256) void sobek_fill_cols(float* out, int N, int CX, int off, int width) {
+  sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (sb_i64)N * width) return;
+  int n = (int)(t / width), c = (int)(t % width);
+  out[(sb_i64)n * CX + off + c] = 0.f;
+}
+
+// Every value of buf[0..n) = 0 (used instead of memset so the stream stays capture-safe).
+extern "C" __global__ __launch_bounds__(256) void sobek_zero(float* buf, sb_i64 n) {
+  sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (t < n) buf[t] = 0.f;
+}

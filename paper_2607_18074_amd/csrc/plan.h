@@ -1,0 +1,97 @@
+// Plan: the static description of one operator signature (irreps, K, layout,
+// normalisation), the path/group/unit decomposition the kernels are generated
+// from, and the compiled kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <map>
+#include <string>
+#include <vector>
+
+namespace sobek {
+
+struct Irrep {
+  int mul, l, p;
+  int off;  // start in the flattened vector
+  int dim() const { return mul * (2 * l + 1); }
+};
+
+// One tensor-product path (Section 2.4): input irrep a, SH order l_sh, output irrep c.
+struct Path {
+  int i_in, i_sh, i_out;
+  int l_in, l_sh, l_out;
+  int c_in, c_out;
+  int64_t w_off = 0;    // offset in the flattened weight axis (eq. num_weights)
+  double alpha = 1.0;   // path normalisation
+  int group = -1;       // index into Plan::groups
+  int64_t koff = 0;     // column offset of this path inside its group's receiver state
+  std::vector<double> cg;  // alpha * Q, dense [d_in][d_sh][d_out]
+};
+
+// Output group g = one output irrep block with its paths (Section 4.2).
+// Receiver state rows are (receiver, m_o); columns k = koff_pi + q * C_in + u.
+struct Group {
+  int i_out, l, d, C, off;
+  std::vector<int> paths;
+  int64_t D;      // K * sum of C_in over the group's paths
+  int64_t s_off;  // per-receiver offset of the group block (floats) = sum of d*D of earlier groups
+  int64_t ktab_off;  // offset of this group's k-table in Plan::ktab
+};
+
+// A wave's share of an edge kernel: input irrep a, channel block [U0, U0 + U)
+// of the input multiplicity, ES edges in flight per wave (lane = sub * U + u),
+// and the list of paths (all with input a).
+struct Unit {
+  int a;
+  int U, U0, ES;
+  std::vector<int> paths;
+  bool first = true;   // backward only: first slab that writes (a, U0) contributions
+  std::vector<int> lds_off;  // backward only: LDS offset of each path's Sbar slice
+};
+
+// Backward slab: wave units whose adjoint state slices are staged in LDS together.
+struct Slab {
+  std::vector<Unit> waves;
+  int lds_floats = 0;
+};
+
+struct Kernels {
+  hipModule_t module = nullptr;
+  hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, bwd_E = nullptr, dbwd_E = nullptr;
+  hipFunction_t gemm_sa[3] = {}, gemm_sbar[3] = {}, gemm_ga[3] = {};  // BN = 16, 32, 64
+  hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
+                zero = nullptr;
+};
+
+struct Plan {
+  std::vector<Irrep> in, out;
+  int lmax = 0, K = 0, layout = 0, dtype = 0, norm = 0;
+  int dim_in = 0, dim_out = 0, nsh = 0;
+  int64_t n_w = 0;
+  std::vector<Path> paths;
+  std::vector<Group> groups;
+  int64_t srow = 0;  // floats of receiver state per receiver (sum over groups of d * D)
+  std::vector<int32_t> ktab;   // host copy of all groups' k-tables
+  std::vector<Unit> fwd_units;
+  std::vector<Slab> slabs;
+  int bwd_eb = 32;              // edges per batch in the backward edge kernel
+  int bwd_lds_max = 0;          // largest slab (floats)
+  std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
+  std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)
+  std::string source;           // generated HIP source
+  std::string cache_key;
+  Kernels k;
+  // device tables
+  int32_t* d_ktab = nullptr;
+  int32_t* d_in_blocks = nullptr;   // [3][n_in]: off, mul, dim(2l+1)
+  int32_t* d_out_blocks = nullptr;  // [3][n_out]
+};
+
+// Builds paths, groups, units and slabs for a validated signature.
+void build_plan(Plan& p);
+// Generates the plan-specific HIP source (prepended by the shared prelude at compile time).
+std::string generate_source(const Plan& p);
+
+}  // namespace sobek
