@@ -1,0 +1,283 @@
+#!/usr/bin/env python
+"""Benchmark: one step = forward + backward + double backward of the TP convolution.
+
+Prints ONE JSON line.  Workload (default): the edge-scaling stress graph
+(200,000 nodes, ~16M directed edges, mean degree 80 at cutoff 6.0, K = 8,
+32x0e+32x1o+32x2e with SH up to l = 2), synthetic and seeded.  The backward
+cotangent is N(0, 1); the double-backward cotangent is the one of the loss
+"sum of squared edge-vector gradients", i.e. t_gevec = 2 * evec_bar with the
+other three cotangents zero.  Inputs are resident in HBM before timing.
+
+value = E / (seconds per step): whole-step edge throughput on one GPU.
+roofline: the kernel with the largest share of the timed region, its
+algorithmic FLOPs per launch (model below) over its mean launch duration,
+measured with HIP events recorded on its launch stream inside the timed region.
+cpu_baseline: the float64 oracle, timed on this host on a bounded receiver
+sample of the same workload, scaled to edges/s.
+
+Per-kernel algorithmic FLOP model (per edge E, per receiver N; SD = sum_pi
+C_in d_out, NZ = sum_pi C_in nnz_pi, G = sum_pi C_in d_out C_out):
+  fwd_S / fwd_dS (r-only tangent)  E (2 K SD + 2 NZ)
+  gemm_sa, gemm_sbar, gemm_ga      N 2 K G each
+  bwd_E                            E (4 K SD + 6 NZ)
+  dbwd_E (r-only tangent)          E (4 K SD + 6 NZ)
+The backward's recomputation of S for the weight gradient is overhead and is
+not counted as algorithmic work.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "edges/s and % roofline for TP-conv fwd/bwd/double-bwd; peak memory (GB)"
+PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 vector / matrix
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def flop_model(plan, N, E):
+    K = plan.K
+    SD = NZ = G = 0
+    for t, (a, _b, c, _w) in enumerate(plan.paths()):
+        cin = plan.irreps_in[a][0]
+        lo = plan.irreps_out[c][1]
+        cout = plan.irreps_out[c][0]
+        nnz = int(np.count_nonzero(plan.cg(t)))
+        SD += cin * (2 * lo + 1)
+        NZ += cin * nnz
+        G += cin * (2 * lo + 1) * cout
+    edge_fwd = E * (2 * K * SD + 2 * NZ)
+    edge_adj = E * (4 * K * SD + 6 * NZ)
+    gemm = N * 2 * K * G
+    per_kernel = {
+        "fwd_S": edge_fwd, "fwd_dS": edge_fwd, "bwd_E": edge_adj, "dbwd_E": edge_adj,
+        "gemm_sa": gemm, "gemm_sbar": gemm, "gemm_ga": gemm,
+    }
+    passes = {"fwd": edge_fwd + gemm, "bwd": 2 * gemm + edge_adj, "dbwd": edge_fwd + 3 * gemm + edge_adj}
+    return dict(SD=SD, NZ=NZ, G=G, per_kernel=per_kernel, passes=passes)
+
+
+def kernel_kind(name):
+    for k in ("fwd_dS", "fwd_S", "bwd_E", "dbwd_E", "gemm_sa", "gemm_sbar", "gemm_ga"):
+        if name == "sobek_" + k or name.startswith("sobek_" + k + "_"):
+            return k
+    return None
+
+
+def cpu_baseline(case, plan_sig, target_s=15.0):
+    """Time the oracle (fwd + bwd + dbwd) on the in-edges of the first receivers."""
+    from oracle import conv as oc
+    g, x, W, gout, rdot = case
+    prob = oc.Problem(*plan_sig)
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+
+    def run(R):
+        Es = int(g.rowptr[R])
+        rp = g.rowptr[:R + 1].astype(np.int64)
+        args = (prob, x, g.evec[:Es], g.phi[:Es], W, rp, g.sender[:Es])
+        gsub = gout[:R]
+        t0 = time.perf_counter()
+        oc.fwd(*args)
+        oc.bwd(*args, gsub)
+        oc.dbwd(*args, gsub, t_gevec=rdot[:Es])
+        return Es, time.perf_counter() - t0
+
+    run(2)                       # first call fills the oracle's table caches
+    R = 4
+    Es, dt = run(R)
+    while dt < 0.5 * target_s and R < g.N:
+        R = min(g.N, max(R + 1, int(R * min(4.0, 0.9 * target_s / max(dt, 1e-3)))))
+        Es, dt = run(R)
+    return dict(value=Es / dt, unit="edges/s", cores=int(cores), kind="oracle",
+                sample=f"fwd+bwd+dbwd (t_gevec-only) float64 oracle on the in-edges of the first {R} receivers "
+                       f"({Es} edges) of the same graph and tensors; {dt:.1f} s",
+                seconds=dt)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="stress")
+    ap.add_argument("--budget", type=float, default=2.0, help="workspace budget per pass, GiB")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--calibrate-copy", type=float, default=0.0,
+                    help="only run a plain device copy of this many MiB (traffic-counter calibration)")
+    args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = int(args.calibrate_copy * (1 << 20)) // 4
+        src = torch.randn(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 3}))
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (see DESIGN.md for how it "
+              "would shard); rerun with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_18074_amd import _lib, api
+    from paper_2607_18074_amd import workloads as wl
+
+    cfg = wl.CONFIGS[args.workload]
+    t0 = time.time()
+    g = wl.config_graph(args.workload)
+    log(f"graph {args.workload}: N={g.N} E={g.E} ({time.time() - t0:.1f}s)")
+    torch.cuda.set_device(0)
+    plan = api.Plan(cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"])
+    x = wl.node_features(g.N, plan.dim_in, cfg["index"])
+    W = wl.weights(plan.K, plan.weight_std(), cfg["index"])
+    gout = wl.out_cotangent(g.N, plan.dim_out, cfg["index"])
+    dev = "cuda"
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    graph = api.Graph(T(g.rowptr), T(g.sender))
+    xt, ev, ph, Wt, gt = T(x), T(g.evec), T(g.phi), T(W), T(gout)
+    budget = int(args.budget * (1 << 30))
+    ws = {p: graph.workspace(plan, p, budget) for p in ("fwd", "bwd", "dbwd")}
+    out = torch.empty(g.N, plan.dim_out, device=dev)
+
+    def fwd():
+        return api.conv_fwd(plan, graph, xt, ev, ph, Wt, out=out, ws=ws["fwd"])
+
+    def bwd():
+        return api.conv_bwd(plan, graph, xt, ev, ph, Wt, gt, ws=ws["bwd"])
+
+    rdot = None
+
+    def dbwd():
+        return api.conv_dbwd(plan, graph, xt, ev, ph, Wt, gt, t_gevec=rdot, ws=ws["dbwd"])
+
+    # cotangent of L2 = sum |evec_bar|^2
+    _, gev, _, _ = bwd()
+    rdot = (2.0 * gev).contiguous()
+    del gev
+
+    def step():
+        fwd()
+        bwd()
+        dbwd()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+
+    # timed region: K steps, with per-launch HIP events on the launch stream
+    _lib.profile_reset()
+    _lib.profile_enable(True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    _lib.profile_enable(False)
+    prof = _lib.profile_read()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    peak_gb = torch.cuda.max_memory_allocated() / 1e9
+
+    # per-pass timing (outside the headline region)
+    pass_ms = {}
+    for name, fn in (("fwd", fwd), ("bwd", bwd), ("dbwd", dbwd)):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(args.steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        pass_ms[name] = a.elapsed_time(b) / args.steps
+
+    fm = flop_model(plan, g.N, g.E)
+    kernels = {}
+    for name, (n, ms) in prof.items():
+        kernels[name] = dict(launches_per_step=n / args.steps, ms_per_step=ms / args.steps,
+                             mean_launch_ms=ms / max(n, 1))
+    dom = max(prof.items(), key=lambda kv: kv[1][1])
+    dom_name, (dom_n, dom_ms) = dom
+    kind = kernel_kind(dom_name)
+    if kind in fm["per_kernel"]:
+        per_step = fm["per_kernel"][kind]
+        if kind.startswith("gemm"):
+            per_step *= {"gemm_sa": 1, "gemm_sbar": 2, "gemm_ga": 2}[kind]  # launches of this GEMM per step
+        flops_per_launch = per_step * args.steps / dom_n
+        achieved = flops_per_launch / (dom_ms / dom_n * 1e-3) / 1e12
+        roof = dict(bound="mfma" if kind.startswith("gemm") else "alu", kernel=dom_name, achieved=achieved,
+                    peak=PEAK_FP32_TFLOPS, unit="TFLOP/s", frac=achieved / PEAK_FP32_TFLOPS, traffic=None,
+                    flops_per_launch=flops_per_launch, mean_launch_ms=dom_ms / dom_n,
+                    share_of_step=dom_ms / args.steps / ms_step)
+    else:
+        roof = dict(bound="hbm", kernel=dom_name, achieved=None, peak=PEAK_HBM_GBS, unit="GB/s", frac=None,
+                    traffic=None)
+
+    passes = {}
+    for name in ("fwd", "bwd", "dbwd"):
+        ms = pass_ms[name]
+        tf = fm["passes"][name] / (ms * 1e-3) / 1e12
+        passes[name] = dict(ms=ms, edges_per_s=g.E / (ms * 1e-3), tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS)
+    step_flops = sum(fm["passes"].values())
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a receiver sample ...")
+        cpu = cpu_baseline((g, x, W, gout, rdot.cpu().numpy()),
+                           (cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"]), args.cpu_seconds)
+
+    result = {
+        "metric": METRIC,
+        "value": g.E / (ms_step * 1e-3),
+        "unit": "edges/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "N": g.N, "E": g.E, "K": plan.K, "irreps_in": cfg["irreps_in"],
+                   "lmax": cfg["lmax"], "irreps_out": cfg["irreps_out"], "step": "fwd+bwd+dbwd",
+                   "dbwd_cotangent": "t_gevec = 2 evec_bar", "workspace_budget_gib": args.budget},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "step_tflops": step_flops / (ms_step * 1e-3) / 1e12,
+        "step_frac_fp32": step_flops / (ms_step * 1e-3) / 1e12 / PEAK_FP32_TFLOPS,
+        "passes": passes,
+        "peak_mem_gb": peak_gb,
+        "workspace_gb": {p: w.numel() / 1e9 for p, w in ws.items()},
+        "kernels": kernels,
+        "wall_s_timed": wall,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

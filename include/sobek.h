@@ -168,6 +168,17 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float *x, const fl
                     float *g_x, float *g_evec, float *g_phi, float *g_W, void *ws, size_t ws_bytes,
                     hipStream_t stream);
 
+/* Measurement instrumentation (not part of the operator).  When enabled, each
+ * kernel launch of the library is bracketed by two hipEvents recorded on the
+ * launch stream.  sobek_profile_query synchronises on those events and reports,
+ * per kernel name (index idx in name order), the launch count and summed
+ * event-to-event milliseconds; it returns SOBEK_E_INVALID past the last name.
+ * sobek_profile_reset drops the records.  Not thread-safe against concurrent
+ * launches on other threads while enabled. */
+int sobek_profile_enable(int on);
+int sobek_profile_reset(void);
+int sobek_profile_query(int idx, char *name, size_t name_bytes, int64_t *launches, double *total_ms);
+
 #ifdef __cplusplus
 }
 #endif

@@ -61,6 +61,9 @@ _SIGNATURES = {
     "sobek_conv_fwd": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "sobek_conv_bwd": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "sobek_conv_dbwd": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "sobek_profile_enable": (_INT, [_INT]),
+    "sobek_profile_reset": (_INT, []),
+    "sobek_profile_query": (_INT, [_INT, ctypes.c_char_p, _SZ, ctypes.POINTER(_I64), ctypes.POINTER(ctypes.c_double)]),
 }
 
 EXPORTED = tuple(_SIGNATURES)
@@ -146,3 +149,24 @@ def sh_table(l, m, max_terms=64):
     pw = (ctypes.c_int32 * (3 * max_terms))()
     check(lib().sobek_sh_table(l, m, ctypes.byref(n), c, pw, max_terms))
     return [(c[t], (pw[3 * t], pw[3 * t + 1], pw[3 * t + 2])) for t in range(n.value)]
+
+
+def profile_enable(on=True):
+    check(lib().sobek_profile_enable(1 if on else 0))
+
+
+def profile_reset():
+    check(lib().sobek_profile_reset())
+
+
+def profile_read():
+    """{kernel name: (launches, total ms)} of the launches recorded since the last reset."""
+    out = {}
+    idx = 0
+    name = ctypes.create_string_buffer(256)
+    n = _I64()
+    ms = ctypes.c_double()
+    while lib().sobek_profile_query(idx, name, 256, ctypes.byref(n), ctypes.byref(ms)) == 0:
+        out[name.value.decode()] = (n.value, ms.value)
+        idx += 1
+    return out

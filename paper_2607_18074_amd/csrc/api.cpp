@@ -23,7 +23,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <memory>
+#include <mutex>
 #include <stdexcept>
 #include <string>
 #include <vector>
@@ -69,11 +71,45 @@ int fail(int code, const char* fmt, ...) {
     if (e_ != hipSuccess) return fail(SOBEK_E_HIP, "%s: %s", #call, hipGetErrorString(e_));  \
   } while (0)
 
+// Optional instrumentation: when enabled, every launch is bracketed by two
+// hipEvents recorded on the launch stream; durations are resolved on query.
+struct ProfRec {
+  std::string name;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::map<hipFunction_t, std::string> g_names;
+std::vector<ProfRec> g_prof;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t pool_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  (void)hipEventCreate(&e);
+  return e;
+}
+
 template <typename... Args>
 hipError_t launch(hipFunction_t f, unsigned gx, unsigned gy, unsigned gz, hipStream_t s, Args... args) {
   if (gx == 0 || gy == 0 || gz == 0) return hipSuccess;
   void* ptrs[] = {(void*)&args...};
-  return hipModuleLaunchKernel(f, gx, gy, gz, 256, 1, 1, 0, s, ptrs, nullptr);
+  if (!g_prof_on) return hipModuleLaunchKernel(f, gx, gy, gz, 256, 1, 1, 0, s, ptrs, nullptr);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  ProfRec r;
+  auto it = g_names.find(f);
+  r.name = it == g_names.end() ? std::string("?") : it->second;
+  r.a = pool_event();
+  r.b = pool_event();
+  (void)hipEventRecord(r.a, s);
+  hipError_t e = hipModuleLaunchKernel(f, gx, gy, gz, 256, 1, 1, 0, s, ptrs, nullptr);
+  (void)hipEventRecord(r.b, s);
+  g_prof.push_back(r);
+  return e;
 }
 
 #define LAUNCH(...) HIPCHK(launch(__VA_ARGS__))
@@ -380,6 +416,8 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   auto get = [&](hipFunction_t& f, const char* name) -> int {
     hipError_t e = hipModuleGetFunction(&f, p.k.module, name);
     if (e != hipSuccess) return fail(SOBEK_E_INTERNAL, "kernel %s missing: %s", name, hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_names[f] = name;
     return SOBEK_OK;
   };
   const char* bns[3] = {"16", "32", "64"};
@@ -441,6 +479,45 @@ int sobek_plan_source(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
     std::memcpy(buf, s.data(), n);
     buf[n] = 0;
   }
+  return SOBEK_OK;
+}
+
+int sobek_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = on != 0;
+  return SOBEK_OK;
+}
+
+int sobek_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& r : g_prof) {
+    g_event_pool.push_back(r.a);
+    g_event_pool.push_back(r.b);
+  }
+  g_prof.clear();
+  return SOBEK_OK;
+}
+
+int sobek_profile_query(int idx, char* name, size_t name_bytes, int64_t* launches, double* total_ms) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  std::map<std::string, std::pair<int64_t, double>> agg;
+  for (auto& r : g_prof) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return fail(SOBEK_E_HIP, "profile event: %s", hipGetErrorString(e));
+    auto& v = agg[r.name];
+    v.first += 1;
+    v.second += ms;
+  }
+  if (idx < 0 || idx >= (int)agg.size()) return fail(SOBEK_E_INVALID, "profile index %d out of range", idx);
+  auto it = agg.begin();
+  std::advance(it, idx);
+  if (name && name_bytes) {
+    std::snprintf(name, name_bytes, "%s", it->first.c_str());
+  }
+  if (launches) *launches = it->second.first;
+  if (total_ms) *total_ms = it->second.second;
   return SOBEK_OK;
 }
 
