@@ -209,7 +209,9 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, WsPlan& w, size
   }
   w.off_P = o;  // partials, sized once the chunk capacity is known
   w.fixed = o;
-  w.nstate = pass == SOBEK_PASS_FWD ? 1 : (pass == SOBEK_PASS_BWD ? 2 : 4);
+  // receiver-state slots: one, reused phase by phase (S, then Sbar); the double
+  // backward needs a second one for Sbar' when dA is active
+  w.nstate = pass == SOBEK_PASS_DBWD ? 2 : 1;
   per_recv = (size_t)w.nstate * p.srow * 4;
   per_edge = pass == SOBEK_PASS_FWD ? 0 : (size_t)p.dim_in * 4;
 }
@@ -320,7 +322,8 @@ int run_state(const Plan& p, const sobek_graph_s& G, const Chunk& c, const WsPla
   const int NU = (int)p.fwd_units.size();
   long long ncap = w.ncap;
   int r0 = c.r0, n = c.n;
-  LAUNCH(tangent ? p.k.fwd_dS : p.k.fwd_S, cdiv((int64_t)n * NU, 4), 1, 1, s, (const int*)G.rowptr,
+  hipFunction_t f = !tangent ? p.k.fwd_S : (flags == 4 ? p.k.fwd_dS_r : p.k.fwd_dS);
+  LAUNCH(f, cdiv((int64_t)n * NU, 4), 1, 1, s, (const int*)G.rowptr,
          (const int*)G.sender, evec, phi, x, S, r0, n, ncap, xdot, evdot, phidot, flags);
   return SOBEK_OK;
 }
@@ -422,7 +425,8 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   };
   const char* bns[3] = {"16", "32", "64"};
   if ((rc = get(p.k.fwd_S, "sobek_fwd_S")) || (rc = get(p.k.fwd_dS, "sobek_fwd_dS")) ||
-      (rc = get(p.k.bwd_E, "sobek_bwd_E")) || (rc = get(p.k.dbwd_E, "sobek_dbwd_E")) ||
+      (rc = get(p.k.fwd_dS_r, "sobek_fwd_dS_r")) || (rc = get(p.k.bwd_E, "sobek_bwd_E")) ||
+      (rc = get(p.k.dbwd_E, "sobek_dbwd_E")) || (rc = get(p.k.dbwd_E_r, "sobek_dbwd_E_r")) ||
       (rc = get(p.k.ga_reduce, "sobek_ga_reduce")) || (rc = get(p.k.sender_reduce, "sobek_sender_reduce")) ||
       (rc = get(p.k.transpose, "sobek_transpose")) || (rc = get(p.k.fill_cols, "sobek_fill_cols")) ||
       (rc = get(p.k.zero, "sobek_zero")))
@@ -714,7 +718,7 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
     if ((rc = transpose(p, gout, (float*)gk, G.N, false, 0, stream))) return rc;
   }
   float* S = state_ptr(w, ws, p, 0);
-  float* Sb = state_ptr(w, ws, p, 1);
+  float* Sb = S;  // the same slot: S is consumed by the weight-gradient GEMM first
   float* contrib = gx ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = gx || gevec || gphi;
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
@@ -772,30 +776,32 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const fl
     if (g_x) gxk = (float*)((char*)ws + w.off_gx);
   }
   if (g_gout && !tan && !t_gW) { if ((rc = fill_zero(p, ggk, G.N * p.dim_out, stream))) return rc; }
+  // one slot reused in stream order: dS (for m_dot and g_W), then S (for m_dot += S dA),
+  // then Sbar; the second slot holds Sbar' when dA is active
   float* dS = state_ptr(w, ws, p, 0);
-  float* S = state_ptr(w, ws, p, 1);
-  float* Sb = state_ptr(w, ws, p, 2);
-  float* Sb2 = state_ptr(w, ws, p, 3);
+  float* S = dS;
+  float* Sb = dS;
+  float* Sb2 = state_ptr(w, ws, p, 1);
   float* contrib = g_x ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = g_x || g_evec || g_phi;
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
-    if (tan && (g_gout || g_W))
+    if (tan && (g_gout || g_W)) {
       if ((rc = run_state(p, G, c, w, dS, true, xk, evec, phi, txk, t_gevec, t_gphi, flags & 7, stream))) return rc;
-    if (t_gW && g_gout)
-      if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
-    if (g_gout) {
-      if (tan && (rc = run_mix(p, c, w, dS, W, ggk, 0, stream))) return rc;
-      if (t_gW && (rc = run_mix(p, c, w, S, t_gW, ggk, tan ? 1 : 0, stream))) return rc;
+      if (g_gout && (rc = run_mix(p, c, w, dS, W, ggk, 0, stream))) return rc;
+      if (g_W && (rc = run_ga(p, c, w, ws, dS, gk, g_W, 0, stream))) return rc;
     }
-    if (g_W && tan && (rc = run_ga(p, c, w, ws, dS, gk, g_W, 0, stream))) return rc;
+    if (t_gW && g_gout) {  // S reuses the slot once dS has been consumed
+      if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
+      if ((rc = run_mix(p, c, w, S, t_gW, ggk, tan ? 1 : 0, stream))) return rc;
+    }
     if (edge) {
       if ((rc = run_sbar(p, c, w, gk, W, Sb, stream))) return rc;
       if (t_gW && (rc = run_sbar(p, c, w, gk, t_gW, Sb2, stream))) return rc;
       int r0 = c.r0, n = c.n, e0 = (int)c.e0;
       long long ncap = w.ncap;
       int fl = flags;
-      LAUNCH(p.k.dbwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
+      LAUNCH(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
              (const float*)Sb, (const float*)Sb2, txk, t_gevec, t_gphi, g_phi, g_evec, contrib, r0, n, ncap, e0, fl);
       if (g_x && (rc = run_sender_reduce(p, G, c, contrib, gxk, ci == 0, stream))) return rc;
     }

@@ -18,8 +18,8 @@ namespace sobek {
 
 namespace {
 constexpr int kAccMax = 128;        // forward accumulators per lane per wave unit
-constexpr int kSlabFloats = 8192;   // backward LDS budget for one slab of adjoint state (32 KiB)
-constexpr int kWaves = 4;           // waves per backward block
+constexpr int kSlabFloats = 10240;  // backward LDS budget for one slab of adjoint state (40 KiB)
+constexpr int kWaves = 4;           // waves per adjoint block
 
 bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 
@@ -135,66 +135,66 @@ void build_plan(Plan& p) {
     }
   }
 
-  // backward slabs: wave units (input irrep, channel block, path subset) whose
-  // adjoint-state slices fit the LDS budget; a given (irrep, block) always runs
-  // on the same wave index, so contribution read-modify-writes stay in one thread
+  // adjoint lane mapping: the smallest power of two >= every input multiplicity
+  // (capped at 64) lanes per edge, the rest of the wave holds further edges
+  int umax = 1;
+  for (auto& r : p.in) umax = std::max(umax, std::min(r.mul, 64));
+  p.adj_U = 1;
+  while (p.adj_U < umax) p.adj_U *= 2;
+  p.adj_ES = 64 / p.adj_U;
+  // items (input irrep, channel block, path chunk) packed into LDS slabs in order
   p.slabs.clear();
-  struct Item { Unit u; int floats; };
-  std::vector<std::vector<Item>> per_pair;  // per (a, block): chunks in order
+  std::vector<AdjItem> items;
+  std::vector<int> item_floats;
   for (int a = 0; a < (int)p.in.size(); ++a) {
     std::vector<int> ps;
     for (int t = 0; t < (int)p.paths.size(); ++t)
       if (p.paths[t].i_in == a) ps.push_back(t);
     if (ps.empty()) continue;
-    for (auto blk : channel_blocks(p.in[a].mul)) {
-      std::vector<Item> chunks;
-      Unit cur;
-      cur.a = a; cur.U = blk[0]; cur.U0 = blk[1]; cur.ES = blk[2];
+    for (int u0 = 0; u0 < p.in[a].mul; u0 += p.adj_U) {
+      AdjItem cur;
+      cur.a = a; cur.u0 = u0;
       int fl = 0;
+      bool first = true;
       for (int t : ps) {
-        int need = p.K * (2 * p.paths[t].l_out + 1) * cur.U;
+        int need = p.K * (2 * p.paths[t].l_out + 1) * p.adj_U;
         if (need > kSlabFloats) throw std::runtime_error("path adjoint slice exceeds the LDS slab budget");
         if (!cur.paths.empty() && fl + need > kSlabFloats) {
-          chunks.push_back({cur, fl});
+          cur.first = first;
+          first = false;
+          items.push_back(cur);
+          item_floats.push_back(fl);
           cur.paths.clear();
           fl = 0;
         }
         cur.paths.push_back(t);
         fl += need;
       }
-      chunks.push_back({cur, fl});
-      for (size_t c = 0; c < chunks.size(); ++c) chunks[c].u.first = (c == 0);
-      per_pair.push_back(chunks);
+      cur.first = first;
+      items.push_back(cur);
+      item_floats.push_back(fl);
     }
   }
   {
-    Slab cur;
-    cur.waves.assign(kWaves, Unit{-1, 0, 0, 0, {}, true, {}});
-    auto flush = [&]() {
-      bool any = false;
-      for (auto& w : cur.waves) any |= (w.a >= 0);
-      if (any) p.slabs.push_back(cur);
-      cur = Slab();
-      cur.waves.assign(kWaves, Unit{-1, 0, 0, 0, {}, true, {}});
-    };
-    for (size_t i = 0; i < per_pair.size(); ++i) {
-      int w = (int)(i % kWaves);
-      for (auto& it : per_pair[i]) {
-        if (cur.waves[w].a >= 0 || cur.lds_floats + it.floats > kSlabFloats) flush();
-        Unit u = it.u;
-        int o = cur.lds_floats;
-        for (int t : u.paths) {
-          u.lds_off.push_back(o);
-          o += p.K * (2 * p.paths[t].l_out + 1) * u.U;
-        }
-        cur.waves[w] = u;
-        cur.lds_floats = o;
+    AdjSlab cur;
+    for (size_t i = 0; i < items.size(); ++i) {
+      if (!cur.items.empty() && cur.floats + item_floats[i] > kSlabFloats) {
+        p.slabs.push_back(cur);
+        cur = AdjSlab();
       }
+      AdjItem it = items[i];
+      int o = cur.floats;
+      for (int t : it.paths) {
+        it.lds_off.push_back(o);
+        o += p.K * (2 * p.paths[t].l_out + 1) * p.adj_U;
+      }
+      cur.items.push_back(it);
+      cur.floats = o;
     }
-    flush();
+    if (!cur.items.empty()) p.slabs.push_back(cur);
   }
   p.bwd_lds_max = 0;
-  for (auto& s : p.slabs) p.bwd_lds_max = std::max(p.bwd_lds_max, s.lds_floats);
+  for (auto& s : p.slabs) p.bwd_lds_max = std::max(p.bwd_lds_max, s.floats);
 }
 
 // ---------------------------------------------------------------------------
@@ -390,10 +390,11 @@ int unit_lsh(const Plan& P, const Unit& u) {
 void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) {
   const Irrep& ri = P.in[u.a];
   const int DA = 2 * ri.l + 1, L = unit_lsh(P, u), NS = (L + 1) * (L + 1);
-  o << "template <bool TAN>\nSB_DEV void sb_fwd_u" << id
+  o << "template <bool TAN, int FL>\nSB_DEV void sb_fwd_u" << id
     << "(int lane, int il, int beg, int end, const int* __restrict__ sender, const float* __restrict__ evec,"
        " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, sb_i64 ncap,"
        " const float* __restrict__ xdot, const float* __restrict__ evdot, const float* __restrict__ phidot, int flags) {\n";
+  o << "  const int fl = FL >= 0 ? FL : flags;\n";
   o << "  constexpr int U = " << u.U << ", U0 = " << u.U0 << ", ES = " << u.ES << ", CA = " << ri.mul
     << ", AOFF = " << ri.off << ";\n";
   o << "  const int sub = lane / U, u = U0 + lane % U;\n"
@@ -412,12 +413,12 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
     << "#pragma unroll\n      for (int m = 0; m < " << DA << "; ++m) xv[m] = x[xrow + m * CA];\n";
   o << "      float Yd[" << NS << "], phd[K], xdv[" << DA << "];\n"
        "      if (TAN) {\n"
-       "        if (flags & 4) {\n"
+       "        if (fl & 4) {\n"
        "          const float dx = evdot[3 * (sb_i64)e], dy = evdot[3 * (sb_i64)e + 1], dz = evdot[3 * (sb_i64)e + 2];\n"
     << "          sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n"
     << "        }\n"
-       "        if (flags & 1) {\n#pragma unroll\n          for (int q = 0; q < K; ++q) phd[q] = phidot[(sb_i64)e * K + q];\n        }\n"
-       "        if (flags & 2) {\n#pragma unroll\n"
+       "        if (fl & 1) {\n#pragma unroll\n          for (int q = 0; q < K; ++q) phd[q] = phidot[(sb_i64)e * K + q];\n        }\n"
+       "        if (fl & 2) {\n#pragma unroll\n"
     << "          for (int m = 0; m < " << DA << "; ++m) xdv[m] = xdot[xrow + m * CA];\n        }\n      }\n";
   for (int t : u.paths) {
     const Path& q = P.paths[t];
@@ -430,13 +431,13 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
       << t << "[q * " << DO << " + m]);\n"
       << "        } else {\n"
       << "          float C2[" << DO << "] = {};\n"
-      << "          if (flags & 2) { sb_C" << t << "(xdv, M, C); for (int m = 0; m < " << DO << "; ++m) C2[m] += C[m]; }\n"
-      << "          if (flags & 4) { float Md[P" << t << "_NP]; sb_M" << t << "(Yd + " << Y0 << ", Md); sb_C" << t
+      << "          if (fl & 2) { sb_C" << t << "(xdv, M, C); for (int m = 0; m < " << DO << "; ++m) C2[m] += C[m]; }\n"
+      << "          if (fl & 4) { float Md[P" << t << "_NP]; sb_M" << t << "(Yd + " << Y0 << ", Md); sb_C" << t
       << "(xv, Md, C); for (int m = 0; m < " << DO << "; ++m) C2[m] += C[m]; }\n"
       << "#pragma unroll\n          for (int q = 0; q < K; ++q)\n#pragma unroll\n"
       << "            for (int m = 0; m < " << DO << "; ++m) acc" << t << "[q * " << DO << " + m] = fmaf(ph[q], C2[m], acc"
       << t << "[q * " << DO << " + m]);\n"
-      << "          if (flags & 1) {\n            sb_C" << t << "(xv, M, C);\n"
+      << "          if (fl & 1) {\n            sb_C" << t << "(xv, M, C);\n"
       << "#pragma unroll\n            for (int q = 0; q < K; ++q)\n#pragma unroll\n"
       << "              for (int m = 0; m < " << DO << "; ++m) acc" << t << "[q * " << DO << " + m] = fmaf(phd[q], C[m], acc"
       << t << "[q * " << DO << " + m]);\n          }\n        }\n      }\n";
@@ -461,98 +462,164 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
   o << "  }\n}\n";
 }
 
-// Backward / double-backward wave unit of one slab.
-void emit_bwd_wave(std::ostringstream& o, const Plan& P, const Unit& u, int s, int w) {
-  const Irrep& ri = P.in[u.a];
-  const int DA = 2 * ri.l + 1, L = unit_lsh(P, u), NS = (L + 1) * (L + 1);
-  const int RW = u.ES > 1 ? u.U : 64;
-  o << "template <bool DB>\nSB_DEV void sb_bw_" << s << "_" << w
-    << "(int lane, int eb, int nb, int e0, const int* __restrict__ sender, const float* __restrict__ evec,"
+// Adjoint (backward / double-backward) code for one slab: every wave runs all
+// items of the slab for the edges it owns (edge k of the block -> wave
+// (k / ES) % 4, sub k % ES).  Per-edge partial sums stay in registers across
+// the slab's paths and are reduced over the channel lanes once per edge.
+void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
+  const AdjSlab& sl = P.slabs[s];
+  const bool first = s == 0, last = s + 1 == (int)P.slabs.size();
+  int L = 0;
+  for (auto& it : sl.items)
+    for (int t : it.paths) L = std::max(L, P.paths[t].l_sh);
+  const int NS = (L + 1) * (L + 1);
+  o << "template <bool DB, int FL>\nSB_DEV void sb_adj_s" << s
+    << "(int w, int lane, int ebase, int nb, int e0, const int* __restrict__ sender, const float* __restrict__ evec,"
        " const float* __restrict__ phi, const float* __restrict__ x, const float* __restrict__ xdot,"
        " const float* __restrict__ evdot, const float* __restrict__ phidot, const float* sS, const float* sS2,"
-       " float* spart, float* __restrict__ contrib, int flags) {\n";
-  o << "  constexpr int U = " << u.U << ", U0 = " << u.U0 << ", ES = " << u.ES << ", CA = " << ri.mul
-    << ", AOFF = " << ri.off << ", RW = " << RW << ";\n"
-    << "  constexpr int NV = DB ? (K + 2 * NSH) : (K + NSH);\n"
-       "  const int sub = lane / U, uu = lane % U, u = U0 + uu;\n"
-       "  const bool act = (lane < ES * U) && (u < CA);\n"
-       "  for (int k0 = 0; k0 < nb; k0 += ES) {\n"
-       "    const int kk = k0 + sub;\n"
-       "    const bool ev = act && kk < nb;\n"
-       "    const int e = eb + kk;\n"
+       " float* sacc, float* __restrict__ gphi, float* __restrict__ gevec, float* __restrict__ contrib, int flags,"
+       " bool multi) {\n"
+    << "  const int fl = FL >= 0 ? FL : flags;\n"
+    << "  constexpr bool HAS_GY = !DB || FL < 0 || (FL & 11);\n"
+       "  constexpr bool HAS_YB = DB && (FL < 0 || (FL & 4));\n"
+       "  constexpr int GY = K, YB = K + (HAS_GY ? NSH : 0);\n"
+       "  constexpr int NV = K + (HAS_GY ? NSH : 0) + (HAS_YB ? NSH : 0);\n"
+       "  constexpr int U = ADJ_U, ES = ADJ_ES;\n"
+       "  const int sub = lane / U, uu = lane % U;\n"
+       "  const int niter = (nb + 4 * ES - 1) / (4 * ES);\n"
+       "  for (int it = 0; it < niter; ++it) {\n"
+       "    const int k = (it * 4 + w) * ES + sub;\n"
+       "    const bool ev = k < nb;\n"
+       "    const int e = ebase + k;\n"
        "    float pv[NV];\n#pragma unroll\n    for (int v = 0; v < NV; ++v) pv[v] = 0.f;\n"
-    << "    float xc[" << DA << "] = {};\n"
-    << "    if (ev) {\n"
+       "    float ux = 0.f, uy = 0.f, uz = 1.f, rinv = 1.f;\n"
+       "    // opaque zero: keeps the adjoint-state reads inside the loop (LDS), instead of\n"
+       "    // hoisting the whole slab into registers\n"
+       "    int zz = 0;\n    asm volatile(\"\" : \"+v\"(zz));\n"
+       "    if (ev) {\n"
        "      const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
-       "      const float rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
-       "      const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
+       "      rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
+       "      ux = vx * rinv; uy = vy * rinv; uz = vz * rinv;\n"
     << "      float Y[" << NS << "];\n      sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
     << "      float ph[K];\n#pragma unroll\n      for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
-       "      const sb_i64 xrow = (sb_i64)sender[e] * CXI + AOFF + u;\n"
-    << "      float xv[" << DA << "];\n#pragma unroll\n      for (int m = 0; m < " << DA << "; ++m) xv[m] = x[xrow + m * CA];\n"
-    << "      float Yd[" << NS << "], phd[K], xdv[" << DA << "];\n"
-    << "      if (DB) {\n"
-       "        if (flags & 4) {\n"
-       "          const float dx = evdot[3 * (sb_i64)e], dy = evdot[3 * (sb_i64)e + 1], dz = evdot[3 * (sb_i64)e + 2];\n"
-    << "          sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n        }\n"
-    << "        if (flags & 1) {\n#pragma unroll\n          for (int q = 0; q < K; ++q) phd[q] = phidot[(sb_i64)e * K + q];\n        }\n"
-    << "        if (flags & 2) {\n#pragma unroll\n          for (int m = 0; m < " << DA << "; ++m) xdv[m] = xdot[xrow + m * CA];\n        }\n"
-    << "      }\n";
-  for (size_t pi = 0; pi < u.paths.size(); ++pi) {
-    const int t = u.paths[pi];
-    const Path& q = P.paths[t];
-    const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
-    const int lo = u.lds_off[pi];
-    o << "      {\n"
-      << "        const float* Sp = sS + " << lo << " + uu;\n"
-      << "        float M[P" << t << "_NP], C[" << DO << "], G[" << DO << "];\n"
-      << "        sb_M" << t << "(Y + " << Y0 << ", M);\n"
-      << "#pragma unroll\n        for (int m = 0; m < " << DO << "; ++m) {\n"
-      << "          float g = 0.f;\n#pragma unroll\n          for (int q = 0; q < K; ++q) g = fmaf(ph[q], Sp[(q * " << DO
-      << " + m) * U], g);\n          G[m] = g;\n        }\n"
-      << "        if (!DB) {\n"
-      << "          sb_C" << t << "(xv, M, C);\n"
-      << "#pragma unroll\n          for (int q = 0; q < K; ++q) {\n            float a = 0.f;\n#pragma unroll\n"
-      << "            for (int m = 0; m < " << DO << "; ++m) a = fmaf(Sp[(q * " << DO << " + m) * U], C[m], a);\n"
-      << "            pv[q] += a;\n          }\n"
-      << "          sb_Y" << t << "(xv, G, pv + K + " << Y0 << ");\n"
-      << "          sb_X" << t << "(G, M, xc);\n"
-      << "        } else {\n"
-      << "          const float* Sp2 = sS2 + " << lo << " + uu;\n"
-      << "          float Gd[" << DO << "] = {}, Cd[" << DO << "] = {};\n"
-      << "          if (flags & 1) {\n#pragma unroll\n            for (int m = 0; m < " << DO << "; ++m) {\n"
-      << "              float g = 0.f;\n#pragma unroll\n              for (int q = 0; q < K; ++q) g = fmaf(phd[q], Sp[(q * " << DO
-      << " + m) * U], g);\n              Gd[m] += g;\n            }\n          }\n"
-      << "          if (flags & 8) {\n#pragma unroll\n            for (int m = 0; m < " << DO << "; ++m) {\n"
-      << "              float g = 0.f;\n#pragma unroll\n              for (int q = 0; q < K; ++q) g = fmaf(ph[q], Sp2[(q * " << DO
-      << " + m) * U], g);\n              Gd[m] += g;\n            }\n          }\n"
-      << "          float Md[P" << t << "_NP];\n"
-      << "          if (flags & 2) { sb_C" << t << "(xdv, M, C); for (int m = 0; m < " << DO << "; ++m) Cd[m] += C[m]; }\n"
-      << "          if (flags & 4) { sb_M" << t << "(Yd + " << Y0 << ", Md); sb_C" << t << "(xv, Md, C); for (int m = 0; m < "
-      << DO << "; ++m) Cd[m] += C[m]; }\n"
-      << "#pragma unroll\n          for (int q = 0; q < K; ++q) {\n            float a = 0.f;\n#pragma unroll\n"
-      << "            for (int m = 0; m < " << DO << "; ++m) a = fmaf(Sp[(q * " << DO << " + m) * U], Cd[m], a);\n"
-      << "            pv[q] += a;\n          }\n"
-      << "          if (flags & 8) {\n            sb_C" << t << "(xv, M, C);\n"
-      << "#pragma unroll\n            for (int q = 0; q < K; ++q) {\n              float a = 0.f;\n#pragma unroll\n"
-      << "              for (int m = 0; m < " << DO << "; ++m) a = fmaf(Sp2[(q * " << DO << " + m) * U], C[m], a);\n"
-      << "              pv[q] += a;\n            }\n          }\n"
-      << "          sb_Y" << t << "(xv, Gd, pv + K + " << Y0 << ");\n"
-      << "          if (flags & 2) sb_Y" << t << "(xdv, G, pv + K + " << Y0 << ");\n"
-      << "          if (flags & 4) sb_Y" << t << "(xv, G, pv + K + NSH + " << Y0 << ");\n"
-      << "          sb_X" << t << "(Gd, M, xc);\n"
-      << "          if (flags & 4) sb_X" << t << "(G, Md, xc);\n"
+    << "      float Yd[" << NS << "], phd[K];\n"
+    << "      if (DB && (fl & 4)) {\n"
+       "        const float dx = evdot[3 * (sb_i64)e], dy = evdot[3 * (sb_i64)e + 1], dz = evdot[3 * (sb_i64)e + 2];\n"
+    << "        sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n      }\n"
+    << "      if (DB && (fl & 1)) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) phd[q] = phidot[(sb_i64)e * K + q];\n      }\n"
+    << "      const sb_i64 srow = (sb_i64)sender[e] * CXI;\n";
+  for (const AdjItem& it : sl.items) {
+    const Irrep& ri = P.in[it.a];
+    const int DA = 2 * ri.l + 1;
+    o << "      {  // input irrep " << it.a << ", channels from " << it.u0 << "\n"
+      << "        constexpr int CA = " << ri.mul << ", AOFF = " << ri.off << ", U0 = " << it.u0 << ", DA = " << DA << ";\n"
+      << "        const int u = U0 + uu;\n"
+      << "        if (u < CA) {\n"
+      << "          float xv[DA], xdv[DA], xc[DA];\n"
+      << "#pragma unroll\n          for (int m = 0; m < DA; ++m) { xv[m] = x[srow + AOFF + m * CA + u]; xc[m] = 0.f; }\n"
+      << "          if (DB && (fl & 2)) {\n#pragma unroll\n            for (int m = 0; m < DA; ++m) xdv[m] = xdot[srow + AOFF + m * CA + u];\n          }\n";
+    for (size_t pi = 0; pi < it.paths.size(); ++pi) {
+      const int t = it.paths[pi];
+      const Path& q = P.paths[t];
+      const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
+      o << "          {  // path " << t << "\n"
+        << "            constexpr int DO = " << DO << ", Y0 = " << Y0 << ";\n"
+        << "            const float* Sp = sS + " << it.lds_off[pi] << " + uu + zz;\n"
+        << "            float M[P" << t << "_NP];\n            sb_M" << t << "(Y + Y0, M);\n"
+        << "            float G[DO];\n#pragma unroll\n            for (int m = 0; m < DO; ++m) G[m] = 0.f;\n"
+        << "            if (!DB) {\n"
+        << "              float C[DO];\n              sb_C" << t << "(xv, M, C);\n"
+        << "#pragma unroll\n              for (int q = 0; q < K; ++q)\n#pragma unroll\n"
+        << "                for (int m = 0; m < DO; ++m) {\n"
+        << "                  const float sv = Sp[(q * DO + m) * U];\n"
+        << "                  G[m] = fmaf(ph[q], sv, G[m]);\n"
+        << "                  pv[q] = fmaf(sv, C[m], pv[q]);\n"
+        << "                }\n"
+        << "              sb_Y" << t << "(xv, G, pv + GY + Y0);\n"
+        << "              sb_X" << t << "(G, M, xc);\n"
+        << "            } else {\n"
+        << "              const float* Sp2 = sS2 + " << it.lds_off[pi] << " + uu + zz;\n"
+        << "              float Md[P" << t << "_NP], Cd[DO], C0[DO], Gd[DO], Ct[DO];\n"
+        << "#pragma unroll\n              for (int m = 0; m < DO; ++m) { Cd[m] = 0.f; Gd[m] = 0.f; }\n"
+        << "              if (fl & 2) { sb_C" << t << "(xdv, M, Ct); for (int m = 0; m < DO; ++m) Cd[m] += Ct[m]; }\n"
+        << "              if (fl & 4) { sb_M" << t << "(Yd + Y0, Md); sb_C" << t
+        << "(xv, Md, Ct); for (int m = 0; m < DO; ++m) Cd[m] += Ct[m]; }\n"
+        << "              if (fl & 8) sb_C" << t << "(xv, M, C0);\n"
+        << "#pragma unroll\n              for (int q = 0; q < K; ++q)\n#pragma unroll\n"
+        << "                for (int m = 0; m < DO; ++m) {\n"
+        << "                  const float sv = Sp[(q * DO + m) * U];\n"
+        << "                  G[m] = fmaf(ph[q], sv, G[m]);\n"
+        << "                  pv[q] = fmaf(sv, Cd[m], pv[q]);\n"
+        << "                  if (fl & 1) Gd[m] = fmaf(phd[q], sv, Gd[m]);\n"
+        << "                  if (fl & 8) {\n"
+        << "                    const float s2 = Sp2[(q * DO + m) * U];\n"
+        << "                    Gd[m] = fmaf(ph[q], s2, Gd[m]);\n"
+        << "                    pv[q] = fmaf(s2, C0[m], pv[q]);\n"
+        << "                  }\n"
+        << "                }\n"
+        << "              if (HAS_GY && (fl & 9)) sb_Y" << t << "(xv, Gd, pv + GY + Y0);\n"
+        << "              if (HAS_GY && (fl & 2)) sb_Y" << t << "(xdv, G, pv + GY + Y0);\n"
+        << "              if (HAS_YB && (fl & 4)) sb_Y" << t << "(xv, G, pv + YB + Y0);\n"
+        << "              if (fl & 9) sb_X" << t << "(Gd, M, xc);\n"
+        << "              if (fl & 4) sb_X" << t << "(G, Md, xc);\n"
+        << "            }\n"
+        << "          }\n";
+    }
+    o << "          if (contrib) {\n"
+      << "            float* cr = contrib + (sb_i64)(e - e0) * CXI + AOFF + u;\n"
+      << "#pragma unroll\n            for (int m = 0; m < DA; ++m) cr[m * CA] = " << (it.first ? "xc[m]" : "cr[m * CA] + xc[m]")
+      << ";\n          }\n"
       << "        }\n      }\n";
+  }
+  if (first) {
+    for (int a : P.dead_in)
+      o << "      if (contrib) for (int t = uu; t < " << P.in[a].dim() << "; t += U) contrib[(sb_i64)(e - e0) * CXI + "
+        << P.in[a].off << " + t] = 0.f;\n";
   }
   o << "    }\n"
        "#pragma unroll\n    for (int v = 0; v < NV; ++v)\n"
-       "      for (int sft = 1; sft < RW; sft <<= 1) pv[v] += __shfl_xor(pv[v], sft);\n"
-       "    if ((lane % RW) == 0 && lane < ES * U && kk < nb) {\n"
-    << "#pragma unroll\n      for (int v = 0; v < NV; ++v) spart[(" << w << " * EB + kk) * NV + v] = pv[v];\n    }\n"
-    << "    if (ev && contrib) {\n"
-       "      float* cr = contrib + (sb_i64)(e - e0) * CXI + AOFF + u;\n"
-    << "#pragma unroll\n      for (int m = 0; m < " << DA << "; ++m) cr[m * CA] = " << (u.first ? "xc[m]" : "cr[m * CA] + xc[m]")
-    << ";\n    }\n  }\n}\n";
+       "      for (int sft = 1; sft < U; sft <<= 1) pv[v] += __shfl_xor(pv[v], sft);\n"
+       "    if (ev && uu == 0) {\n"
+       "      if (multi) {\n"
+       "#pragma unroll\n        for (int v = 0; v < NV; ++v) {\n"
+    << "          float tv = pv[v];\n"
+    << (first ? "" : "          tv += sacc[k * NV + v];\n")
+    << (last ? "          pv[v] = tv;\n" : "          sacc[k * NV + v] = tv;\n")
+    << "        }\n      }\n";
+  if (last) {
+    o << "      if (gphi) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = pv[q];\n      }\n"
+         "      if (gevec) {\n"
+         "        float g[3] = {0.f, 0.f, 0.f};\n"
+         "        if (HAS_GY) sb_sh_vjp(ux, uy, uz, rinv, pv + GY, g);\n"
+         "        if (HAS_YB && (fl & 4)) {\n"
+         "          float h[3];\n"
+         "          sb_sh_hvp(ux, uy, uz, rinv, pv + YB, evdot[3 * (sb_i64)e], evdot[3 * (sb_i64)e + 1],"
+         " evdot[3 * (sb_i64)e + 2], h);\n"
+         "          g[0] += h[0]; g[1] += h[1]; g[2] += h[2];\n"
+         "        }\n"
+         "        gevec[3 * (sb_i64)e] = g[0]; gevec[3 * (sb_i64)e + 1] = g[1]; gevec[3 * (sb_i64)e + 2] = g[2];\n"
+         "      }\n";
+  }
+  o << "    }\n  }\n}\n";
+}
+
+// Staging of one slab's adjoint-state slices (and the second slice set when dA is active).
+void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* indent) {
+  for (const AdjItem& it : P.slabs[s].items)
+    for (size_t pi = 0; pi < it.paths.size(); ++pi) {
+      const Path& q = P.paths[it.paths[pi]];
+      const Group& g = P.groups[q.group];
+      const int DO = 2 * q.l_out + 1, U = P.adj_U, n = P.K * DO * U;
+      o << indent << "for (int t = tid; t < " << n << "; t += 256) {\n"
+        << indent << "  const int q = t / " << DO * U << ", r = t % " << DO * U << ", m = r / " << U << ", uc = " << it.u0
+        << " + r % " << U << ";\n"
+        << indent << "  const sb_i64 src = ncap * " << g.s_off << "LL + ((sb_i64)il * " << g.d << " + m) * " << g.D
+        << "LL + " << q.koff << " + q * " << q.c_in << " + uc;\n"
+        << indent << "  const bool ok = uc < " << q.c_in << ";\n"
+        << indent << "  sS[" << it.lds_off[pi] << " + t] = ok ? Sb[src] : 0.f;\n"
+        << indent << "  if (DB && (fl & 8)) sS2[" << it.lds_off[pi] << " + t] = ok ? Sb2[src] : 0.f;\n"
+        << indent << "}\n";
+    }
 }
 
 }  // namespace
@@ -566,15 +633,17 @@ std::string generate_source(const Plan& P) {
   for (auto& r : P.out) o << r.mul << "x" << r.l << (r.p > 0 ? "e" : "o") << " ";
   o << "norm=" << P.norm << "\n";
   o << "#define K " << P.K << "\n#define NSH " << P.nsh << "\n#define CXI " << P.dim_in << "\n#define CXO " << P.dim_out
-    << "\n#define EB " << P.bwd_eb << "\n";
+    << "\n#define EB " << P.bwd_eb << "\n#define ADJ_U " << P.adj_U << "\n#define ADJ_ES " << P.adj_ES << "\n";
   emit_sh(o, P.lmax);
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
 
   // forward S / dS kernels: one wave per (receiver, unit)
   for (int t = 0; t < (int)P.fwd_units.size(); ++t) emit_fwd_unit(o, P, P.fwd_units[t], t);
   const int NU = (int)P.fwd_units.size();
-  for (int tan = 0; tan < 2; ++tan) {
-    o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_fwd_" << (tan ? "dS" : "S")
+  struct FV { const char* name; bool tan; int fl; };
+  const FV fvs[] = {{"S", false, 0}, {"dS_r", true, 4}, {"dS", true, -1}};
+  for (const FV& fv : fvs) {
+    o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_fwd_" << fv.name
       << "(const int* __restrict__ rowptr, const int* __restrict__ sender, const float* __restrict__ evec,"
          " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, int r0, int n_recv,"
          " sb_i64 ncap, const float* __restrict__ xdot, const float* __restrict__ evdot,"
@@ -585,104 +654,63 @@ std::string generate_source(const Plan& P) {
          "  const int beg = rowptr[r0 + il], end = rowptr[r0 + il + 1];\n"
          "  switch (t) {\n";
     for (int t = 0; t < NU; ++t)
-      o << "    case " << t << ": sb_fwd_u" << t << "<" << (tan ? "true" : "false")
+      o << "    case " << t << ": sb_fwd_u" << t << "<" << (fv.tan ? "true" : "false") << ", " << fv.fl
         << ">(lane, il, beg, end, sender, evec, phi, x, S, ncap, xdot, evdot, phidot, flags); break;\n";
     o << "  }\n}\n";
   }
 
-  // backward / double-backward edge kernels: one block per receiver, slabs of
-  // adjoint state staged in LDS, per-edge partials reduced in a fixed order
-  for (int s = 0; s < (int)P.slabs.size(); ++s)
-    for (int w = 0; w < (int)P.slabs[s].waves.size(); ++w)
-      if (P.slabs[s].waves[w].a >= 0) emit_bwd_wave(o, P, P.slabs[s].waves[w], s, w);
+  // adjoint edge kernels: one block per receiver, adjoint state staged in LDS
+  // slab by slab, every wave owning a disjoint set of the receiver's edges
+  for (int s = 0; s < (int)P.slabs.size(); ++s) emit_adj_slab(o, P, s);
   const int LDSF = std::max(1, P.bwd_lds_max);
-  o << "template <bool DB>\nSB_DEV void sb_edge_body(const int* __restrict__ rowptr, const int* __restrict__ sender,"
+  const int NSL = (int)P.slabs.size();
+  o << "template <bool DB, int FL>\nSB_DEV void sb_adj_body(const int* __restrict__ rowptr, const int* __restrict__ sender,"
        " const float* __restrict__ evec, const float* __restrict__ phi, const float* __restrict__ x,"
        " const float* __restrict__ Sb, const float* __restrict__ Sb2, const float* __restrict__ xdot,"
        " const float* __restrict__ evdot, const float* __restrict__ phidot, float* __restrict__ gphi,"
        " float* __restrict__ gevec, float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags,"
-       " float* sS, float* sS2, float* sacc, float* spart) {\n"
-    << "  constexpr int NV = DB ? (K + 2 * NSH) : (K + NSH);\n"
+       " float* sS, float* sS2, float* sacc) {\n"
        "  const int il = blockIdx.x;\n"
        "  if (il >= n_recv) return;\n"
-       "  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;\n"
-       "  const int beg = rowptr[r0 + il], end = rowptr[r0 + il + 1];\n"
-       "  for (int eb = beg; eb < end; eb += EB) {\n"
-       "    const int nb = min(EB, end - eb);\n"
-       "    for (int t = tid; t < EB * NV; t += 256) sacc[t] = 0.f;\n";
-  for (int s = 0; s < (int)P.slabs.size(); ++s) {
-    const Slab& sl = P.slabs[s];
-    o << "    // slab " << s << "\n    __syncthreads();\n";
-    for (int w = 0; w < (int)sl.waves.size(); ++w) {
-      const Unit& u = sl.waves[w];
-      if (u.a < 0) continue;
-      for (size_t pi = 0; pi < u.paths.size(); ++pi) {
-        const Path& q = P.paths[u.paths[pi]];
-        const Group& g = P.groups[q.group];
-        const int DO = 2 * q.l_out + 1, n = P.K * DO * u.U;
-        o << "    for (int t = tid; t < " << n << "; t += 256) {\n"
-          << "      const int q = t / " << DO * u.U << ", r = t % " << DO * u.U << ", m = r / " << u.U << ", uu = r % "
-          << u.U << ";\n"
-          << "      const int uc = " << u.U0 << " + uu;\n"
-          << "      const sb_i64 src = ncap * " << g.s_off << "LL + ((sb_i64)il * " << g.d << " + m) * " << g.D << "LL + "
-          << q.koff << " + q * " << q.c_in << " + uc;\n"
-          << "      sS[" << u.lds_off[pi] << " + t] = (uc < " << q.c_in << ") ? Sb[src] : 0.f;\n"
-          << "      if (DB && (flags & 8)) sS2[" << u.lds_off[pi] << " + t] = (uc < " << q.c_in << ") ? Sb2[src] : 0.f;\n"
-          << "    }\n";
-      }
+       "  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;\n"
+       "  const int fl = FL >= 0 ? FL : flags;\n"
+       "  const int beg = rowptr[r0 + il], end = rowptr[r0 + il + 1];\n";
+  if (NSL == 1) {
+    emit_adj_stage(o, P, 0, "  ");
+    o << "  __syncthreads();\n"
+         "  sb_adj_s0<DB, FL>(w, lane, beg, end - beg, e0, sender, evec, phi, x, xdot, evdot, phidot, sS, sS2, sacc, gphi,"
+         " gevec, contrib, flags, false);\n";
+  } else {
+    o << "  for (int eb = beg; eb < end; eb += EB) {\n"
+         "    const int nb = min(EB, end - eb);\n";
+    for (int s = 0; s < NSL; ++s) {
+      o << "    __syncthreads();\n";
+      emit_adj_stage(o, P, s, "    ");
+      o << "    __syncthreads();\n"
+        << "    sb_adj_s" << s << "<DB, FL>(w, lane, eb, nb, e0, sender, evec, phi, x, xdot, evdot, phidot, sS, sS2, sacc,"
+           " gphi, gevec, contrib, flags, true);\n";
     }
-    o << "    __syncthreads();\n    switch (wave) {\n";
-    for (int w = 0; w < (int)sl.waves.size(); ++w)
-      if (sl.waves[w].a >= 0)
-        o << "      case " << w << ": sb_bw_" << s << "_" << w
-          << "<DB>(lane, eb, nb, e0, sender, evec, phi, x, xdot, evdot, phidot, sS, sS2, spart, contrib, flags); break;\n";
-    o << "      default: break;\n    }\n    __syncthreads();\n"
-      << "    for (int t = tid; t < nb * NV; t += 256) {\n      float s = 0.f;\n";
-    for (int w = 0; w < (int)sl.waves.size(); ++w)
-      if (sl.waves[w].a >= 0) o << "      s += spart[" << w << " * EB * NV + t];\n";
-    o << "      sacc[t] += s;\n    }\n";
+    o << "  }\n";
   }
-  o << "    __syncthreads();\n";
-  // zero contributions of input irreps that no path reads
-  for (int a : P.dead_in) {
-    o << "    if (contrib) for (int t = tid; t < nb * " << P.in[a].dim() << "; t += 256)\n"
-      << "      contrib[(sb_i64)(eb + t / " << P.in[a].dim() << " - e0) * CXI + " << P.in[a].off << " + t % "
-      << P.in[a].dim() << "] = 0.f;\n";
-  }
-  o << "    if (tid < nb) {\n"
-       "      const int e = eb + tid;\n"
-       "      const float* a = sacc + tid * NV;\n"
-       "      if (gphi) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = a[q];\n      }\n"
-       "      if (gevec) {\n"
-       "        const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
-       "        const float rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
-       "        const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
-       "        float g[3];\n"
-       "        sb_sh_vjp(ux, uy, uz, rinv, a + K, g);\n"
-       "        if (DB && (flags & 4)) {\n"
-       "          float h[3];\n"
-       "          sb_sh_hvp(ux, uy, uz, rinv, a + K + NSH, evdot[3 * (sb_i64)e], evdot[3 * (sb_i64)e + 1],"
-       " evdot[3 * (sb_i64)e + 2], h);\n"
-       "          g[0] += h[0]; g[1] += h[1]; g[2] += h[2];\n"
-       "        }\n"
-       "        gevec[3 * (sb_i64)e] = g[0]; gevec[3 * (sb_i64)e + 1] = g[1]; gevec[3 * (sb_i64)e + 2] = g[2];\n"
-       "      }\n"
-       "    }\n"
-       "    __syncthreads();\n"
-       "  }\n}\n";
-  for (int db = 0; db < 2; ++db) {
-    o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_" << (db ? "dbwd" : "bwd")
-      << "_E(const int* __restrict__ rowptr, const int* __restrict__ sender, const float* __restrict__ evec,"
+  o << "}\n";
+  o << "#define SB_ADJ_NV(DB, FL) (K + ((!(DB) || (FL) < 0 || ((FL) & 11)) ? NSH : 0) + (((DB) && ((FL) < 0 || ((FL) & 4))) ? NSH : 0))\n";
+  struct KV { const char* name; bool db; int fl; int lds_mult; };
+  const KV kvs[] = {{"sobek_bwd_E", false, 0, 1}, {"sobek_dbwd_E_r", true, 4, 1}, {"sobek_dbwd_E", true, -1, 2}};
+  for (const KV& kv : kvs) {
+    o << "extern \"C\" __global__ __launch_bounds__(256) void " << kv.name
+      << "(const int* __restrict__ rowptr, const int* __restrict__ sender, const float* __restrict__ evec,"
          " const float* __restrict__ phi, const float* __restrict__ x, const float* __restrict__ Sb,"
          " const float* __restrict__ Sb2, const float* __restrict__ xdot, const float* __restrict__ evdot,"
          " const float* __restrict__ phidot, float* __restrict__ gphi, float* __restrict__ gevec,"
          " float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags) {\n"
-      << "  constexpr int NV = " << (db ? "K + 2 * NSH" : "K + NSH") << ";\n"
-      << "  __shared__ float sS[" << LDSF * (db ? 2 : 1) << "];\n"
-      << "  __shared__ float sacc[EB * NV];\n  __shared__ float spart[4 * EB * NV];\n"
-      << "  sb_edge_body<" << (db ? "true" : "false")
+      << "  __shared__ float sS[" << LDSF * kv.lds_mult << "];\n";
+    if (NSL > 1)
+      o << "  __shared__ float sacc[EB * SB_ADJ_NV(" << (kv.db ? "true" : "false") << ", " << kv.fl << ")];\n";
+    else
+      o << "  float* sacc = nullptr;\n";
+    o << "  sb_adj_body<" << (kv.db ? "true" : "false") << ", " << kv.fl
       << ">(rowptr, sender, evec, phi, x, Sb, Sb2, xdot, evdot, phidot, gphi, gevec, contrib, r0, n_recv, ncap, e0,"
-         " flags, sS, sS + " << (db ? LDSF : 0) << ", sacc, spart);\n}\n";
+         " flags, sS, sS + " << (kv.lds_mult == 2 ? LDSF : 0) << ", sacc);\n}\n";
   }
   return o.str();
 }

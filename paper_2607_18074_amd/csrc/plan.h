@@ -40,26 +40,36 @@ struct Group {
   int64_t ktab_off;  // offset of this group's k-table in Plan::ktab
 };
 
-// A wave's share of an edge kernel: input irrep a, channel block [U0, U0 + U)
-// of the input multiplicity, ES edges in flight per wave (lane = sub * U + u),
-// and the list of paths (all with input a).
+// A wave's share of the forward state kernel: input irrep a, channel block
+// [U0, U0 + U) of the input multiplicity, ES edges in flight per wave
+// (lane = sub * U + u), and the list of paths (all with input a).
 struct Unit {
   int a;
   int U, U0, ES;
   std::vector<int> paths;
-  bool first = true;   // backward only: first slab that writes (a, U0) contributions
-  std::vector<int> lds_off;  // backward only: LDS offset of each path's Sbar slice
 };
 
-// Backward slab: wave units whose adjoint state slices are staged in LDS together.
-struct Slab {
-  std::vector<Unit> waves;
-  int lds_floats = 0;
+// Adjoint edge kernels: one lane mapping for the whole plan (lane = sub * adj_U + uu,
+// adj_ES = 64 / adj_U edges in flight per wave); every wave owns a disjoint set of
+// edges and runs every item of a slab for them.  An item is (input irrep a,
+// channel block starting at u0, paths with input a); its adjoint-state slices are
+// staged in LDS as [path][q][m_o][uu].
+struct AdjItem {
+  int a, u0;
+  std::vector<int> paths;
+  bool first = true;          // first slab that writes (a, u0) contributions
+  std::vector<int> lds_off;   // LDS offset (floats) of each path's slice
+};
+
+struct AdjSlab {
+  std::vector<AdjItem> items;
+  int floats = 0;
 };
 
 struct Kernels {
   hipModule_t module = nullptr;
-  hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, bwd_E = nullptr, dbwd_E = nullptr;
+  hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, fwd_dS_r = nullptr;
+  hipFunction_t bwd_E = nullptr, dbwd_E = nullptr, dbwd_E_r = nullptr;
   hipFunction_t gemm_sa[3] = {}, gemm_sbar[3] = {}, gemm_ga[3] = {};  // BN = 16, 32, 64
   hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
                 zero = nullptr;
@@ -75,8 +85,9 @@ struct Plan {
   int64_t srow = 0;  // floats of receiver state per receiver (sum over groups of d * D)
   std::vector<int32_t> ktab;   // host copy of all groups' k-tables
   std::vector<Unit> fwd_units;
-  std::vector<Slab> slabs;
-  int bwd_eb = 32;              // edges per batch in the backward edge kernel
+  int adj_U = 64, adj_ES = 1;   // adjoint lane mapping
+  std::vector<AdjSlab> slabs;
+  int bwd_eb = 64;              // edges per batch when the adjoint state needs several slabs
   int bwd_lds_max = 0;          // largest slab (floats)
   std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
   std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)
