@@ -169,7 +169,8 @@ struct Chunk {
 
 struct WsPlan {
   // byte offsets
-  size_t off_x = 0, off_gout = 0, off_tgx = 0, off_out = 0, off_gx = 0, off_P = 0, off_state = 0, off_contrib = 0;
+  size_t off_x = 0, off_gout = 0, off_tgx = 0, off_out = 0, off_gx = 0, off_cursor = 0, off_P = 0, off_state = 0,
+         off_contrib = 0;
   size_t fixed = 0;
   int nstate = 0;
   int64_t ncap = 0, ecap = 0;
@@ -180,9 +181,9 @@ struct WsPlan {
 int gemm_bn(int C) { return C <= 16 ? 16 : (C <= 32 ? 32 : 64); }
 int bn_index(int bn) { return bn == 16 ? 0 : (bn == 32 ? 1 : 2); }
 
-int nsplit_for(const sobek::Group& g, int64_t nrows) {
+int nsplit_for(const sobek::Group& g, int64_t nrows, bool vec4) {
   int bn = gemm_bn(g.C);
-  int64_t tiles = (int64_t)cdiv(g.D, 64) * cdiv(g.C, bn);
+  int64_t tiles = (int64_t)cdiv(g.D, vec4 ? 128 : 64) * cdiv(g.C, bn);
   int64_t ns = (512 + tiles - 1) / tiles;
   ns = std::max<int64_t>(1, std::min<int64_t>(ns, 64));
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, nrows / 64));
@@ -191,7 +192,7 @@ int nsplit_for(const sobek::Group& g, int64_t nrows) {
 
 size_t partial_floats(const Plan& p, int64_t ncap) {
   size_t m = 0;
-  for (auto& g : p.groups) m = std::max(m, (size_t)nsplit_for(g, ncap * g.d) * g.D * g.C);
+  for (auto& g : p.groups) m = std::max(m, (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C);
   return m;
 }
 
@@ -207,6 +208,7 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, WsPlan& w, size
     if (pass >= SOBEK_PASS_BWD) { w.off_gout = take(no); w.off_gx = take(nx); }
     if (pass == SOBEK_PASS_DBWD) w.off_tgx = take(nx);
   }
+  if (pass != SOBEK_PASS_FWD) w.off_cursor = take((size_t)(G.N + 1) * 4);  // per-sender chunk cursors
   w.off_P = o;  // partials, sized once the chunk capacity is known
   w.fixed = o;
   // receiver-state slots: one, reused phase by phase (S, then Sbar); the double
@@ -335,8 +337,12 @@ int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, const float* S, cons
     const float* Sg = S + (size_t)w.ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     int bn = gemm_bn(g.C);
-    LAUNCH(p.k.gemm_sa[bn_index(bn)], cdiv(nrows, 64), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
-           (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
+    if (p.vec4)
+      LAUNCH(p.k.gemm_sa_v[bn_index(bn)], cdiv(nrows, 128), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
+             (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
+    else
+      LAUNCH(p.k.gemm_sa[bn_index(bn)], cdiv(nrows, 64), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
+             (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
   }
   return SOBEK_OK;
 }
@@ -347,8 +353,12 @@ int run_sbar(const Plan& p, const Chunk& c, const WsPlan& w, const float* M, con
   for (auto& g : p.groups) {
     float* Sg = Sbar + (size_t)w.ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
-    LAUNCH(p.k.gemm_sbar[2], cdiv(nrows, 64), cdiv(D, 64), 1, s, M, nrows, D, W,
-           (const int*)(p.d_ktab + g.ktab_off), Sg, dg, Cg, off, CX, r0);
+    if (p.vec4)
+      LAUNCH(p.k.gemm_sbar_v, cdiv(nrows, 128), cdiv(D, 64), 1, s, M, nrows, D, W,
+             (const int*)(p.d_ktab + g.ktab_off), Sg, dg, Cg, off, CX, r0);
+    else
+      LAUNCH(p.k.gemm_sbar[2], cdiv(nrows, 64), cdiv(D, 64), 1, s, M, nrows, D, W,
+             (const int*)(p.d_ktab + g.ktab_off), Sg, dg, Cg, off, CX, r0);
   }
   return SOBEK_OK;
 }
@@ -360,21 +370,27 @@ int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float
   for (auto& g : p.groups) {
     const float* Sg = S + (size_t)w.ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
-    int ns = nsplit_for(g, (int64_t)w.ncap * g.d);
-    int rps = (int)(((int64_t)cdiv(nrows, ns) + 15) / 16 * 16);
+    int ns = nsplit_for(g, (int64_t)w.ncap * g.d, p.vec4);
+    int rps = (int)(((int64_t)cdiv(nrows, ns) + 31) / 32 * 32);
     int bn = gemm_bn(g.C);
-    LAUNCH(p.k.gemm_ga[bn_index(bn)], cdiv(D, 64), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0, rps);
+    if (p.vec4)
+      LAUNCH(p.k.gemm_ga_v[bn_index(bn)], cdiv(D, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
+             rps);
+    else
+      LAUNCH(p.k.gemm_ga[bn_index(bn)], cdiv(D, 64), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
+             rps);
     LAUNCH(p.k.ga_reduce, cdiv((int64_t)D * Cg, 256), 1, 1, s, (const float*)P, ns, D, Cg,
            (const int*)(p.d_ktab + g.ktab_off), gW, first);
   }
   return SOBEK_OK;
 }
 
-int run_sender_reduce(const Plan& p, const sobek_graph_s& G, const Chunk& c, const float* contrib, float* gx,
-                      int first, hipStream_t s) {
+int run_sender_reduce(const Plan& p, const sobek_graph_s& G, const Chunk& c, const WsPlan& w, void* ws,
+                      const float* contrib, float* gx, int first, hipStream_t s) {
   int N = (int)G.N, CX = p.dim_in, e0 = (int)c.e0, e1 = (int)c.e1;
+  int* cursor = (int*)((char*)ws + w.off_cursor);
   LAUNCH(p.k.sender_reduce, cdiv(G.N, 4), 1, 1, s, (const int*)G.send_rowptr, (const int*)G.send_perm, contrib, gx,
-         N, CX, e0, e1, first);
+         cursor, N, CX, e0, e1, first);
   return SOBEK_OK;
 }
 
@@ -433,11 +449,14 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
     return rc;
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
-                ga = std::string("sobek_gemm_ga_") + bns[b];
+                ga = std::string("sobek_gemm_ga_") + bns[b], sav = std::string("sobek_gemm_sa_v") + bns[b],
+                gav = std::string("sobek_gemm_ga_v") + bns[b];
     if ((rc = get(p.k.gemm_sa[b], sa.c_str())) || (rc = get(p.k.gemm_sbar[b], sb.c_str())) ||
-        (rc = get(p.k.gemm_ga[b], ga.c_str())))
+        (rc = get(p.k.gemm_ga[b], ga.c_str())) || (rc = get(p.k.gemm_sa_v[b], sav.c_str())) ||
+        (rc = get(p.k.gemm_ga_v[b], gav.c_str())))
       return rc;
   }
+  if ((rc = get(p.k.gemm_sbar_v, "sobek_gemm_sbar_v"))) return rc;
   HIPCHK(hipMalloc(&p.d_ktab, std::max<size_t>(4, p.ktab.size() * 4)));
   HIPCHK(hipMemcpy(p.d_ktab, p.ktab.data(), p.ktab.size() * 4, hipMemcpyHostToDevice));
   auto blocks = [](const std::vector<sobek::Irrep>& v) {
@@ -734,7 +753,7 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
       LAUNCH(p.k.bwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
              (const float*)Sb, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
              (const float*)nullptr, gphi, gevec, contrib, r0, n, ncap, e0, flags);
-      if (gx && (rc = run_sender_reduce(p, G, c, contrib, gxk, ci == 0, stream))) return rc;
+      if (gx && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
     }
   }
   if (mulir && gx && (rc = transpose(p, gxk, gx, G.N, true, 1, stream))) return rc;
@@ -803,7 +822,7 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const fl
       int fl = flags;
       LAUNCH(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
              (const float*)Sb, (const float*)Sb2, txk, t_gevec, t_gphi, g_phi, g_evec, contrib, r0, n, ncap, e0, fl);
-      if (g_x && (rc = run_sender_reduce(p, G, c, contrib, gxk, ci == 0, stream))) return rc;
+      if (g_x && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
     }
   }
   if (g_gout && (rc = zero_dead_out(p, ggk, G.N, stream))) return rc;

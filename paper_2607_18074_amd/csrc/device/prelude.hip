@@ -189,6 +189,286 @@ SB_GEMM_ENTRY(16)
 SB_GEMM_ENTRY(32)
 SB_GEMM_ENTRY(64)
 
+// ---------------------------------------------------------------------------
+// Vectorised channel GEMMs (every multiplicity a multiple of 4, so rows of S,
+// W and the node tensors are 16-byte aligned): 128-row tiles (4 waves x 32
+// rows), BK = 32, float4 global loads, and the next tile prefetched into
+// registers while the MFMAs consume the current one from LDS.
+// ---------------------------------------------------------------------------
+#define SB_VM 128
+#define SB_VK 32
+
+typedef float sb_v4 __attribute__((ext_vector_type(4)));
+
+SB_DEV sb_v4 sb_ld4(const float* p) { return *(const sb_v4*)p; }
+
+// out rows (r0 + r / dg, r % dg) (+)= S[r, :] A_g, S row-major with row length D
+template <int BN>
+SB_DEV void sb_gemm_sa_v(const float* __restrict__ S, int nrows, int D, const float* __restrict__ W,
+                         const int* __restrict__ ktab, float* __restrict__ out, int dg, int Cg, int off, int CX,
+                         int r0, int accumulate) {
+  __shared__ float sA[SB_VK][SB_VM + 4];
+  __shared__ float sB[SB_VK][BN + 4];
+  constexpr int NB = (SB_VK * BN / 4 + 255) / 256;  // float4 loads of B per thread
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int rb = blockIdx.x * SB_VM, cb = blockIdx.y * BN;
+  sb_f4 acc[2][BN / 16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t) acc[i][t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  sb_v4 ra[4], rbv[NB];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (tid >> 3) + 32 * i, k = k0 + 4 * (tid & 7);
+      const int gr = rb + row;
+      ra[i] = (gr < nrows && k < D) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      const int kk = idx / (BN / 4), c = 4 * (idx % (BN / 4));
+      const int gk = k0 + kk;
+      rbv[i] = (idx < SB_VK * BN / 4 && gk < D && cb + c < Cg) ? sb_ld4(W + (sb_i64)ktab[gk] + cb + c)
+                                                                : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (tid >> 3) + 32 * i, kq = 4 * (tid & 7);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) sA[kq + c][row] = ra[i][c];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < SB_VK * BN / 4) *(sb_v4*)&sB[idx / (BN / 4)][4 * (idx % (BN / 4))] = rbv[i];
+    }
+  };
+  load(0);
+  store();
+  __syncthreads();
+  for (int k0 = 0; k0 < D; k0 += SB_VK) {
+    const bool more = k0 + SB_VK < D;
+    if (more) load(k0 + SB_VK);
+#pragma unroll
+    for (int kk = 0; kk < SB_VK; kk += 4) {
+      const float a0 = sA[kk + (lane >> 4)][32 * wave + (lane & 15)];
+      const float a1 = sA[kk + (lane >> 4)][32 * wave + 16 + (lane & 15)];
+#pragma unroll
+      for (int t = 0; t < BN / 16; ++t) {
+        const float b = sB[kk + (lane >> 4)][16 * t + (lane & 15)];
+        acc[0][t] = sb_mfma(a0, b, acc[0][t]);
+        acc[1][t] = sb_mfma(a1, b, acc[1][t]);
+      }
+    }
+    __syncthreads();
+    if (more) {
+      store();
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb + 32 * wave + 16 * i + 4 * (lane >> 4) + r;
+        const int col = cb + 16 * t + (lane & 15);
+        if (row < nrows && col < Cg) {
+          float* o = out + sb_row_addr(row, dg, Cg, off, CX, r0) + col;
+          *o = accumulate ? (*o + acc[i][t][r]) : acc[i][t][r];
+        }
+      }
+}
+
+// Sbar[r, k] = sum_w mbar(r, w) A_g[k, w]; 128 rows x 64 k-columns per block, reduction over w
+SB_DEV void sb_gemm_sbar_v(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
+                           const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int Cg, int off, int CX,
+                           int r0) {
+  constexpr int BN = 64;
+  __shared__ float sA[SB_VK][SB_VM + 4];
+  __shared__ float sB[SB_VK][BN + 4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int rb = blockIdx.x * SB_VM, kb = blockIdx.y * BN;
+  sb_f4 acc[2][BN / 16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t) acc[i][t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  sb_v4 ra[4], rbv[2];
+  auto load = [&](int w0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (tid >> 3) + 32 * i, w = w0 + 4 * (tid & 7);
+      const int gr = rb + row;
+      ra[i] = (gr < nrows && w < Cg) ? sb_ld4(M + sb_row_addr(gr, dg, Cg, off, CX, r0) + w)
+                                     : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int kc = (tid >> 3) + 32 * i, w = w0 + 4 * (tid & 7);
+      const int gk = kb + kc;
+      rbv[i] = (gk < D && w < Cg) ? sb_ld4(W + (sb_i64)ktab[gk] + w) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (tid >> 3) + 32 * i, wq = 4 * (tid & 7);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) sA[wq + c][row] = ra[i][c];
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int kc = (tid >> 3) + 32 * i, wq = 4 * (tid & 7);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) sB[wq + c][kc] = rbv[i][c];
+    }
+  };
+  load(0);
+  store();
+  __syncthreads();
+  for (int w0 = 0; w0 < Cg; w0 += SB_VK) {
+    const bool more = w0 + SB_VK < Cg;
+    if (more) load(w0 + SB_VK);
+#pragma unroll
+    for (int kk = 0; kk < SB_VK; kk += 4) {
+      const float a0 = sA[kk + (lane >> 4)][32 * wave + (lane & 15)];
+      const float a1 = sA[kk + (lane >> 4)][32 * wave + 16 + (lane & 15)];
+#pragma unroll
+      for (int t = 0; t < BN / 16; ++t) {
+        const float b = sB[kk + (lane >> 4)][16 * t + (lane & 15)];
+        acc[0][t] = sb_mfma(a0, b, acc[0][t]);
+        acc[1][t] = sb_mfma(a1, b, acc[1][t]);
+      }
+    }
+    __syncthreads();
+    if (more) {
+      store();
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb + 32 * wave + 16 * i + 4 * (lane >> 4) + r;
+        const int col = kb + 16 * t + (lane & 15);
+        if (row < nrows && col < D) Sbar[(sb_i64)row * D + col] = acc[i][t][r];
+      }
+}
+
+// P[split, k, w] = sum_{r in split} S[r, k] mbar(r, w); 128 k-rows x BN columns per block
+template <int BN>
+SB_DEV void sb_gemm_ga_v(const float* __restrict__ S, int nrows, int D, const float* __restrict__ M,
+                         float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split) {
+  __shared__ float sA[SB_VK][SB_VM + 4];
+  __shared__ float sB[SB_VK][BN + 4];
+  constexpr int NB = (SB_VK * BN / 4 + 255) / 256;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int kb = blockIdx.x * SB_VM, cb = blockIdx.y * BN, split = blockIdx.z;
+  const int rbeg = split * rows_per_split;
+  const int rend = min(nrows, rbeg + rows_per_split);
+  sb_f4 acc[2][BN / 16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t) acc[i][t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  sb_v4 ra[4], rbv[NB];
+  auto load = [&](int rr0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = (tid >> 5) + 8 * i, k = kb + 4 * (tid & 31);
+      const int gr = rr0 + rr;
+      ra[i] = (gr < rend && k < D) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      const int rr = idx / (BN / 4), c = 4 * (idx % (BN / 4));
+      const int gr = rr0 + rr;
+      rbv[i] = (idx < SB_VK * BN / 4 && gr < rend && cb + c < Cg)
+                   ? sb_ld4(M + sb_row_addr(gr, dg, Cg, off, CX, r0) + cb + c)
+                   : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = (tid >> 5) + 8 * i;
+      *(sb_v4*)&sA[rr][4 * (tid & 31)] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < SB_VK * BN / 4) *(sb_v4*)&sB[idx / (BN / 4)][4 * (idx % (BN / 4))] = rbv[i];
+    }
+  };
+  if (rbeg < rend) {
+    load(rbeg);
+    store();
+  }
+  __syncthreads();
+  for (int rr0 = rbeg; rr0 < rend; rr0 += SB_VK) {
+    const bool more = rr0 + SB_VK < rend;
+    if (more) load(rr0 + SB_VK);
+#pragma unroll
+    for (int kk = 0; kk < SB_VK; kk += 4) {
+      const float a0 = sA[kk + (lane >> 4)][32 * wave + (lane & 15)];
+      const float a1 = sA[kk + (lane >> 4)][32 * wave + 16 + (lane & 15)];
+#pragma unroll
+      for (int t = 0; t < BN / 16; ++t) {
+        const float b = sB[kk + (lane >> 4)][16 * t + (lane & 15)];
+        acc[0][t] = sb_mfma(a0, b, acc[0][t]);
+        acc[1][t] = sb_mfma(a1, b, acc[1][t]);
+      }
+    }
+    __syncthreads();
+    if (more) {
+      store();
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int k = kb + 32 * wave + 16 * i + 4 * (lane >> 4) + r;
+        const int col = cb + 16 * t + (lane & 15);
+        if (k < D && col < Cg) P[((sb_i64)split * D + k) * Cg + col] = acc[i][t][r];
+      }
+}
+
+#define SB_GEMM_V_ENTRY(BN)                                                                          \
+  extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sa_v##BN(                            \
+      const float* S, int nrows, int D, const float* W, const int* ktab, float* out, int dg,       \
+      int Cg, int off, int CX, int r0, int accumulate) {                                           \
+    sb_gemm_sa_v<BN>(S, nrows, D, W, ktab, out, dg, Cg, off, CX, r0, accumulate);                  \
+  }                                                                                                \
+  extern "C" __global__ __launch_bounds__(256) void sobek_gemm_ga_v##BN(                            \
+      const float* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \
+      int r0, int rows_per_split) {                                                                \
+    sb_gemm_ga_v<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split);                      \
+  }
+
+SB_GEMM_V_ENTRY(16)
+SB_GEMM_V_ENTRY(32)
+SB_GEMM_V_ENTRY(64)
+
+extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sbar_v(const float* M, int nrows, int D, const float* W,
+                                                                    const int* ktab, float* Sbar, int dg, int Cg,
+                                                                    int off, int CX, int r0) {
+  sb_gemm_sbar_v(M, nrows, D, W, ktab, Sbar, dg, Cg, off, CX, r0);
+}
+
 // gW[ktab[k] + w] = (first ? 0 : gW[..]) + sum_{s < nsplit} P[s, k, w]   (fixed split order)
 extern "C" __global__ __launch_bounds__(256) void sobek_ga_reduce(const float* P, int nsplit, int D, int Cg,
                                                                   const int* ktab, float* gW, int first) {
@@ -203,31 +483,43 @@ extern "C" __global__ __launch_bounds__(256) void sobek_ga_reduce(const float* P
 
 // One wave per sender j: x-gradient rows are the sum, in sender-CSR order, of the
 // per-edge contribution rows of its out-edges inside the receiver chunk [e0, e1)
-// (contributions are stored at row e - e0).  first: chunk 0 overwrites every row.
+// (contributions are stored at row e - e0).  Chunks arrive in increasing edge
+// order, so each sender's edges inside a chunk continue where the previous chunk
+// stopped: cursor[j] keeps that position.  first: chunk 0 overwrites every row
+// and initialises the cursors.
 extern "C" __global__ __launch_bounds__(256) void sobek_sender_reduce(const int* send_rowptr, const int* send_perm,
-                                                                      const float* contrib, float* gx, int N,
-                                                                      int CX, int e0, int e1, int first) {
-  int j = blockIdx.x * 4 + (threadIdx.x >> 6);
-  int lane = threadIdx.x & 63;
+                                                                      const float* contrib, float* gx, int* cursor,
+                                                                      int N, int CX, int e0, int e1, int first) {
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (j >= N) return;
-  int b = send_rowptr[j], e = send_rowptr[j + 1];
-  int lo = b, hi = e;
-  while (lo < hi) {  // first position with edge id >= e0
-    int mid = (lo + hi) >> 1;
-    if (send_perm[mid] < e0) lo = mid + 1; else hi = mid;
+  const int start = first ? send_rowptr[j] : cursor[j];
+  const int lim = send_rowptr[j + 1];
+  // the chunk's edges of this sender form a prefix of [start, lim): find its length
+  int n = 0;
+  for (;;) {
+    const int p = start + n + lane;
+    const bool in = p < lim && send_perm[p] < e1;
+    const unsigned long long m = __ballot(in);
+    const int cnt = __popcll(m);
+    n += cnt;
+    if (cnt < 64) break;
   }
-  int start = lo;
-  hi = e;
-  while (lo < hi) {  // first position with edge id >= e1
-    int mid = (lo + hi) >> 1;
-    if (send_perm[mid] < e1) lo = mid + 1; else hi = mid;
-  }
-  int stop = lo;
-  if (!first && start == stop) return;
-  for (int c = lane; c < CX; c += 64) {
-    float s = first ? 0.f : gx[(sb_i64)j * CX + c];
-    for (int p = start; p < stop; ++p) s += contrib[(sb_i64)(send_perm[p] - e0) * CX + c];
-    gx[(sb_i64)j * CX + c] = s;
+  if (lane == 0) cursor[j] = start + n;
+  if (!first && n == 0) return;
+  float* row = gx + (sb_i64)j * CX;
+  if ((CX & 3) == 0) {
+    for (int c = 4 * lane; c < CX; c += 256) {
+      sb_v4 s = first ? (sb_v4){0.f, 0.f, 0.f, 0.f} : *(const sb_v4*)(row + c);
+      for (int t = 0; t < n; ++t) s += sb_ld4(contrib + (sb_i64)(send_perm[start + t] - e0) * CX + c);
+      *(sb_v4*)(row + c) = s;
+    }
+  } else {
+    for (int c = lane; c < CX; c += 64) {
+      float s = first ? 0.f : row[c];
+      for (int t = 0; t < n; ++t) s += contrib[(sb_i64)(send_perm[start + t] - e0) * CX + c];
+      row[c] = s;
+    }
   }
 }
 

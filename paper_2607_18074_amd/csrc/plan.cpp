@@ -44,6 +44,9 @@ void build_plan(Plan& p) {
   for (auto& r : p.out) { r.off = off; off += r.dim(); }
   p.dim_out = off;
   p.nsh = (p.lmax + 1) * (p.lmax + 1);
+  p.vec4 = true;
+  for (auto& r : p.in) p.vec4 = p.vec4 && r.mul % 4 == 0;
+  for (auto& r : p.out) p.vec4 = p.vec4 && r.mul % 4 == 0;
 
   // paths (Section 2.2 eq. cg_selection_rules; lexicographic (in, sh, out) order)
   p.paths.clear();

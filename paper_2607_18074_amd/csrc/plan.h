@@ -71,6 +71,7 @@ struct Kernels {
   hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, fwd_dS_r = nullptr;
   hipFunction_t bwd_E = nullptr, dbwd_E = nullptr, dbwd_E_r = nullptr;
   hipFunction_t gemm_sa[3] = {}, gemm_sbar[3] = {}, gemm_ga[3] = {};  // BN = 16, 32, 64
+  hipFunction_t gemm_sa_v[3] = {}, gemm_ga_v[3] = {}, gemm_sbar_v = nullptr;  // 16-byte aligned operands
   hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
                 zero = nullptr;
 };
@@ -89,6 +90,7 @@ struct Plan {
   std::vector<AdjSlab> slabs;
   int bwd_eb = 64;              // edges per batch when the adjoint state needs several slabs
   int bwd_lds_max = 0;          // largest slab (floats)
+  bool vec4 = false;            // every multiplicity a multiple of 4: vectorised GEMMs apply
   std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
   std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)
   std::string source;           // generated HIP source
