@@ -390,79 +390,143 @@ int unit_lsh(const Plan& P, const Unit& u) {
   return L;
 }
 
+// Forward state (S) or directional state (dS) of one wave unit.  Lane = sub * U + u:
+// ES edges in flight, one input channel u per lane.  The edge loop has the same
+// trip count on every lane (inactive lanes contribute zeros), so the rank-1
+// accumulation S[u, q] += C[u] phi[q] can run on v_mfma_f32_4x4x1_16b_f32 when
+// U and K are multiples of 4: each 4-lane block multiplies its 4 channel values
+// (A) by a quad of radial features (B), and lane 4b + j, register i accumulates
+// S[u = 4b + i][q = 4 qq + j].  Otherwise it runs on the VALU, one channel per lane.
 void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) {
   const Irrep& ri = P.in[u.a];
   const int DA = 2 * ri.l + 1, L = unit_lsh(P, u), NS = (L + 1) * (L + 1);
+  const bool mf = (u.U % 4 == 0) && (P.K % 4 == 0);
+  const int KQ = P.K / 4;
   o << "template <bool TAN, int FL>\nSB_DEV void sb_fwd_u" << id
     << "(int lane, int il, int beg, int end, const int* __restrict__ sender, const float* __restrict__ evec,"
        " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, sb_i64 ncap,"
        " const float* __restrict__ xdot, const float* __restrict__ evdot, const float* __restrict__ phidot, int flags) {\n";
   o << "  const int fl = FL >= 0 ? FL : flags;\n";
   o << "  constexpr int U = " << u.U << ", U0 = " << u.U0 << ", ES = " << u.ES << ", CA = " << ri.mul
-    << ", AOFF = " << ri.off << ";\n";
+    << ", AOFF = " << ri.off << ", DA = " << DA << ";\n";
   o << "  const int sub = lane / U, u = U0 + lane % U;\n"
-       "  const bool act = (lane < ES * U) && (u < CA);\n";
-  for (int t : u.paths) o << "  float acc" << t << "[K * " << 2 * P.paths[t].l_out + 1 << "] = {};\n";
-  o << "  if (act) {\n"
-       "    for (int e = beg + sub; e < end; e += ES) {\n"
-       "      const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
-       "      const float rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
-       "      const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
-    << "      float Y[" << NS << "];\n      sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
-    << "      float ph[K];\n"
-       "#pragma unroll\n      for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
-       "      const sb_i64 xrow = (sb_i64)sender[e] * CXI + AOFF + u;\n"
-    << "      float xv[" << DA << "];\n"
-    << "#pragma unroll\n      for (int m = 0; m < " << DA << "; ++m) xv[m] = x[xrow + m * CA];\n";
-  o << "      float Yd[" << NS << "], phd[K], xdv[" << DA << "];\n"
-       "      if (TAN) {\n"
-       "        if (fl & 4) {\n"
-       "          const float dx = evdot[3 * (sb_i64)e], dy = evdot[3 * (sb_i64)e + 1], dz = evdot[3 * (sb_i64)e + 2];\n"
-    << "          sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n"
-    << "        }\n"
-       "        if (fl & 1) {\n#pragma unroll\n          for (int q = 0; q < K; ++q) phd[q] = phidot[(sb_i64)e * K + q];\n        }\n"
-       "        if (fl & 2) {\n#pragma unroll\n"
-    << "          for (int m = 0; m < " << DA << "; ++m) xdv[m] = xdot[xrow + m * CA];\n        }\n      }\n";
+       "  const bool act = (lane < ES * U) && (u < CA);\n"
+       "  const int niter = (end - beg + ES - 1) / ES;\n";
+  for (int t : u.paths) {
+    const int DO = 2 * P.paths[t].l_out + 1;
+    if (mf)
+      o << "  sb_f4 acc" << t << "[" << DO * KQ << "];\n"
+        << "#pragma unroll\n  for (int v = 0; v < " << DO * KQ << "; ++v) acc" << t << "[v] = (sb_f4){0.f, 0.f, 0.f, 0.f};\n";
+    else
+      o << "  float acc" << t << "[K * " << DO << "] = {};\n";
+  }
+  // software pipeline: the receiver's sender ids are loaded 64 at a time and
+  // shared through the wave; the edge data of iteration it + 1 is fetched into
+  // the n* registers before iteration it is computed
+  const int NPH = mf ? KQ : P.K;
+  o << "  int snd = (beg + lane < end) ? sender[beg + lane] : 0;\n"
+       "  float nvx, nvy, nvz, ndx, ndy, ndz, nxv[DA], nxdv[DA], nph[" << NPH << "], nphd[" << NPH << "];\n"
+       "  auto fetch = [&](int itn) {\n"
+       "    const int kb = itn * ES;\n"
+       "    if (itn > 0 && (kb & 63) == 0) snd = (beg + kb + lane < end) ? sender[beg + kb + lane] : 0;\n"
+       "    const int j = __shfl(snd, (kb & 63) + sub);\n"
+       "    const int e = beg + kb + sub;\n"
+       "    const bool ev = act && e < end;\n"
+       "    nvx = 0.f; nvy = 0.f; nvz = 1.f; ndx = 0.f; ndy = 0.f; ndz = 0.f;\n"
+       "#pragma unroll\n    for (int m = 0; m < DA; ++m) { nxv[m] = 0.f; nxdv[m] = 0.f; }\n"
+       "#pragma unroll\n    for (int q = 0; q < " << NPH << "; ++q) { nph[q] = 0.f; nphd[q] = 0.f; }\n"
+       "    if (ev) {\n"
+       "      nvx = evec[3 * (sb_i64)e]; nvy = evec[3 * (sb_i64)e + 1]; nvz = evec[3 * (sb_i64)e + 2];\n"
+       "      const sb_i64 xrow = (sb_i64)j * CXI + AOFF + u;\n"
+       "#pragma unroll\n      for (int m = 0; m < DA; ++m) nxv[m] = x[xrow + m * CA];\n";
+  if (mf)
+    o << "#pragma unroll\n      for (int qq = 0; qq < " << KQ << "; ++qq) nph[qq] = phi[(sb_i64)e * K + 4 * qq + (lane & 3)];\n"
+      << "      if (TAN && (fl & 1)) {\n#pragma unroll\n        for (int qq = 0; qq < " << KQ
+      << "; ++qq) nphd[qq] = phidot[(sb_i64)e * K + 4 * qq + (lane & 3)];\n      }\n";
+  else
+    o << "#pragma unroll\n      for (int q = 0; q < K; ++q) nph[q] = phi[(sb_i64)e * K + q];\n"
+      << "      if (TAN && (fl & 1)) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) nphd[q] = phidot[(sb_i64)e * K + q];\n      }\n";
+  o << "      if (TAN && (fl & 2)) {\n#pragma unroll\n        for (int m = 0; m < DA; ++m) nxdv[m] = xdot[xrow + m * CA];\n      }\n"
+       "      if (TAN && (fl & 4)) { ndx = evdot[3 * (sb_i64)e]; ndy = evdot[3 * (sb_i64)e + 1]; ndz = evdot[3 * (sb_i64)e + 2]; }\n"
+       "    }\n"
+       "  };\n"
+       "  fetch(0);\n"
+       "  for (int it = 0; it < niter; ++it) {\n"
+       "    const float vx = nvx, vy = nvy, vz = nvz, dx = ndx, dy = ndy, dz = ndz;\n"
+    << "    float xv[DA], xdv[DA], " << (mf ? "bq" : "ph") << "[" << NPH << "], " << (mf ? "bqd" : "phd") << "[" << NPH << "];\n"
+    << "#pragma unroll\n    for (int m = 0; m < DA; ++m) { xv[m] = nxv[m]; xdv[m] = nxdv[m]; }\n"
+    << "#pragma unroll\n    for (int q = 0; q < " << NPH << "; ++q) { " << (mf ? "bq" : "ph") << "[q] = nph[q]; "
+    << (mf ? "bqd" : "phd") << "[q] = nphd[q]; }\n"
+    << "    if (it + 1 < niter) fetch(it + 1);\n"
+       "    const float rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
+       "    const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
+    << "    float Y[" << NS << "], Yd[" << NS << "];\n    sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
+    << "    if (TAN && (fl & 4)) sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n";
   for (int t : u.paths) {
     const Path& q = P.paths[t];
     const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
-    o << "      {\n        float M[P" << t << "_NP], C[" << DO << "];\n"
-      << "        sb_M" << t << "(Y + " << Y0 << ", M);\n"
-      << "        if (!TAN) {\n          sb_C" << t << "(xv, M, C);\n"
-      << "#pragma unroll\n          for (int q = 0; q < K; ++q)\n#pragma unroll\n"
-      << "            for (int m = 0; m < " << DO << "; ++m) acc" << t << "[q * " << DO << " + m] = fmaf(ph[q], C[m], acc"
-      << t << "[q * " << DO << " + m]);\n"
-      << "        } else {\n"
-      << "          float C2[" << DO << "] = {};\n"
-      << "          if (fl & 2) { sb_C" << t << "(xdv, M, C); for (int m = 0; m < " << DO << "; ++m) C2[m] += C[m]; }\n"
-      << "          if (fl & 4) { float Md[P" << t << "_NP]; sb_M" << t << "(Yd + " << Y0 << ", Md); sb_C" << t
-      << "(xv, Md, C); for (int m = 0; m < " << DO << "; ++m) C2[m] += C[m]; }\n"
-      << "#pragma unroll\n          for (int q = 0; q < K; ++q)\n#pragma unroll\n"
-      << "            for (int m = 0; m < " << DO << "; ++m) acc" << t << "[q * " << DO << " + m] = fmaf(ph[q], C2[m], acc"
-      << t << "[q * " << DO << " + m]);\n"
-      << "          if (fl & 1) {\n            sb_C" << t << "(xv, M, C);\n"
-      << "#pragma unroll\n            for (int q = 0; q < K; ++q)\n#pragma unroll\n"
-      << "              for (int m = 0; m < " << DO << "; ++m) acc" << t << "[q * " << DO << " + m] = fmaf(phd[q], C[m], acc"
-      << t << "[q * " << DO << " + m]);\n          }\n        }\n      }\n";
+    o << "    {  // path " << t << "\n"
+      << "      constexpr int DO = " << DO << ";\n"
+      << "      float M[P" << t << "_NP], C[DO], C2[DO];\n"
+      << "      sb_M" << t << "(Y + " << Y0 << ", M);\n"
+      << "      if (!TAN) {\n        sb_C" << t << "(xv, M, C2);\n      } else {\n"
+      << "#pragma unroll\n        for (int m = 0; m < DO; ++m) C2[m] = 0.f;\n"
+      << "        if (fl & 2) { sb_C" << t << "(xdv, M, C); for (int m = 0; m < DO; ++m) C2[m] += C[m]; }\n"
+      << "        if (fl & 4) { float Md[P" << t << "_NP]; sb_M" << t << "(Yd + " << Y0 << ", Md); sb_C" << t
+      << "(xv, Md, C); for (int m = 0; m < DO; ++m) C2[m] += C[m]; }\n"
+      << "        if (fl & 1) sb_C" << t << "(xv, M, C);\n"
+      << "      }\n";
+    if (mf) {
+      o << "#pragma unroll\n      for (int m = 0; m < DO; ++m)\n#pragma unroll\n"
+        << "        for (int qq = 0; qq < " << KQ << "; ++qq) {\n"
+        << "          acc" << t << "[m * " << KQ << " + qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(C2[m], bq[qq], acc" << t
+        << "[m * " << KQ << " + qq], 0, 0, 0);\n"
+        << "          if (TAN && (fl & 1)) acc" << t << "[m * " << KQ << " + qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(C[m], bqd[qq], acc"
+        << t << "[m * " << KQ << " + qq], 0, 0, 0);\n"
+        << "        }\n";
+    } else {
+      o << "#pragma unroll\n      for (int q = 0; q < K; ++q)\n#pragma unroll\n"
+        << "        for (int m = 0; m < DO; ++m) {\n"
+        << "          acc" << t << "[q * DO + m] = fmaf(ph[q], C2[m], acc" << t << "[q * DO + m]);\n"
+        << "          if (TAN && (fl & 1)) acc" << t << "[q * DO + m] = fmaf(phd[q], C[m], acc" << t << "[q * DO + m]);\n"
+        << "        }\n";
+    }
+    o << "    }\n";
   }
-  o << "    }\n  }\n";
+  o << "  }\n";
   if (u.ES > 1) {
-    for (int t : u.paths)
-      o << "#pragma unroll\n  for (int v = 0; v < K * " << 2 * P.paths[t].l_out + 1 << "; ++v)\n"
-        << "    for (int s = U; s < 64; s <<= 1) acc" << t << "[v] += __shfl_xor(acc" << t << "[v], s);\n";
+    for (int t : u.paths) {
+      const int DO = 2 * P.paths[t].l_out + 1;
+      if (mf)
+        o << "#pragma unroll\n  for (int v = 0; v < " << DO * KQ << "; ++v)\n#pragma unroll\n    for (int i = 0; i < 4; ++i)\n"
+          << "      for (int s = U; s < 64; s <<= 1) acc" << t << "[v][i] += __shfl_xor(acc" << t << "[v][i], s);\n";
+      else
+        o << "#pragma unroll\n  for (int v = 0; v < K * " << DO << "; ++v)\n"
+          << "    for (int s = U; s < 64; s <<= 1) acc" << t << "[v] += __shfl_xor(acc" << t << "[v], s);\n";
+    }
   }
-  o << "  if (act && sub == 0) {\n";
+  o << "  if (sub == 0 && lane < U) {\n";
   for (int t : u.paths) {
     const Path& q = P.paths[t];
     const Group& g = P.groups[q.group];
     const int DO = 2 * q.l_out + 1;
-    o << "    {\n      float* Sg = S + ncap * " << g.s_off << "LL + (sb_i64)il * " << (int64_t)g.d * g.D << "LL + "
-      << q.koff << " + u;\n"
-      << "#pragma unroll\n      for (int q = 0; q < K; ++q)\n#pragma unroll\n"
-      << "        for (int m = 0; m < " << DO << "; ++m) Sg[(sb_i64)m * " << g.D << " + q * " << q.c_in << "] = acc" << t
-      << "[q * " << DO << " + m];\n    }\n";
+    o << "    {\n      constexpr int DO = " << DO << ";\n      float* Sg = S + ncap * " << g.s_off
+      << "LL + (sb_i64)il * " << (int64_t)g.d * g.D << "LL + " << q.koff << ";\n";
+    if (mf) {
+      o << "      const int ub = U0 + 4 * ((lane % U) >> 2), j = lane & 3;\n"
+        << "#pragma unroll\n      for (int m = 0; m < DO; ++m)\n#pragma unroll\n"
+        << "        for (int qq = 0; qq < " << KQ << "; ++qq)\n#pragma unroll\n"
+        << "          for (int i = 0; i < 4; ++i)\n"
+        << "            if (ub + i < CA) Sg[(sb_i64)m * " << g.D << " + (4 * qq + j) * " << q.c_in << " + ub + i] = acc" << t
+        << "[m * " << KQ << " + qq][i];\n";
+    } else {
+      o << "      if (u < CA) {\n#pragma unroll\n        for (int q = 0; q < K; ++q)\n#pragma unroll\n"
+        << "          for (int m = 0; m < DO; ++m) Sg[(sb_i64)m * " << g.D << " + q * " << q.c_in << " + u] = acc" << t
+        << "[q * DO + m];\n      }\n";
+    }
+    o << "    }\n";
   }
-  o << "  }\n}\n";
+  o << "  }\n}\n\n";
 }
 
 // Adjoint (backward / double-backward) code for one slab: every wave runs all
@@ -490,7 +554,21 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        "  constexpr int U = ADJ_U, ES = ADJ_ES;\n"
        "  const int sub = lane / U, uu = lane % U;\n"
        "  const int niter = (nb + 4 * ES - 1) / (4 * ES);\n"
+       // sender ids of this wave's edge slots are preloaded 64 at a time (slot t ->
+       // edge k = ((t / ES) * 4 + w) * ES + t % ES) and shared through the wave, so
+       // the sender-row gather is the only dependent load of an iteration.  (Fetching
+       // the next iteration's data ahead doubles these registers and, with the slab
+       // resident in flight, drops the kernel to one wave per SIMD: measured slower.)
+       "  constexpr int SPB = 64 / ES;\n"
+       "  int snd;\n"
+       "  {\n    const int kk = ((lane / ES) * 4 + w) * ES + lane % ES;\n    snd = kk < nb ? sender[ebase + kk] : 0;\n  }\n"
        "  for (int it = 0; it < niter; ++it) {\n"
+       "    if (it > 0 && it % SPB == 0) {\n"
+       "      const int t = it * ES + lane;\n"
+       "      const int kk = ((t / ES) * 4 + w) * ES + t % ES;\n"
+       "      snd = kk < nb ? sender[ebase + kk] : 0;\n"
+       "    }\n"
+       "    const int jsnd = __shfl(snd, (it % SPB) * ES + sub);\n"
        "    const int k = (it * 4 + w) * ES + sub;\n"
        "    const bool ev = k < nb;\n"
        "    const int e = ebase + k;\n"
@@ -510,7 +588,7 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        "        const float dx = evdot[3 * (sb_i64)e], dy = evdot[3 * (sb_i64)e + 1], dz = evdot[3 * (sb_i64)e + 2];\n"
     << "        sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n      }\n"
     << "      if (DB && (fl & 1)) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) phd[q] = phidot[(sb_i64)e * K + q];\n      }\n"
-    << "      const sb_i64 srow = (sb_i64)sender[e] * CXI;\n";
+    << "      const sb_i64 srow = (sb_i64)jsnd * CXI;\n";
   for (const AdjItem& it : sl.items) {
     const Irrep& ri = P.in[it.a];
     const int DA = 2 * ri.l + 1;
@@ -646,7 +724,9 @@ std::string generate_source(const Plan& P) {
   struct FV { const char* name; bool tan; int fl; };
   const FV fvs[] = {{"S", false, 0}, {"dS_r", true, 4}, {"dS", true, -1}};
   for (const FV& fv : fvs) {
-    o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_fwd_" << fv.name
+    // two waves per SIMD: keeps the MFMA accumulators in VGPRs without spilling
+    o << "extern \"C\" __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void sobek_fwd_"
+      << fv.name
       << "(const int* __restrict__ rowptr, const int* __restrict__ sender, const float* __restrict__ evec,"
          " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, int r0, int n_recv,"
          " sb_i64 ncap, const float* __restrict__ xdot, const float* __restrict__ evdot,"
