@@ -76,6 +76,37 @@ def kernel_kind(name):
     return None
 
 
+def source_sha256(sig):
+    import hashlib
+    from paper_2607_18074_amd import _lib
+    return hashlib.sha256(_lib.plan_source(*sig).encode()).hexdigest()
+
+
+def traffic_record(kernel, sha, launches_per_step):
+    """HBM bytes per launch of `kernel` from a committed counter summary, if it still describes this code.
+
+    A summary under profiles/ carries a block
+        <!-- traffic-record
+        kernel: <name>  source_sha256: <hex>  launches_per_step: <n>
+        fetch_bytes_per_launch: <b>  write_bytes_per_launch: <b>
+        -->
+    (one key per line).  It applies only when the kernel, the hash of the compiled source and the number of
+    launches per step all match; otherwise the traffic is unknown (None).
+    """
+    import glob
+    import re
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        text = open(path).read()
+        for block in re.findall(r"<!-- traffic-record(.*?)-->", text, re.S):
+            rec = dict(re.findall(r"^\s*(\w+):\s*(\S+)\s*$", block, re.M))
+            if (rec.get("kernel") == kernel and rec.get("source_sha256") == sha
+                    and abs(float(rec.get("launches_per_step", -1)) - launches_per_step) < 1e-6):
+                return dict(bytes=float(rec["fetch_bytes_per_launch"]) + float(rec["write_bytes_per_launch"]),
+                            fetch=float(rec["fetch_bytes_per_launch"]), write=float(rec["write_bytes_per_launch"]),
+                            source=os.path.relpath(path, ROOT))
+    return None
+
+
 def cpu_baseline(case, plan_sig, target_s=15.0):
     """Time the oracle (fwd + bwd + dbwd) on the in-edges of the first receivers."""
     from oracle import conv as oc
@@ -216,6 +247,7 @@ def main():
         pass_ms[name] = a.elapsed_time(b) / args.steps
 
     fm = flop_model(plan, g.N, g.E)
+    sha = source_sha256((cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"]))
     kernels = {}
     for name, (n, ms) in prof.items():
         kernels[name] = dict(launches_per_step=n / args.steps, ms_per_step=ms / args.steps,
@@ -229,10 +261,16 @@ def main():
             per_step *= {"gemm_sa": 1, "gemm_sbar": 2, "gemm_ga": 2}[kind]  # launches of this GEMM per step
         flops_per_launch = per_step * args.steps / dom_n
         achieved = flops_per_launch / (dom_ms / dom_n * 1e-3) / 1e12
+        tr = traffic_record(dom_name, sha, dom_n / args.steps)
         roof = dict(bound="mfma" if kind.startswith("gemm") else "alu", kernel=dom_name, achieved=achieved,
-                    peak=PEAK_FP32_TFLOPS, unit="TFLOP/s", frac=achieved / PEAK_FP32_TFLOPS, traffic=None,
+                    peak=PEAK_FP32_TFLOPS, unit="TFLOP/s", frac=achieved / PEAK_FP32_TFLOPS,
+                    traffic=None if tr is None else tr["bytes"],
                     flops_per_launch=flops_per_launch, mean_launch_ms=dom_ms / dom_n,
-                    share_of_step=dom_ms / args.steps / ms_step)
+                    launches_per_step=dom_n / args.steps, share_of_step=dom_ms / args.steps / ms_step,
+                    source_sha256=sha)
+        if tr is not None:
+            roof["traffic_gbs"] = tr["bytes"] / (dom_ms / dom_n * 1e-3) / 1e9
+            roof["traffic_source"] = tr["source"]
     else:
         roof = dict(bound="hbm", kernel=dom_name, achieved=None, peak=PEAK_HBM_GBS, unit="GB/s", frac=None,
                     traffic=None)

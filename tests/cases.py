@@ -61,3 +61,23 @@ def make_case(sig, N, E, seed, isolated=0):
     gout = wl.out_cotangent(N, dout, seed)
     cot = wl.cotangents(N, g.E, K, din, len(std), seed)
     return dict(sig=(irr_in, lmax, irr_out, K), graph=g, x=x, W=W, gout=gout, cot=cot, dim_in=din, dim_out=dout)
+
+
+def edge_subgraph(g, edges):
+    """CSR of the edges `edges` (ascending ids of a receiver-sorted graph) with their receivers renumbered.
+
+    Returns (rowptr, sender, evec, phi, receivers): senders keep their node ids, so node tensors are
+    passed whole; `receivers[r]` is the original id of renumbered receiver r (row r of a receiver-indexed
+    result, and the row to gather from receiver-indexed inputs).
+    """
+    edges = np.asarray(edges, dtype=np.int64)
+    recv = np.repeat(np.arange(g.N), np.diff(g.rowptr))[edges]
+    receivers, local = np.unique(recv, return_inverse=True)
+    rowptr = np.concatenate([[0], np.cumsum(np.bincount(local, minlength=len(receivers)))]).astype(np.int64)
+    return rowptr, g.sender[edges], g.evec[edges], g.phi[edges], receivers
+
+
+def in_edges(g, receivers):
+    """Ids of the edges into `receivers`, ascending."""
+    receivers = np.sort(np.asarray(receivers, dtype=np.int64))
+    return np.concatenate([np.arange(g.rowptr[r], g.rowptr[r + 1]) for r in receivers]).astype(np.int64)
