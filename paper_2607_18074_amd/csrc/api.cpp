@@ -95,10 +95,11 @@ hipEvent_t pool_event() {
 }
 
 template <typename... Args>
-hipError_t launch(hipFunction_t f, unsigned gx, unsigned gy, unsigned gz, hipStream_t s, Args... args) {
+hipError_t launch_n(hipFunction_t f, unsigned nthreads, unsigned gx, unsigned gy, unsigned gz, hipStream_t s,
+                    Args... args) {
   if (gx == 0 || gy == 0 || gz == 0) return hipSuccess;
   void* ptrs[] = {(void*)&args...};
-  if (!g_prof_on) return hipModuleLaunchKernel(f, gx, gy, gz, 256, 1, 1, 0, s, ptrs, nullptr);
+  if (!g_prof_on) return hipModuleLaunchKernel(f, gx, gy, gz, nthreads, 1, 1, 0, s, ptrs, nullptr);
   std::lock_guard<std::mutex> lk(g_prof_mu);
   ProfRec r;
   auto it = g_names.find(f);
@@ -106,13 +107,19 @@ hipError_t launch(hipFunction_t f, unsigned gx, unsigned gy, unsigned gz, hipStr
   r.a = pool_event();
   r.b = pool_event();
   (void)hipEventRecord(r.a, s);
-  hipError_t e = hipModuleLaunchKernel(f, gx, gy, gz, 256, 1, 1, 0, s, ptrs, nullptr);
+  hipError_t e = hipModuleLaunchKernel(f, gx, gy, gz, nthreads, 1, 1, 0, s, ptrs, nullptr);
   (void)hipEventRecord(r.b, s);
   g_prof.push_back(r);
   return e;
 }
 
+template <typename... Args>
+hipError_t launch(hipFunction_t f, unsigned gx, unsigned gy, unsigned gz, hipStream_t s, Args... args) {
+  return launch_n(f, 256, gx, gy, gz, s, args...);
+}
+
 #define LAUNCH(...) HIPCHK(launch(__VA_ARGS__))
+#define LAUNCH_N(...) HIPCHK(launch_n(__VA_ARGS__))
 
 constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
@@ -750,7 +757,7 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
       if ((rc = run_sbar(p, c, w, gk, W, Sb, stream))) return rc;
       int r0 = c.r0, n = c.n, e0 = (int)c.e0, flags = 0;
       long long ncap = w.ncap;
-      LAUNCH(p.k.bwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
+      LAUNCH_N(p.k.bwd_E, 64 * p.adj_waves, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
              (const float*)Sb, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
              (const float*)nullptr, gphi, gevec, contrib, r0, n, ncap, e0, flags);
       if (gx && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
@@ -820,7 +827,7 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const fl
       int r0 = c.r0, n = c.n, e0 = (int)c.e0;
       long long ncap = w.ncap;
       int fl = flags;
-      LAUNCH(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
+      LAUNCH_N(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, 64 * p.adj_waves, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
              (const float*)Sb, (const float*)Sb2, txk, t_gevec, t_gphi, g_phi, g_evec, contrib, r0, n, ncap, e0, fl);
       if (g_x && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
     }

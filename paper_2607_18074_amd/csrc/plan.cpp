@@ -19,7 +19,7 @@ namespace sobek {
 namespace {
 constexpr int kAccMax = 128;        // forward accumulators per lane per wave unit
 constexpr int kSlabFloats = 10240;  // backward LDS budget for one slab of adjoint state (40 KiB)
-constexpr int kWaves = 4;           // waves per adjoint block
+constexpr int kAdjWaves = 2;        // waves per adjoint block
 
 bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 
@@ -138,14 +138,13 @@ void build_plan(Plan& p) {
     }
   }
 
-  // adjoint lane mapping: the smallest power of two >= every input multiplicity
-  // (capped at 64) lanes per edge, the rest of the wave holds further edges
-  int umax = 1;
-  for (auto& r : p.in) umax = std::max(umax, std::min(r.mul, 64));
-  p.adj_U = 1;
-  while (p.adj_U < umax) p.adj_U *= 2;
-  p.adj_ES = 64 / p.adj_U;
-  // items (input irrep, channel block, path chunk) packed into LDS slabs in order
+  // adjoint tiles: 16 channels per item, radial index padded to a multiple of 4
+  p.adj_U = 16;
+  p.adj_KP = (p.K + 3) / 4 * 4;
+  p.adj_waves = kAdjWaves;
+  p.bwd_eb = 16 * kAdjWaves * 2;
+  auto slice = [&](int t) { return p.adj_KP * (2 * p.paths[t].l_out + 1) * p.adj_U; };
+  // items (input irrep, channel tile, path chunk) packed into LDS slabs in order
   p.slabs.clear();
   std::vector<AdjItem> items;
   std::vector<int> item_floats;
@@ -160,7 +159,7 @@ void build_plan(Plan& p) {
       int fl = 0;
       bool first = true;
       for (int t : ps) {
-        int need = p.K * (2 * p.paths[t].l_out + 1) * p.adj_U;
+        int need = slice(t);
         if (need > kSlabFloats) throw std::runtime_error("path adjoint slice exceeds the LDS slab budget");
         if (!cur.paths.empty() && fl + need > kSlabFloats) {
           cur.first = first;
@@ -189,7 +188,7 @@ void build_plan(Plan& p) {
       int o = cur.floats;
       for (int t : it.paths) {
         it.lds_off.push_back(o);
-        o += p.K * (2 * p.paths[t].l_out + 1) * p.adj_U;
+        o += slice(t);
       }
       cur.items.push_back(it);
       cur.floats = o;
@@ -325,13 +324,16 @@ void emit_sh(std::ostringstream& o, int lmax) {
 
 struct PairTerm { int my; double c; };
 
-// Path p: M[(mi,mo) pairs] = sum_my c Y[my];  C[mo] = sum_mi x[mi] M[mi,mo];
-// X: xb[mi] += sum_mo M[mi,mo] G[mo];  Yb[my] += sum c x[mi] G[mo].
-void emit_path(std::ostringstream& o, const Plan& P, int t) {
-  const Path& q = P.paths[t];
-  const int di = 2 * q.l_in + 1, ds = 2 * q.l_sh + 1, dd = 2 * q.l_out + 1;
+// Sparse structure of a path's coupling: the (m_i, m_o) pairs with a nonzero
+// coefficient, each with its (m_y, c) terms.
+struct PathTerms {
   std::vector<std::pair<int, int>> pairs;
   std::vector<std::vector<PairTerm>> terms;
+};
+
+PathTerms path_terms(const Path& q) {
+  const int di = 2 * q.l_in + 1, ds = 2 * q.l_sh + 1, dd = 2 * q.l_out + 1;
+  PathTerms r;
   for (int mi = 0; mi < di; ++mi)
     for (int mo = 0; mo < dd; ++mo) {
       std::vector<PairTerm> tt;
@@ -339,8 +341,18 @@ void emit_path(std::ostringstream& o, const Plan& P, int t) {
         double c = q.cg[((size_t)mi * ds + my) * dd + mo];
         if (std::abs(c) > 1e-14) tt.push_back({my, c});
       }
-      if (!tt.empty()) { pairs.push_back({mi, mo}); terms.push_back(tt); }
+      if (!tt.empty()) { r.pairs.push_back({mi, mo}); r.terms.push_back(tt); }
     }
+  return r;
+}
+
+// Path p: M[(mi,mo) pairs] = sum_my c Y[my];  C[mo] = sum_mi x[mi] M[mi,mo].
+void emit_path(std::ostringstream& o, const Plan& P, int t) {
+  const Path& q = P.paths[t];
+  const int dd = 2 * q.l_out + 1;
+  const PathTerms pt = path_terms(q);
+  const std::vector<std::pair<int, int>>& pairs = pt.pairs;
+  const std::vector<std::vector<PairTerm>>& terms = pt.terms;
   const int np = (int)pairs.size();
   o << "// path " << t << ": l_in=" << q.l_in << " l_sh=" << q.l_sh << " l_out=" << q.l_out << " alpha=" << q.alpha
     << "\n#define P" << t << "_NP " << np << "\n";
@@ -353,33 +365,11 @@ void emit_path(std::ostringstream& o, const Plan& P, int t) {
   }
   o << "}\nSB_DEV void sb_C" << t << "(const float* x, const float* M, float* C) {\n";
   for (int mo = 0; mo < dd; ++mo) {
-    o << "  C[" << mo << "] = 0.0f";
-    for (int k = 0; k < np; ++k)
-      if (pairs[k].second == mo) o << " + x[" << pairs[k].first << "]*M[" << k << "]";
-    o << ";\n";
-  }
-  o << "}\nSB_DEV void sb_X" << t << "(const float* G, const float* M, float* xb) {\n";
-  for (int mi = 0; mi < di; ++mi) {
+    o << "  C[" << mo << "] =";
     bool any = false;
-    for (int k = 0; k < np; ++k) any |= pairs[k].first == mi;
-    if (!any) continue;
-    o << "  xb[" << mi << "] +=";
-    bool first = true;
     for (int k = 0; k < np; ++k)
-      if (pairs[k].first == mi) { o << (first ? " " : " + ") << "M[" << k << "]*G[" << pairs[k].second << "]"; first = false; }
-    o << ";\n";
-  }
-  o << "}\nSB_DEV void sb_Y" << t << "(const float* x, const float* G, float* yb) {\n";
-  for (int my = 0; my < ds; ++my) {
-    std::ostringstream e;
-    bool first = true;
-    for (int k = 0; k < np; ++k)
-      for (auto& tt : terms[k])
-        if (tt.my == my) {
-          e << (first ? " " : " + ") << fl(tt.c) << "*(x[" << pairs[k].first << "]*G[" << pairs[k].second << "])";
-          first = false;
-        }
-    if (!first) o << "  yb[" << my << "] +=" << e.str() << ";\n";
+      if (pairs[k].second == mo) { o << (any ? " + " : " ") << "x[" << pairs[k].first << "]*M[" << k << "]"; any = true; }
+    o << (any ? ";\n" : " 0.0f;\n");
   }
   o << "}\n";
 }
@@ -529,10 +519,148 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
   o << "  }\n}\n\n";
 }
 
-// Adjoint (backward / double-backward) code for one slab: every wave runs all
-// items of the slab for the edges it owns (edge k of the block -> wave
-// (k / ES) % 4, sub k % ES).  Per-edge partial sums stay in registers across
-// the slab's paths and are reduced over the channel lanes once per edge.
+// One path of an adjoint item, output component by output component so that
+// only one m_o's coupling values, channel values and G tile are live at a time.
+// For output component m the lane computes, for its edge and its 4 channels r:
+//   M_k = sum c Y[m_y]               (pairs k = (m_i, m) of the path)
+//   G[r] = sum_q phi[q] Sbar[q][m][u_r]                       (16x16x4 MFMA)
+//   C[r] = sum_k x[r][m_i] M_k;  phibar[q] += Sbar[q][m][u_r] C[r]  (4x4x1)
+//   xbar[r][m_i] += M_k G[r];   Ybar[m_y] += c sum_r x[r][m_i] G[r]
+// and the double-backward analogues with the tangents of Y, phi, x and A.
+void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off) {
+  const Path& q = P.paths[t];
+  const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
+  const PathTerms pt = path_terms(q);
+  auto yexpr = [&](const std::vector<PairTerm>& tt, const char* Yn) {
+    std::ostringstream e;
+    for (size_t j = 0; j < tt.size(); ++j) e << (j ? " + " : "") << fl(tt[j].c) << "*" << Yn << "[" << Y0 + tt[j].my << "]";
+    return e.str();
+  };
+  auto cexpr = [&](const std::vector<int>& ks, const char* xn, const char* Mn, int r) {
+    std::ostringstream e;
+    for (size_t j = 0; j < ks.size(); ++j)
+      e << (j ? " + " : "") << xn << "[" << r << "][" << pt.pairs[ks[j]].first << "]*" << Mn << ks[j];
+    return e.str();
+  };
+  // G tile of component m against radial features `ph` and adjoint state `sp`
+  auto gtile = [&](const char* dst, const char* sp, const char* ph, int m) {
+    std::ostringstream e;
+    e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) " << dst << " = sb_mfma(" << sp << "[((4 * v + g) * " << DO
+      << " + " << m << ") * 16 + es], " << ph << "[v], " << dst << ");\n";
+    return e.str();
+  };
+  // phibar[q] += sum_r Sbar[q][m][u_r] c[r]
+  auto ptile = [&](const char* sp, const char* cn, int m) {
+    std::ostringstream e;
+    e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) {\n"
+      << "              const sb_f4 a = *(const sb_f4*)(" << sp << " + ((4 * v + l3) * " << DO << " + " << m << ") * 16 + 4 * g);\n"
+      << "              pacc[v] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[0], " << cn << "0, pacc[v], 0, 0, 0);\n"
+      << "              pacc[v] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[1], " << cn << "1, pacc[v], 0, 0, 0);\n"
+      << "              pacc[v] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[2], " << cn << "2, pacc[v], 0, 0, 0);\n"
+      << "              pacc[v] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[3], " << cn << "3, pacc[v], 0, 0, 0);\n"
+      << "            }\n";
+    return e.str();
+  };
+  // xbar[r][m_i] += Mk G[r] over the pairs
+  auto xupd = [&](const std::vector<int>& ks, const char* Mn, const char* Gn) {
+    std::ostringstream e;
+    for (int k : ks)
+      for (int r = 0; r < 4; ++r)
+        e << "            xc[" << r << "][" << pt.pairs[k].first << "] = fmaf(" << Mn << k << ", " << Gn << "[" << r
+          << "], xc[" << r << "][" << pt.pairs[k].first << "]);\n";
+    return e.str();
+  };
+  // acc[Y0 + m_y] += c sum_r xs[r][m_i] G[r]
+  auto yupd = [&](const std::vector<int>& ks, const char* xs, const char* Gn, const char* acc) {
+    std::ostringstream e;
+    for (int k : ks) {
+      const int mi = pt.pairs[k].first;
+      e << "            {\n              float pp = " << xs << "[0][" << mi << "] * " << Gn << "[0];\n";
+      for (int r = 1; r < 4; ++r)
+        e << "              pp = fmaf(" << xs << "[" << r << "][" << mi << "], " << Gn << "[" << r << "], pp);\n";
+      for (auto& tt : pt.terms[k])
+        e << "              " << acc << "[" << Y0 + tt.my << "] = fmaf(" << fl(tt.c) << ", pp, " << acc << "[" << Y0 + tt.my
+          << "]);\n";
+      e << "            }\n";
+    }
+    return e.str();
+  };
+  o << "      {  // path " << t << ": l_in=" << q.l_in << " l_sh=" << q.l_sh << " l_out=" << q.l_out << "\n"
+    << "        const float* Sp = sS + " << off << " + zz;\n"
+    << "        const float* Sp2 = sS2 + " << off << " + zz;\n"
+    << "        (void)Sp2;\n";
+  for (int m = 0; m < DO; ++m) {
+    std::vector<int> ks;
+    for (int k = 0; k < (int)pt.pairs.size(); ++k)
+      if (pt.pairs[k].second == m) ks.push_back(k);
+    if (ks.empty()) continue;
+    o << "        {  // m_o = " << m << "\n";
+    for (int k : ks) o << "          const float M" << k << " = " << yexpr(pt.terms[k], "Y") << ";\n";
+    o << "          sb_f4 G = (sb_f4){0.f, 0.f, 0.f, 0.f};\n" << "  " << gtile("G", "Sp", "phB", m);
+    o << "          if (!DB) {\n";
+    for (int r = 0; r < 4; ++r) o << "            const float c" << r << " = " << cexpr(ks, "xv", "M", r) << ";\n";
+    o << ptile("Sp", "c", m) << xupd(ks, "M", "G") << yupd(ks, "xv", "G", "gy");
+    o << "          } else {\n";
+    for (int k : ks) o << "            float D" << k << " = 0.f;\n";
+    o << "            if (fl & 4) {\n";
+    for (int k : ks) o << "              D" << k << " = " << yexpr(pt.terms[k], "Yd") << ";\n";
+    o << "            }\n"
+      << "            sb_f4 Gd = (sb_f4){0.f, 0.f, 0.f, 0.f};\n"
+      << "            if (fl & 1) {\n" << "  " << gtile("Gd", "Sp", "phdB", m) << "            }\n"
+      << "            if (fl & 8) {\n" << "  " << gtile("Gd", "Sp2", "phB", m) << "            }\n";
+    for (int r = 0; r < 4; ++r)
+      o << "            float d" << r << " = 0.f, z" << r << " = 0.f;\n";
+    o << "            if (fl & 2) {\n";
+    for (int r = 0; r < 4; ++r) o << "              d" << r << " += " << cexpr(ks, "xdv", "M", r) << ";\n";
+    o << "            }\n            if (fl & 4) {\n";
+    for (int r = 0; r < 4; ++r) o << "              d" << r << " += " << cexpr(ks, "xv", "D", r) << ";\n";
+    o << "            }\n            if (fl & 8) {\n";
+    for (int r = 0; r < 4; ++r) o << "              z" << r << " = " << cexpr(ks, "xv", "M", r) << ";\n";
+    o << "            }\n"
+      << ptile("Sp", "d", m)
+      << "            if (fl & 8) {\n" << ptile("Sp2", "z", m) << "            }\n"
+      << "            if (HAS_GY && (fl & 9)) {\n" << yupd(ks, "xv", "Gd", "gy") << "            }\n"
+      << "            if (HAS_GY && (fl & 2)) {\n" << yupd(ks, "xdv", "G", "gy") << "            }\n"
+      << "            if (HAS_YB && (fl & 4)) {\n" << yupd(ks, "xv", "G", "yb") << "            }\n"
+      << "            if (fl & 9) {\n" << xupd(ks, "M", "Gd") << "            }\n"
+      << "            if (fl & 4) {\n" << xupd(ks, "D", "G") << "            }\n"
+      << "          }\n";
+    // pin the updated partial sums here: left alone, the compiler sinks these
+    // multiply-adds into the conditional blocks that finally use them, which
+    // keeps every G tile of the item alive until then
+    {
+      std::vector<int> mis, mys;
+      for (int k : ks) {
+        if (std::find(mis.begin(), mis.end(), pt.pairs[k].first) == mis.end()) mis.push_back(pt.pairs[k].first);
+        for (auto& tt : pt.terms[k])
+          if (std::find(mys.begin(), mys.end(), tt.my) == mys.end()) mys.push_back(tt.my);
+      }
+      for (int mi : mis)
+        for (int r = 0; r < 4; ++r) o << "          asm volatile(\"\" : \"+v\"(xc[" << r << "][" << mi << "]));\n";
+      for (int my : mys) {
+        o << "          if (HAS_GY) asm volatile(\"\" : \"+v\"(gy[" << Y0 + my << "]));\n";
+        o << "          if (HAS_YB) asm volatile(\"\" : \"+v\"(yb[" << Y0 + my << "]));\n";
+      }
+    }
+    o << "          __builtin_amdgcn_sched_barrier(0);\n"
+      << "        }\n";
+  }
+  o << "      }\n";
+}
+
+// Adjoint (backward / double-backward) code for one slab.  A wave takes 16
+// edges per iteration (edge k of the batch -> wave (k / 16) % ADJ_W, slot
+// k % 16); lane l holds slot l % 16 and channels 4 (l / 16) .. 4 (l / 16) + 3 of
+// each 16-channel tile.  The products with the staged adjoint state run on MFMA:
+//   G[e][u][m_o] = sum_q phi[e][q] Sbar[q][m_o][u]
+//     16x16x4: rows = the tile's channels, columns = edge slots, k = q;
+//   phibar[e][q] += sum_{m_o, u} Sbar[q][m_o][u] C[e][u][m_o]
+//     4x4x1 blocks of 4 lanes: rows = q, columns = the block's 4 edge slots,
+//     one channel per step;
+// and the CG contractions of each lane's 4 channels on the VALU.  Per-edge
+// partial sums are reduced over the 4 channel quads once per edge.  MFMAs run
+// with the whole wave: lanes past the last edge carry zero radial features and
+// zero channel values, never a branch around a matrix instruction.
 void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
   const AdjSlab& sl = P.slabs[s];
   const bool first = s == 0, last = s + 1 == (int)P.slabs.size();
@@ -547,33 +675,33 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        " float* sacc, float* __restrict__ gphi, float* __restrict__ gevec, float* __restrict__ contrib, int flags,"
        " bool multi) {\n"
     << "  const int fl = FL >= 0 ? FL : flags;\n"
-    << "  constexpr bool HAS_GY = !DB || FL < 0 || (FL & 11);\n"
+       "  constexpr bool HAS_GY = !DB || FL < 0 || (FL & 11);\n"
        "  constexpr bool HAS_YB = DB && (FL < 0 || (FL & 4));\n"
        "  constexpr int GY = K, YB = K + (HAS_GY ? NSH : 0);\n"
        "  constexpr int NV = K + (HAS_GY ? NSH : 0) + (HAS_YB ? NSH : 0);\n"
-       "  constexpr int U = ADJ_U, ES = ADJ_ES;\n"
-       "  const int sub = lane / U, uu = lane % U;\n"
-       "  const int niter = (nb + 4 * ES - 1) / (4 * ES);\n"
-       // sender ids of this wave's edge slots are preloaded 64 at a time (slot t ->
-       // edge k = ((t / ES) * 4 + w) * ES + t % ES) and shared through the wave, so
-       // the sender-row gather is the only dependent load of an iteration.  (Fetching
-       // the next iteration's data ahead doubles these registers and, with the slab
-       // resident in flight, drops the kernel to one wave per SIMD: measured slower.)
-       "  constexpr int SPB = 64 / ES;\n"
+       "  constexpr int KQ = KP / 4;\n"
+       "  const int es = lane & 15, g = lane >> 4, l3 = lane & 3;\n"
+       "  const int niter = (nb + 16 * ADJ_W - 1) / (16 * ADJ_W);\n"
+       // sender ids of four iterations per load (lane l -> iteration it + l / 16,
+       // slot l % 16), shared through the wave
        "  int snd;\n"
-       "  {\n    const int kk = ((lane / ES) * 4 + w) * ES + lane % ES;\n    snd = kk < nb ? sender[ebase + kk] : 0;\n  }\n"
+       "  {\n    const int kk = (g * ADJ_W + w) * 16 + es;\n    snd = kk < nb ? sender[ebase + kk] : 0;\n  }\n"
        "  for (int it = 0; it < niter; ++it) {\n"
-       "    if (it > 0 && it % SPB == 0) {\n"
-       "      const int t = it * ES + lane;\n"
-       "      const int kk = ((t / ES) * 4 + w) * ES + t % ES;\n"
+       "    if (it > 0 && (it & 3) == 0) {\n"
+       "      const int kk = ((it + g) * ADJ_W + w) * 16 + es;\n"
        "      snd = kk < nb ? sender[ebase + kk] : 0;\n"
        "    }\n"
-       "    const int jsnd = __shfl(snd, (it % SPB) * ES + sub);\n"
-       "    const int k = (it * 4 + w) * ES + sub;\n"
+       "    const int jsnd = __shfl(snd, ((it & 3) << 4) + es);\n"
+       "    const int k = (it * ADJ_W + w) * 16 + es;\n"
        "    const bool ev = k < nb;\n"
        "    const int e = ebase + k;\n"
-       "    float pv[NV];\n#pragma unroll\n    for (int v = 0; v < NV; ++v) pv[v] = 0.f;\n"
-       "    float ux = 0.f, uy = 0.f, uz = 1.f, rinv = 1.f;\n"
+       "    sb_f4 pacc[KQ];\n"
+       "#pragma unroll\n    for (int v = 0; v < KQ; ++v) pacc[v] = (sb_f4){0.f, 0.f, 0.f, 0.f};\n"
+       "    float gy[NSH], yb[NSH];\n"
+       "#pragma unroll\n    for (int v = 0; v < NSH; ++v) { gy[v] = 0.f; yb[v] = 0.f; }\n"
+       "    float ux = 0.f, uy = 0.f, uz = 1.f, rinv = 1.f, dx = 0.f, dy = 0.f, dz = 0.f;\n"
+       "    float phB[KQ], phdB[KQ];\n"
+       "#pragma unroll\n    for (int v = 0; v < KQ; ++v) { phB[v] = 0.f; phdB[v] = 0.f; }\n"
        "    // opaque zero: keeps the adjoint-state reads inside the loop (LDS), instead of\n"
        "    // hoisting the whole slab into registers\n"
        "    int zz = 0;\n    asm volatile(\"\" : \"+v\"(zz));\n"
@@ -581,86 +709,85 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        "      const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
        "      rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
        "      ux = vx * rinv; uy = vy * rinv; uz = vz * rinv;\n"
-    << "      float Y[" << NS << "];\n      sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
-    << "      float ph[K];\n#pragma unroll\n      for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
-    << "      float Yd[" << NS << "], phd[K];\n"
-    << "      if (DB && (fl & 4)) {\n"
-       "        const float dx = evdot[3 * (sb_i64)e], dy = evdot[3 * (sb_i64)e + 1], dz = evdot[3 * (sb_i64)e + 2];\n"
-    << "        sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n      }\n"
-    << "      if (DB && (fl & 1)) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) phd[q] = phidot[(sb_i64)e * K + q];\n      }\n"
-    << "      const sb_i64 srow = (sb_i64)jsnd * CXI;\n";
+       "#pragma unroll\n      for (int v = 0; v < KQ; ++v) {\n"
+       "        const int q = 4 * v + g;\n"
+       "        if (q < K) phB[v] = phi[(sb_i64)e * K + q];\n"
+       "      }\n"
+       "      if (DB && (fl & 1)) {\n"
+       "#pragma unroll\n        for (int v = 0; v < KQ; ++v) {\n"
+       "          const int q = 4 * v + g;\n"
+       "          if (q < K) phdB[v] = phidot[(sb_i64)e * K + q];\n"
+       "        }\n      }\n"
+       "      if (DB && (fl & 4)) { dx = evdot[3 * (sb_i64)e]; dy = evdot[3 * (sb_i64)e + 1]; dz = evdot[3 * (sb_i64)e + 2]; }\n"
+       "    }\n"
+    << "    float Y[" << NS << "], Yd[" << NS << "];\n    sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
+    << "    if (DB && (fl & 4)) sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n"
+    << "    const sb_i64 srow = (sb_i64)jsnd * CXI;\n";
   for (const AdjItem& it : sl.items) {
     const Irrep& ri = P.in[it.a];
     const int DA = 2 * ri.l + 1;
-    o << "      {  // input irrep " << it.a << ", channels from " << it.u0 << "\n"
-      << "        constexpr int CA = " << ri.mul << ", AOFF = " << ri.off << ", U0 = " << it.u0 << ", DA = " << DA << ";\n"
-      << "        const int u = U0 + uu;\n"
-      << "        if (u < CA) {\n"
-      << "          float xv[DA], xdv[DA], xc[DA];\n"
-      << "#pragma unroll\n          for (int m = 0; m < DA; ++m) { xv[m] = x[srow + AOFF + m * CA + u]; xc[m] = 0.f; }\n"
-      << "          if (DB && (fl & 2)) {\n#pragma unroll\n            for (int m = 0; m < DA; ++m) xdv[m] = xdot[srow + AOFF + m * CA + u];\n          }\n";
-    for (size_t pi = 0; pi < it.paths.size(); ++pi) {
-      const int t = it.paths[pi];
-      const Path& q = P.paths[t];
-      const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
-      o << "          {  // path " << t << "\n"
-        << "            constexpr int DO = " << DO << ", Y0 = " << Y0 << ";\n"
-        << "            const float* Sp = sS + " << it.lds_off[pi] << " + uu + zz;\n"
-        << "            float M[P" << t << "_NP];\n            sb_M" << t << "(Y + Y0, M);\n"
-        << "            float G[DO];\n#pragma unroll\n            for (int m = 0; m < DO; ++m) G[m] = 0.f;\n"
-        << "            if (!DB) {\n"
-        << "              float C[DO];\n              sb_C" << t << "(xv, M, C);\n"
-        << "#pragma unroll\n              for (int q = 0; q < K; ++q)\n#pragma unroll\n"
-        << "                for (int m = 0; m < DO; ++m) {\n"
-        << "                  const float sv = Sp[(q * DO + m) * U];\n"
-        << "                  G[m] = fmaf(ph[q], sv, G[m]);\n"
-        << "                  pv[q] = fmaf(sv, C[m], pv[q]);\n"
-        << "                }\n"
-        << "              sb_Y" << t << "(xv, G, pv + GY + Y0);\n"
-        << "              sb_X" << t << "(G, M, xc);\n"
-        << "            } else {\n"
-        << "              const float* Sp2 = sS2 + " << it.lds_off[pi] << " + uu + zz;\n"
-        << "              float Md[P" << t << "_NP], Cd[DO], C0[DO], Gd[DO], Ct[DO];\n"
-        << "#pragma unroll\n              for (int m = 0; m < DO; ++m) { Cd[m] = 0.f; Gd[m] = 0.f; }\n"
-        << "              if (fl & 2) { sb_C" << t << "(xdv, M, Ct); for (int m = 0; m < DO; ++m) Cd[m] += Ct[m]; }\n"
-        << "              if (fl & 4) { sb_M" << t << "(Yd + Y0, Md); sb_C" << t
-        << "(xv, Md, Ct); for (int m = 0; m < DO; ++m) Cd[m] += Ct[m]; }\n"
-        << "              if (fl & 8) sb_C" << t << "(xv, M, C0);\n"
-        << "#pragma unroll\n              for (int q = 0; q < K; ++q)\n#pragma unroll\n"
-        << "                for (int m = 0; m < DO; ++m) {\n"
-        << "                  const float sv = Sp[(q * DO + m) * U];\n"
-        << "                  G[m] = fmaf(ph[q], sv, G[m]);\n"
-        << "                  pv[q] = fmaf(sv, Cd[m], pv[q]);\n"
-        << "                  if (fl & 1) Gd[m] = fmaf(phd[q], sv, Gd[m]);\n"
-        << "                  if (fl & 8) {\n"
-        << "                    const float s2 = Sp2[(q * DO + m) * U];\n"
-        << "                    Gd[m] = fmaf(ph[q], s2, Gd[m]);\n"
-        << "                    pv[q] = fmaf(s2, C0[m], pv[q]);\n"
-        << "                  }\n"
-        << "                }\n"
-        << "              if (HAS_GY && (fl & 9)) sb_Y" << t << "(xv, Gd, pv + GY + Y0);\n"
-        << "              if (HAS_GY && (fl & 2)) sb_Y" << t << "(xdv, G, pv + GY + Y0);\n"
-        << "              if (HAS_YB && (fl & 4)) sb_Y" << t << "(xv, G, pv + YB + Y0);\n"
-        << "              if (fl & 9) sb_X" << t << "(Gd, M, xc);\n"
-        << "              if (fl & 4) sb_X" << t << "(G, Md, xc);\n"
-        << "            }\n"
+    const bool v4 = ri.mul % 4 == 0 && ri.off % 4 == 0 && P.dim_in % 4 == 0;
+    o << "    {  // input irrep " << it.a << ", channels " << it.u0 << " .. " << it.u0 + 15 << "\n"
+      << "      constexpr int CA = " << ri.mul << ", AOFF = " << ri.off << ", U0 = " << it.u0 << ", DA = " << DA << ";\n"
+      << "      const int u = U0 + 4 * g;\n"
+      << "      float xv[4][DA], xdv[4][DA], xc[4][DA];\n"
+      << "#pragma unroll\n      for (int r = 0; r < 4; ++r)\n#pragma unroll\n"
+      << "        for (int m = 0; m < DA; ++m) { xv[r][m] = 0.f; xdv[r][m] = 0.f; xc[r][m] = 0.f; }\n";
+    if (v4)
+      o << "      if (ev && u < CA) {\n"
+        << "#pragma unroll\n        for (int m = 0; m < DA; ++m) {\n"
+        << "          const sb_f4 v = *(const sb_f4*)(x + srow + AOFF + m * CA + u);\n"
+        << "          xv[0][m] = v[0]; xv[1][m] = v[1]; xv[2][m] = v[2]; xv[3][m] = v[3];\n"
+        << "        }\n"
+        << "        if (DB && (fl & 2)) {\n"
+        << "#pragma unroll\n          for (int m = 0; m < DA; ++m) {\n"
+        << "            const sb_f4 v = *(const sb_f4*)(xdot + srow + AOFF + m * CA + u);\n"
+        << "            xdv[0][m] = v[0]; xdv[1][m] = v[1]; xdv[2][m] = v[2]; xdv[3][m] = v[3];\n"
+        << "          }\n        }\n      }\n";
+    else
+      o << "      if (ev) {\n"
+        << "#pragma unroll\n        for (int r = 0; r < 4; ++r)\n"
+        << "          if (u + r < CA) {\n"
+        << "#pragma unroll\n            for (int m = 0; m < DA; ++m) xv[r][m] = x[srow + AOFF + m * CA + u + r];\n"
+        << "            if (DB && (fl & 2)) {\n"
+        << "#pragma unroll\n              for (int m = 0; m < DA; ++m) xdv[r][m] = xdot[srow + AOFF + m * CA + u + r];\n"
+        << "            }\n          }\n      }\n";
+    for (size_t pi = 0; pi < it.paths.size(); ++pi) emit_adj_path(o, P, it.paths[pi], it.lds_off[pi]);
+    o << "      if (contrib && ev) {\n"
+      << "        float* cr = contrib + (sb_i64)(e - e0) * CXI + AOFF + u;\n";
+    if (v4)
+      o << "        if (u < CA) {\n"
+        << "#pragma unroll\n          for (int m = 0; m < DA; ++m) {\n"
+        << "            sb_f4 v = (sb_f4){xc[0][m], xc[1][m], xc[2][m], xc[3][m]};\n"
+        << (it.first ? "" : "            v += *(const sb_f4*)(cr + m * CA);\n")
+        << "            *(sb_f4*)(cr + m * CA) = v;\n"
+        << "          }\n        }\n";
+    else
+      o << "#pragma unroll\n        for (int r = 0; r < 4; ++r)\n"
+        << "          if (u + r < CA) {\n"
+        << "#pragma unroll\n            for (int m = 0; m < DA; ++m) cr[m * CA + r] = "
+        << (it.first ? "xc[r][m]" : "cr[m * CA + r] + xc[r][m]") << ";\n"
         << "          }\n";
-    }
-    o << "          if (contrib) {\n"
-      << "            float* cr = contrib + (sb_i64)(e - e0) * CXI + AOFF + u;\n"
-      << "#pragma unroll\n            for (int m = 0; m < DA; ++m) cr[m * CA] = " << (it.first ? "xc[m]" : "cr[m * CA] + xc[m]")
-      << ";\n          }\n"
-      << "        }\n      }\n";
+    o << "      }\n    }\n";
   }
   if (first) {
     for (int a : P.dead_in)
-      o << "      if (contrib) for (int t = uu; t < " << P.in[a].dim() << "; t += U) contrib[(sb_i64)(e - e0) * CXI + "
+      o << "    if (contrib && ev) for (int t = g; t < " << P.in[a].dim() << "; t += 4) contrib[(sb_i64)(e - e0) * CXI + "
         << P.in[a].off << " + t] = 0.f;\n";
   }
-  o << "    }\n"
-       "#pragma unroll\n    for (int v = 0; v < NV; ++v)\n"
-       "      for (int sft = 1; sft < U; sft <<= 1) pv[v] += __shfl_xor(pv[v], sft);\n"
-       "    if (ev && uu == 0) {\n"
+  o << "    // sum the four channel quads of each edge slot\n"
+       "#pragma unroll\n    for (int v = 0; v < KQ; ++v)\n#pragma unroll\n"
+       "      for (int i = 0; i < 4; ++i) {\n"
+       "        pacc[v][i] += __shfl_xor(pacc[v][i], 16);\n"
+       "        pacc[v][i] += __shfl_xor(pacc[v][i], 32);\n"
+       "      }\n"
+       "    if (HAS_GY) {\n#pragma unroll\n      for (int v = 0; v < NSH; ++v) { gy[v] += __shfl_xor(gy[v], 16); gy[v] += __shfl_xor(gy[v], 32); }\n    }\n"
+       "    if (HAS_YB) {\n#pragma unroll\n      for (int v = 0; v < NSH; ++v) { yb[v] += __shfl_xor(yb[v], 16); yb[v] += __shfl_xor(yb[v], 32); }\n    }\n"
+       "    if (ev && g == 0) {\n"
+       "      float pv[NV];\n"
+       "#pragma unroll\n      for (int q = 0; q < K; ++q) pv[q] = pacc[q >> 2][q & 3];\n"
+       "      if (HAS_GY) {\n#pragma unroll\n        for (int v = 0; v < NSH; ++v) pv[GY + v] = gy[v];\n      }\n"
+       "      if (HAS_YB) {\n#pragma unroll\n        for (int v = 0; v < NSH; ++v) pv[YB + v] = yb[v];\n      }\n"
        "      if (multi) {\n"
        "#pragma unroll\n        for (int v = 0; v < NV; ++v) {\n"
     << "          float tv = pv[v];\n"
@@ -670,33 +797,33 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
   if (last) {
     o << "      if (gphi) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = pv[q];\n      }\n"
          "      if (gevec) {\n"
-         "        float g[3] = {0.f, 0.f, 0.f};\n"
-         "        if (HAS_GY) sb_sh_vjp(ux, uy, uz, rinv, pv + GY, g);\n"
+         "        float gg[3] = {0.f, 0.f, 0.f};\n"
+         "        if (HAS_GY) sb_sh_vjp(ux, uy, uz, rinv, pv + GY, gg);\n"
          "        if (HAS_YB && (fl & 4)) {\n"
          "          float h[3];\n"
-         "          sb_sh_hvp(ux, uy, uz, rinv, pv + YB, evdot[3 * (sb_i64)e], evdot[3 * (sb_i64)e + 1],"
-         " evdot[3 * (sb_i64)e + 2], h);\n"
-         "          g[0] += h[0]; g[1] += h[1]; g[2] += h[2];\n"
+         "          sb_sh_hvp(ux, uy, uz, rinv, pv + YB, dx, dy, dz, h);\n"
+         "          gg[0] += h[0]; gg[1] += h[1]; gg[2] += h[2];\n"
          "        }\n"
-         "        gevec[3 * (sb_i64)e] = g[0]; gevec[3 * (sb_i64)e + 1] = g[1]; gevec[3 * (sb_i64)e + 2] = g[2];\n"
+         "        gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n"
          "      }\n";
   }
   o << "    }\n  }\n}\n";
 }
 
-// Staging of one slab's adjoint-state slices (and the second slice set when dA is active).
+// Staging of one slab's adjoint-state slices (and the second slice set when dA
+// is active): [q < KP][m_o][16 channels] per path, zero past K and past C_in.
 void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* indent) {
   for (const AdjItem& it : P.slabs[s].items)
     for (size_t pi = 0; pi < it.paths.size(); ++pi) {
       const Path& q = P.paths[it.paths[pi]];
       const Group& g = P.groups[q.group];
-      const int DO = 2 * q.l_out + 1, U = P.adj_U, n = P.K * DO * U;
-      o << indent << "for (int t = tid; t < " << n << "; t += 256) {\n"
-        << indent << "  const int q = t / " << DO * U << ", r = t % " << DO * U << ", m = r / " << U << ", uc = " << it.u0
-        << " + r % " << U << ";\n"
+      const int DO = 2 * q.l_out + 1, n = P.adj_KP * DO * 16;
+      o << indent << "for (int t = tid; t < " << n << "; t += 64 * ADJ_W) {\n"
+        << indent << "  const int q = t / " << DO * 16 << ", r = t % " << DO * 16 << ", m = r / 16, uc = " << it.u0
+        << " + r % 16;\n"
+        << indent << "  const bool ok = q < K && uc < " << q.c_in << ";\n"
         << indent << "  const sb_i64 src = ncap * " << g.s_off << "LL + ((sb_i64)il * " << g.d << " + m) * " << g.D
         << "LL + " << q.koff << " + q * " << q.c_in << " + uc;\n"
-        << indent << "  const bool ok = uc < " << q.c_in << ";\n"
         << indent << "  sS[" << it.lds_off[pi] << " + t] = ok ? Sb[src] : 0.f;\n"
         << indent << "  if (DB && (fl & 8)) sS2[" << it.lds_off[pi] << " + t] = ok ? Sb2[src] : 0.f;\n"
         << indent << "}\n";
@@ -714,7 +841,7 @@ std::string generate_source(const Plan& P) {
   for (auto& r : P.out) o << r.mul << "x" << r.l << (r.p > 0 ? "e" : "o") << " ";
   o << "norm=" << P.norm << "\n";
   o << "#define K " << P.K << "\n#define NSH " << P.nsh << "\n#define CXI " << P.dim_in << "\n#define CXO " << P.dim_out
-    << "\n#define EB " << P.bwd_eb << "\n#define ADJ_U " << P.adj_U << "\n#define ADJ_ES " << P.adj_ES << "\n";
+    << "\n#define EB " << P.bwd_eb << "\n#define KP " << P.adj_KP << "\n#define ADJ_W " << P.adj_waves << "\n";
   emit_sh(o, P.lmax);
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
 
@@ -742,8 +869,9 @@ std::string generate_source(const Plan& P) {
     o << "  }\n}\n";
   }
 
-  // adjoint edge kernels: one block per receiver, adjoint state staged in LDS
-  // slab by slab, every wave owning a disjoint set of the receiver's edges
+  // adjoint edge kernels: one block of ADJ_W waves per receiver, adjoint state
+  // staged in LDS slab by slab, every wave owning a disjoint set of the
+  // receiver's edges
   for (int s = 0; s < (int)P.slabs.size(); ++s) emit_adj_slab(o, P, s);
   const int LDSF = std::max(1, P.bwd_lds_max);
   const int NSL = (int)P.slabs.size();
@@ -780,13 +908,13 @@ std::string generate_source(const Plan& P) {
   struct KV { const char* name; bool db; int fl; int lds_mult; };
   const KV kvs[] = {{"sobek_bwd_E", false, 0, 1}, {"sobek_dbwd_E_r", true, 4, 1}, {"sobek_dbwd_E", true, -1, 2}};
   for (const KV& kv : kvs) {
-    o << "extern \"C\" __global__ __launch_bounds__(256) void " << kv.name
+    o << "extern \"C\" __global__ __launch_bounds__(" << 64 * P.adj_waves << ") __attribute__((amdgpu_waves_per_eu(2))) void " << kv.name
       << "(const int* __restrict__ rowptr, const int* __restrict__ sender, const float* __restrict__ evec,"
          " const float* __restrict__ phi, const float* __restrict__ x, const float* __restrict__ Sb,"
          " const float* __restrict__ Sb2, const float* __restrict__ xdot, const float* __restrict__ evdot,"
          " const float* __restrict__ phidot, float* __restrict__ gphi, float* __restrict__ gevec,"
          " float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags) {\n"
-      << "  __shared__ float sS[" << LDSF * kv.lds_mult << "];\n";
+      << "  __shared__ __attribute__((aligned(16))) float sS[" << LDSF * kv.lds_mult << "];\n";
     if (NSL > 1)
       o << "  __shared__ float sacc[EB * SB_ADJ_NV(" << (kv.db ? "true" : "false") << ", " << kv.fl << ")];\n";
     else

@@ -35,9 +35,9 @@ struct Path {
 struct Group {
   int i_out, l, d, C, off;
   std::vector<int> paths;
-  int64_t D;      // K * sum of C_in over the group's paths
-  int64_t s_off;  // per-receiver offset of the group block (floats) = sum of d*D of earlier groups
-  int64_t ktab_off;  // offset of this group's k-table in Plan::ktab
+  int64_t D = 0;  // K * sum of C_in over the group's paths
+  int64_t s_off = 0;  // per-receiver offset of the group block (floats) = sum of d*D of earlier groups
+  int64_t ktab_off = 0;  // offset of this group's k-table in Plan::ktab
 };
 
 // A wave's share of the forward state kernel: input irrep a, channel block
@@ -49,11 +49,12 @@ struct Unit {
   std::vector<int> paths;
 };
 
-// Adjoint edge kernels: one lane mapping for the whole plan (lane = sub * adj_U + uu,
-// adj_ES = 64 / adj_U edges in flight per wave); every wave owns a disjoint set of
-// edges and runs every item of a slab for them.  An item is (input irrep a,
-// channel block starting at u0, paths with input a); its adjoint-state slices are
-// staged in LDS as [path][q][m_o][uu].
+// Adjoint edge kernels: a wave takes 16 edges at a time.  Lane l holds edge
+// slot l % 16 and the channel quad l / 16 of a 16-channel tile; the products
+// with the staged adjoint state run on fp32 MFMA (16x16x4 for the q-contraction
+// G = phi Sbar, 4x4x1 blocks for the channel contraction <Sbar, C>).  An item is
+// (input irrep a, tile starting at channel u0, paths with input a); its
+// adjoint-state slices are staged in LDS as [path][q < KP][m_o][16 channels].
 struct AdjItem {
   int a, u0;
   std::vector<int> paths;
@@ -86,7 +87,9 @@ struct Plan {
   int64_t srow = 0;  // floats of receiver state per receiver (sum over groups of d * D)
   std::vector<int32_t> ktab;   // host copy of all groups' k-tables
   std::vector<Unit> fwd_units;
-  int adj_U = 64, adj_ES = 1;   // adjoint lane mapping
+  int adj_U = 16;               // channels per adjoint tile
+  int adj_KP = 4;               // K rounded up to a multiple of 4
+  int adj_waves = 2;            // waves per adjoint block (16 edges each per iteration)
   std::vector<AdjSlab> slabs;
   int bwd_eb = 64;              // edges per batch when the adjoint state needs several slabs
   int bwd_lds_max = 0;          // largest slab (floats)
