@@ -812,22 +812,54 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
 
 // Staging of one slab's adjoint-state slices (and the second slice set when dA
 // is active): [q < KP][m_o][16 channels] per path, zero past K and past C_in.
+// Every load of the slab is issued before the first LDS write, so a block pays
+// one memory round trip for its receiver's state instead of one per element.
+// With every multiplicity a multiple of 4 the copy moves float4s (a channel
+// quad never straddles C_in and every source offset is 16-byte aligned).
 void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* indent) {
+  const int NT = 64 * P.adj_waves;
+  struct Sl { const Path* q; const Group* g; int u0, off, DO; };
+  std::vector<Sl> sls;
   for (const AdjItem& it : P.slabs[s].items)
     for (size_t pi = 0; pi < it.paths.size(); ++pi) {
       const Path& q = P.paths[it.paths[pi]];
-      const Group& g = P.groups[q.group];
-      const int DO = 2 * q.l_out + 1, n = P.adj_KP * DO * 16;
-      o << indent << "for (int t = tid; t < " << n << "; t += 64 * ADJ_W) {\n"
-        << indent << "  const int q = t / " << DO * 16 << ", r = t % " << DO * 16 << ", m = r / 16, uc = " << it.u0
-        << " + r % 16;\n"
-        << indent << "  const bool ok = q < K && uc < " << q.c_in << ";\n"
-        << indent << "  const sb_i64 src = ncap * " << g.s_off << "LL + ((sb_i64)il * " << g.d << " + m) * " << g.D
-        << "LL + " << q.koff << " + q * " << q.c_in << " + uc;\n"
-        << indent << "  sS[" << it.lds_off[pi] << " + t] = ok ? Sb[src] : 0.f;\n"
-        << indent << "  if (DB && (fl & 8)) sS2[" << it.lds_off[pi] << " + t] = ok ? Sb2[src] : 0.f;\n"
-        << indent << "}\n";
+      sls.push_back({&q, &P.groups[q.group], it.u0, it.lds_off[pi], 2 * q.l_out + 1});
     }
+  const int W = P.vec4 ? 4 : 1;  // floats per copy unit
+  auto src_expr = [&](const Sl& x, const std::string& t) {
+    std::ostringstream e;
+    const int per_q = x.DO * 16 / W;   // copy units per q row
+    e << "const int q = " << t << " / " << per_q << ", r = " << t << " % " << per_q << ", m = r / " << 16 / W
+      << ", uc = " << x.u0 << " + " << W << " * (r % " << 16 / W << ");\n"
+      << indent << "    const bool ok = q < K && uc < " << x.q->c_in << ";\n"
+      << indent << "    const sb_i64 src = ncap * " << x.g->s_off << "LL + ((sb_i64)il * " << x.g->d << " + m) * " << x.g->D
+      << "LL + " << x.q->koff << " + q * " << x.q->c_in << " + uc;\n";
+    return e.str();
+  };
+  const char* T = W == 4 ? "sb_f4" : "float";
+  const char* Z = W == 4 ? "(sb_f4){0.f, 0.f, 0.f, 0.f}" : "0.f";
+  for (int pass = 0; pass < 2; ++pass) {   // pass 0: Sbar, pass 1: Sbar' (dA active)
+    const char* src = pass ? "Sb2" : "Sb";
+    const char* dst = pass ? "sS2" : "sS";
+    o << indent << (pass ? "if (DB && (fl & 8)) {\n" : "{\n");
+    int reg = 0;
+    std::ostringstream stores;
+    for (const Sl& x : sls) {
+      const int n = P.adj_KP * x.DO * 16 / W;
+      for (int j = 0; j * NT < n; ++j, ++reg) {
+        const std::string t = "t" + std::to_string(reg);
+        o << indent << "  " << T << " v" << reg << " = " << Z << ";\n"
+          << indent << "  const int " << t << " = tid + " << j * NT << ";\n"
+          << indent << "  if (" << t << " < " << n << ") {\n"
+          << indent << "    " << src_expr(x, t)
+          << indent << "    if (ok) v" << reg << " = " << (W == 4 ? "*(const sb_f4*)(" : "*(") << src << " + src);\n"
+          << indent << "  }\n";
+        stores << indent << "  if (" << t << " < " << n << ") *(" << T << "*)(" << dst << " + " << x.off << " + " << W
+               << " * " << t << ") = v" << reg << ";\n";
+      }
+    }
+    o << stores.str() << indent << "}\n";
+  }
 }
 
 }  // namespace
