@@ -156,6 +156,31 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float *x, const flo
                    const float *phi, const float *W, const float *gout, float *gx, float *gevec,
                    float *gphi, float *gW, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Retained receiver state (Section 4.3: the weight gradient needs S; it is kept
+ * from the forward when it fits, else recomputed).  sobek_state_size gives the
+ * bytes of the state of every receiver of a graph: N * (sum over output groups
+ * of (2l+1) * K * sum of C_in of the group's paths) floats, in a library-defined
+ * order that callers treat as opaque.  It is bounded by the node count, never
+ * by the edge count.
+ *
+ * sobek_conv_fwd_save is sobek_conv_fwd that also leaves S of every receiver in
+ * `state` (caller-owned device memory of sobek_state_size bytes, 16-byte
+ * aligned; overwritten).  sobek_conv_bwd_saved is sobek_conv_bwd that reads
+ * the weight gradient's S from such a state instead of recomputing it; the
+ * state must come from sobek_conv_fwd_save with the same plan, graph, x, evec
+ * and phi (W may differ: S does not depend on it).  Both take the workspace
+ * of their pass (sobek_workspace_size with SOBEK_PASS_FWD / SOBEK_PASS_BWD);
+ * results agree with sobek_conv_fwd / sobek_conv_bwd within rounding (the
+ * weight gradient's summation splits differ). */
+int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t *bytes);
+int sobek_conv_fwd_save(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                        const float *phi, const float *W, float *out, float *state, void *ws,
+                        size_t ws_bytes, hipStream_t stream);
+int sobek_conv_bwd_saved(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                         const float *phi, const float *W, const float *gout, const float *state,
+                         float *gx, float *gevec, float *gphi, float *gW, void *ws, size_t ws_bytes,
+                         hipStream_t stream);
+
 /* Double backward (Sections 3.3 and 4.4): vector-Jacobian product of the
  * backward map (gout, x, evec, phi, W) -> (gx, gevec, gphi, gW) with
  * cotangents t_gx [N][dim_in], t_gevec [E][3], t_gphi [E][K], t_gW [K][n_weights]

@@ -140,23 +140,53 @@ def _ws(plan, graph, pass_, ws, budget):
     return ws
 
 
-def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0):
+def state_floats(plan, graph):
+    """Length of the retained receiver state of `graph` (fp32 elements; node-bounded)."""
+    nb = ctypes.c_size_t()
+    check(lib().sobek_state_size(plan.handle, graph.handle, ctypes.byref(nb)))
+    return int(nb.value) // 4
+
+
+def new_state(plan, graph, device=None):
+    """An uninitialised buffer for the retained receiver state."""
+    return torch.empty(max(state_floats(plan, graph), 4), dtype=torch.float32,
+                       device=device or graph.rowptr.device)
+
+
+def _check_state(plan, graph, state):
+    if state is not None:
+        _check_tensor(state, "state", (state.numel(),))
+        if state.numel() < state_floats(plan, graph):
+            raise ValueError("state buffer is smaller than sobek_state_size")
+
+
+def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=None):
+    """m = conv(x, evec, phi, W); with `state` (from new_state) S of every receiver is kept in it."""
     N, E = graph.N, graph.E
     _check_tensor(x, "x", (N, plan.dim_in))
     _check_tensor(evec, "evec", (E, 3))
     _check_tensor(phi, "phi", (E, plan.K))
     _check_tensor(W, "W", (plan.K, plan.n_weights))
+    _check_state(plan, graph, state)
     if out is None:
         out = torch.empty(N, plan.dim_out, dtype=torch.float32, device=x.device)
     _check_tensor(out, "out", (N, plan.dim_out))
     ws = _ws(plan, graph, "fwd", ws, budget)
-    check(lib().sobek_conv_fwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(out),
-                               _ptr(ws), ws.numel(), _stream()))
+    if state is None:
+        check(lib().sobek_conv_fwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(out),
+                                   _ptr(ws), ws.numel(), _stream()))
+    else:
+        check(lib().sobek_conv_fwd_save(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W),
+                                        _ptr(out), _ptr(state), _ptr(ws), ws.numel(), _stream()))
     return out
 
 
-def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), ws=None, budget=0):
-    """(gx, gevec, gphi, gW); entries not in `need` are None."""
+def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), ws=None, budget=0, state=None):
+    """(gx, gevec, gphi, gW); entries not in `need` are None.
+
+    `state`: the retained receiver state of conv_fwd(..., state=...) with the same x, evec and phi; the
+    weight gradient then reads it instead of recomputing S.
+    """
     N, E = graph.N, graph.E
     _check_tensor(x, "x", (N, plan.dim_in))
     _check_tensor(evec, "evec", (E, 3))
@@ -166,9 +196,15 @@ def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), 
     dev = x.device
     shapes = [(N, plan.dim_in), (E, 3), (E, plan.K), (plan.K, plan.n_weights)]
     outs = [torch.empty(s, dtype=torch.float32, device=dev) if n else None for s, n in zip(shapes, need)]
+    _check_state(plan, graph, state)
     ws = _ws(plan, graph, "bwd", ws, budget)
-    check(lib().sobek_conv_bwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(gout),
-                               *[_ptr(o) for o in outs], _ptr(ws), ws.numel(), _stream()))
+    if state is None:
+        check(lib().sobek_conv_bwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(gout),
+                                   *[_ptr(o) for o in outs], _ptr(ws), ws.numel(), _stream()))
+    else:
+        check(lib().sobek_conv_bwd_saved(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W),
+                                         _ptr(gout), _ptr(state), *[_ptr(o) for o in outs], _ptr(ws), ws.numel(),
+                                         _stream()))
     return tuple(outs)
 
 
@@ -205,34 +241,38 @@ def _c(t):
 
 class _TPConvBackward(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x, evec, phi, W, gout, plan, graph):
+    def forward(ctx, x, evec, phi, W, gout, plan, graph, state):
         ctx.plan, ctx.graph = plan, graph
         ctx.save_for_backward(x, evec, phi, W, gout)
-        return conv_bwd(plan, graph, x, evec, phi, W, gout)
+        return conv_bwd(plan, graph, x, evec, phi, W, gout, state=state)
 
     @staticmethod
     def backward(ctx, t_gx, t_gevec, t_gphi, t_gW):
         x, evec, phi, W, gout = ctx.saved_tensors
         g_gout, g_x, g_evec, g_phi, g_W = conv_dbwd(ctx.plan, ctx.graph, x, evec, phi, W, gout, _c(t_gx),
                                                     _c(t_gevec), _c(t_gphi), _c(t_gW))
-        return g_x, g_evec, g_phi, g_W, g_gout, None, None
+        return g_x, g_evec, g_phi, g_W, g_gout, None, None, None
 
 
 class TPConv(torch.autograd.Function):
     """m = conv(x, evec, phi, W) with first and second derivatives through the library."""
 
     @staticmethod
-    def forward(ctx, x, evec, phi, W, plan, graph):
+    def forward(ctx, x, evec, phi, W, plan, graph, retain_state):
         ctx.plan, ctx.graph = plan, graph
         ctx.save_for_backward(x, evec, phi, W)
-        return conv_fwd(plan, graph, x, evec, phi, W)
+        ctx.state = new_state(plan, graph, x.device) if retain_state else None
+        return conv_fwd(plan, graph, x, evec, phi, W, state=ctx.state)
 
     @staticmethod
     def backward(ctx, gout):
         x, evec, phi, W = ctx.saved_tensors
-        gx, gevec, gphi, gW = _TPConvBackward.apply(x, evec, phi, W, gout.contiguous(), ctx.plan, ctx.graph)
-        return gx, gevec, gphi, gW, None, None
+        gx, gevec, gphi, gW = _TPConvBackward.apply(x, evec, phi, W, gout.contiguous(), ctx.plan, ctx.graph,
+                                                    ctx.state)
+        return gx, gevec, gphi, gW, None, None, None
 
 
-def tp_conv(plan, graph, x, evec, phi, W):
-    return TPConv.apply(x, evec, phi, W, plan, graph)
+def tp_conv(plan, graph, x, evec, phi, W, retain_state=False):
+    """Differentiable convolution.  retain_state=True keeps S of every receiver from the forward (memory
+    N * sobek_state_size / N) so that the backward's weight gradient does not recompute it."""
+    return TPConv.apply(x, evec, phi, W, plan, graph, bool(retain_state))

@@ -50,12 +50,28 @@ def build_library(verbose=False):
     return LIB
 
 
-def prewarm(signatures):
-    """JIT-compile kernels for (irreps_in, lmax, irreps_out, K[, layout, norm]) signatures."""
+def _compile_one(sig):
     sys.path.insert(0, ROOT)
     from paper_2607_18074_amd import _lib
-    for sig in signatures:
-        _lib.jit_compile(*sig)
+    _lib.jit_compile(*sig)
+    return sig
+
+
+def prewarm(signatures, jobs=None):
+    """JIT-compile kernels for (irreps_in, lmax, irreps_out, K[, layout, norm]) signatures.
+
+    Each signature compiles in a process of its own (hipRTC holds one compilation per
+    process at a time); the code-object cache publishes every result atomically.
+    """
+    import multiprocessing as mp
+    jobs = jobs or max(1, min(len(signatures), 4, os.cpu_count() or 1))
+    if jobs == 1:
+        for sig in signatures:
+            _compile_one(sig)
+        return
+    with mp.get_context("spawn").Pool(jobs) as pool:
+        for _ in pool.imap_unordered(_compile_one, signatures):
+            pass
 
 
 if __name__ == "__main__":

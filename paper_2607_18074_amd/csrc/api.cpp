@@ -197,14 +197,17 @@ int nsplit_for(const sobek::Group& g, int64_t nrows, bool vec4) {
   return (int)ns;
 }
 
+// split partials of the weight-gradient GEMMs: one region per output group,
+// accumulated over the receiver chunks of a pass and reduced once at its end
 size_t partial_floats(const Plan& p, int64_t ncap) {
   size_t m = 0;
-  for (auto& g : p.groups) m = std::max(m, (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C);
+  for (auto& g : p.groups) m += (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C;
   return m;
 }
 
 // fixed part + per-receiver + per-edge bytes of a pass
-void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, WsPlan& w, size_t& per_recv, size_t& per_edge) {
+void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, int nstate, WsPlan& w, size_t& per_recv,
+                size_t& per_edge) {
   const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes); return at; };
@@ -220,7 +223,7 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, WsPlan& w, size
   w.fixed = o;
   // receiver-state slots: one, reused phase by phase (S, then Sbar); the double
   // backward needs a second one for Sbar' when dA is active
-  w.nstate = pass == SOBEK_PASS_DBWD ? 2 : 1;
+  w.nstate = nstate >= 0 ? nstate : (pass == SOBEK_PASS_DBWD ? 2 : 1);
   per_recv = (size_t)w.nstate * p.srow * 4;
   per_edge = pass == SOBEK_PASS_FWD ? 0 : (size_t)p.dim_in * 4;
 }
@@ -235,9 +238,12 @@ size_t layout_total(const Plan& p, WsPlan& w, int pass) {
   return o;
 }
 
-int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_bytes, WsPlan& w, bool sizing_only) {
+// nstate: receiver-state slots per receiver (-1: the pass's general need; the
+// forward with a retained state needs none, the double backward without dA one)
+int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_bytes, WsPlan& w, bool sizing_only,
+                   int nstate = -1) {
   size_t per_recv, per_edge;
-  pass_costs(p, G, pass, w, per_recv, per_edge);
+  pass_costs(p, G, pass, nstate, w, per_recv, per_edge);
   const int64_t N = G.N, E = G.E;
   // try a single chunk, else split the remaining bytes between state and contributions
   w.ncap = std::max<int64_t>(1, N);
@@ -370,24 +376,33 @@ int run_sbar(const Plan& p, const Chunk& c, const WsPlan& w, const float* M, con
   return SOBEK_OK;
 }
 
-// gW (first ? = : +=) S_g^T mbar_g, deterministic split reduction
-int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float* S, const float* M, float* gW,
-           int first, hipStream_t s) {
+// gW = sum over the pass's chunks of S_g^T mbar_g, deterministic: each chunk adds
+// its rows into fixed split partials (chunk 0 overwrites them), and after the
+// last chunk the splits are summed in fixed order into W's layout
+// S holds the state of receivers [c.r0, c.r0 + c.n) at row 0 of each group block,
+// group blocks s_ncap receivers apart (the chunk slot, or a retained full state).
+int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float* S, int64_t s_ncap, const float* M,
+           float* gW, bool first_chunk, bool last_chunk, hipStream_t s) {
   float* P = (float*)((char*)ws + w.off_P);
   for (auto& g : p.groups) {
-    const float* Sg = S + (size_t)w.ncap * g.s_off;
+    const float* Sg = S + (size_t)s_ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     int ns = nsplit_for(g, (int64_t)w.ncap * g.d, p.vec4);
     int rps = (int)(((int64_t)cdiv(nrows, ns) + 31) / 32 * 32);
     int bn = gemm_bn(g.C);
+    int acc = first_chunk ? 0 : 1;
     if (p.vec4)
       LAUNCH(p.k.gemm_ga_v[bn_index(bn)], cdiv(D, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
-             rps);
+             rps, acc);
     else
       LAUNCH(p.k.gemm_ga[bn_index(bn)], cdiv(D, 64), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
-             rps);
-    LAUNCH(p.k.ga_reduce, cdiv((int64_t)D * Cg, 256), 1, 1, s, (const float*)P, ns, D, Cg,
-           (const int*)(p.d_ktab + g.ktab_off), gW, first);
+             rps, acc);
+    if (last_chunk) {
+      int one = 1;
+      LAUNCH(p.k.ga_reduce, cdiv((int64_t)D * Cg, 256), 1, 1, s, (const float*)P, ns, D, Cg,
+             (const int*)(p.d_ktab + g.ktab_off), gW, one);
+    }
+    P += (size_t)ns * g.D * g.C;
   }
   return SOBEK_OK;
 }
@@ -689,16 +704,23 @@ int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t bu
   return SOBEK_OK;
 }
 
-int sobek_conv_fwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
-                   const float* W, float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Forward; with `state` non-NULL the receiver state of every receiver is
+// computed into it in one pass (and kept), otherwise chunk by chunk in the workspace.
+int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                  const float* W, float* out, float* state, void* ws, size_t ws_bytes, hipStream_t stream) {
   int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
   if (rc) return rc;
   if (!out && graph->N) return fail(SOBEK_E_INVALID, "out is NULL");
   if (out && !aligned16(out)) return fail(SOBEK_E_ALIGN, "out is not 16-byte aligned");
   const Plan& p = plan->p;
   const sobek_graph_s& G = *graph;
+  if (state && !aligned16(state)) return fail(SOBEK_E_ALIGN, "state is not 16-byte aligned");
   WsPlan w;
-  if ((rc = plan_workspace(p, G, SOBEK_PASS_FWD, ws_bytes, w, false))) return rc;
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_FWD, ws_bytes, w, false, state ? 0 : -1))) return rc;
   if (G.N == 0) return SOBEK_OK;
   const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
   const float* xk = x;
@@ -708,7 +730,7 @@ int sobek_conv_fwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
     ok = (float*)((char*)ws + w.off_out);
     if ((rc = transpose(p, x, (float*)xk, G.N, true, 0, stream))) return rc;
   }
-  float* S = state_ptr(w, ws, p, 0);
+  float* S = state ? state : state_ptr(w, ws, p, 0);  // a retained state is one chunk of all N receivers
   for (auto& c : w.chunks) {
     if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
     if ((rc = run_mix(p, c, w, S, W, ok, 0, stream))) return rc;
@@ -718,9 +740,11 @@ int sobek_conv_fwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
   return SOBEK_OK;
 }
 
-int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
-                   const float* W, const float* gout, float* gx, float* gevec, float* gphi, float* gW, void* ws,
-                   size_t ws_bytes, hipStream_t stream) {
+// Backward; with `state` non-NULL (the retained state of conv_fwd_impl) the weight
+// gradient reads it in one pass instead of recomputing S chunk by chunk.
+int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                  const float* W, const float* gout, const float* state, float* gx, float* gevec, float* gphi,
+                  float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
   int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
   if (rc) return rc;
   if (!gout && graph->N) return fail(SOBEK_E_INVALID, "gout is NULL");
@@ -747,11 +771,15 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
   float* Sb = S;  // the same slot: S is consumed by the weight-gradient GEMM first
   float* contrib = gx ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = gx || gevec || gphi;
+  if (gW && state) {
+    const Chunk all{0, (int)G.N, 0, G.E};
+    if ((rc = run_ga(p, all, w, ws, state, G.N, gk, gW, true, true, stream))) return rc;
+  }
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
-    if (gW) {
+    if (gW && !state) {
       if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
-      if ((rc = run_ga(p, c, w, ws, S, gk, gW, 0, stream))) return rc;
+      if ((rc = run_ga(p, c, w, ws, S, w.ncap, gk, gW, ci == 0, ci + 1 == w.chunks.size(), stream))) return rc;
     }
     if (edge) {
       if ((rc = run_sbar(p, c, w, gk, W, Sb, stream))) return rc;
@@ -765,6 +793,41 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
   }
   if (mulir && gx && (rc = transpose(p, gxk, gx, G.N, true, 1, stream))) return rc;
   return SOBEK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t* bytes) {
+  if (!plan || !graph || !bytes) return fail(SOBEK_E_INVALID, "NULL argument");
+  *bytes = (size_t)graph->N * plan->p.srow * 4;
+  return SOBEK_OK;
+}
+
+int sobek_conv_fwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                   const float* W, float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return conv_fwd_impl(plan, graph, x, evec, phi, W, out, nullptr, ws, ws_bytes, stream);
+}
+
+int sobek_conv_fwd_save(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                        const float* W, float* out, float* state, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!state && graph && graph->N) return fail(SOBEK_E_INVALID, "state is NULL");
+  return conv_fwd_impl(plan, graph, x, evec, phi, W, out, state, ws, ws_bytes, stream);
+}
+
+int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                   const float* W, const float* gout, float* gx, float* gevec, float* gphi, float* gW, void* ws,
+                   size_t ws_bytes, hipStream_t stream) {
+  return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, nullptr, gx, gevec, gphi, gW, ws, ws_bytes, stream);
+}
+
+int sobek_conv_bwd_saved(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                         const float* W, const float* gout, const float* state, float* gx, float* gevec, float* gphi,
+                         float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!state && graph && graph->N) return fail(SOBEK_E_INVALID, "state is NULL");
+  if (state && !aligned16(state)) return fail(SOBEK_E_ALIGN, "state is not 16-byte aligned");
+  return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, state, gx, gevec, gphi, gW, ws, ws_bytes, stream);
 }
 
 int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
@@ -781,7 +844,8 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const fl
   const Plan& p = plan->p;
   const sobek_graph_s& G = *graph;
   WsPlan w;
-  if ((rc = plan_workspace(p, G, SOBEK_PASS_DBWD, ws_bytes, w, false))) return rc;
+  // the second state slot (Sbar') is needed only with a dA cotangent
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_DBWD, ws_bytes, w, false, t_gW ? 2 : 1))) return rc;
   const int flags = (t_gphi ? 1 : 0) | (t_gx ? 2 : 0) | (t_gevec ? 4 : 0) | (t_gW ? 8 : 0);
   const bool tan = flags & 7;
   if (g_W) { if ((rc = fill_zero(p, g_W, (int64_t)p.K * p.n_w, stream))) return rc; }
@@ -815,7 +879,8 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const fl
     if (tan && (g_gout || g_W)) {
       if ((rc = run_state(p, G, c, w, dS, true, xk, evec, phi, txk, t_gevec, t_gphi, flags & 7, stream))) return rc;
       if (g_gout && (rc = run_mix(p, c, w, dS, W, ggk, 0, stream))) return rc;
-      if (g_W && (rc = run_ga(p, c, w, ws, dS, gk, g_W, 0, stream))) return rc;
+      if (g_W && (rc = run_ga(p, c, w, ws, dS, w.ncap, gk, g_W, ci == 0, ci + 1 == w.chunks.size(), stream)))
+        return rc;
     }
     if (t_gW && g_gout) {  // S reuses the slot once dS has been consumed
       if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;

@@ -128,7 +128,8 @@ SB_DEV void sb_gemm_sbar(const float* __restrict__ M, int nrows, int D, const fl
 
 template <int BN>
 SB_DEV void sb_gemm_ga(const float* __restrict__ S, int nrows, int D, const float* __restrict__ M,
-                       float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split) {
+                       float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split,
+                       int accumulate) {
   __shared__ float sA[SB_BK][SB_BM + 4];
   __shared__ float sB[SB_BK][BN + 4];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -164,7 +165,10 @@ SB_DEV void sb_gemm_ga(const float* __restrict__ S, int nrows, int D, const floa
     for (int r = 0; r < 4; ++r) {
       int k = kb + 16 * wave + 4 * (lane >> 4) + r;
       int col = cb + 16 * t + (lane & 15);
-      if (k < D && col < Cg) P[((sb_i64)split * D + k) * Cg + col] = acc[t][r];
+      if (k < D && col < Cg) {
+        float* o = P + ((sb_i64)split * D + k) * Cg + col;
+        *o = accumulate ? (*o + acc[t][r]) : acc[t][r];
+      }
     }
 }
 
@@ -181,8 +185,8 @@ SB_DEV void sb_gemm_ga(const float* __restrict__ S, int nrows, int D, const floa
   }                                                                                                \
   extern "C" __global__ __launch_bounds__(256) void sobek_gemm_ga_##BN(                            \
       const float* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \
-      int r0, int rows_per_split) {                                                                \
-    sb_gemm_ga<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split);                        \
+      int r0, int rows_per_split, int accumulate) {                                                \
+    sb_gemm_ga<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split, accumulate);            \
   }
 
 SB_GEMM_ENTRY(16)
@@ -367,7 +371,8 @@ SB_DEV void sb_gemm_sbar_v(const float* __restrict__ M, int nrows, int D, const 
 // P[split, k, w] = sum_{r in split} S[r, k] mbar(r, w); 128 k-rows x BN columns per block
 template <int BN>
 SB_DEV void sb_gemm_ga_v(const float* __restrict__ S, int nrows, int D, const float* __restrict__ M,
-                         float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split) {
+                         float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split,
+                         int accumulate) {
   __shared__ float sA[SB_VK][SB_VM + 4];
   __shared__ float sB[SB_VK][BN + 4];
   constexpr int NB = (SB_VK * BN / 4 + 255) / 256;
@@ -443,7 +448,10 @@ SB_DEV void sb_gemm_ga_v(const float* __restrict__ S, int nrows, int D, const fl
       for (int r = 0; r < 4; ++r) {
         const int k = kb + 32 * wave + 16 * i + 4 * (lane >> 4) + r;
         const int col = cb + 16 * t + (lane & 15);
-        if (k < D && col < Cg) P[((sb_i64)split * D + k) * Cg + col] = acc[i][t][r];
+        if (k < D && col < Cg) {
+          float* o = P + ((sb_i64)split * D + k) * Cg + col;
+          *o = accumulate ? (*o + acc[i][t][r]) : acc[i][t][r];
+        }
       }
 }
 
@@ -455,8 +463,8 @@ SB_DEV void sb_gemm_ga_v(const float* __restrict__ S, int nrows, int D, const fl
   }                                                                                                \
   extern "C" __global__ __launch_bounds__(256) void sobek_gemm_ga_v##BN(                            \
       const float* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \
-      int r0, int rows_per_split) {                                                                \
-    sb_gemm_ga_v<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split);                      \
+      int r0, int rows_per_split, int accumulate) {                                                \
+    sb_gemm_ga_v<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split, accumulate);          \
   }
 
 SB_GEMM_V_ENTRY(16)
@@ -475,8 +483,18 @@ extern "C" __global__ __launch_bounds__(256) void sobek_ga_reduce(const float* P
   sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
   if (t >= (sb_i64)D * Cg) return;
   int k = (int)(t / Cg), w = (int)(t % Cg);
+  const sb_i64 stride = (sb_i64)D * Cg;
+  const float* src = P + t;
   float s = 0.f;
-  for (int p = 0; p < nsplit; ++p) s += P[((sb_i64)p * D + k) * Cg + w];
+  int p = 0;
+  for (; p + 8 <= nsplit; p += 8) {  // eight loads in flight, added in split order
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = src[(p + i) * stride];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += v[i];
+  }
+  for (; p < nsplit; ++p) s += src[p * stride];
   float* o = gW + (sb_i64)ktab[k] + w;
   *o = first ? s : (*o + s);
 }
@@ -487,38 +505,67 @@ extern "C" __global__ __launch_bounds__(256) void sobek_ga_reduce(const float* P
 // order, so each sender's edges inside a chunk continue where the previous chunk
 // stopped: cursor[j] keeps that position.  first: chunk 0 overwrites every row
 // and initialises the cursors.
-extern "C" __global__ __launch_bounds__(256) void sobek_sender_reduce(const int* send_rowptr, const int* send_perm,
-                                                                      const float* contrib, float* gx, int* cursor,
-                                                                      int N, int CX, int e0, int e1, int first) {
+//
+// The wave reads 64 sender-CSR slots at once (one per lane); the edge ids of
+// the chunk are handed to the whole wave with readlane, and the rows of four
+// edges are loaded before they are added (in edge order), so every lane keeps
+// several row loads in flight.  Lane l owns the float4 columns l, l + 64, ... of
+// the row (CX a multiple of 4) or the scalar columns l, l + 64, ... (otherwise).
+template <int CX>
+SB_DEV void sb_sender_reduce(const int* __restrict__ send_rowptr, const int* __restrict__ send_perm,
+                             const float* __restrict__ contrib, float* __restrict__ gx, int* __restrict__ cursor,
+                             int N, int e0, int e1, int first) {
+  constexpr bool V4 = (CX % 4) == 0;
+  constexpr int W = V4 ? 4 : 1;             // floats per lane access
+  constexpr int NC = CX / W;                // accesses per row
+  constexpr int R = (NC + 63) / 64;         // accesses per lane per row
+  typedef float vt __attribute__((ext_vector_type(W)));
   const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (j >= N) return;
   const int start = first ? send_rowptr[j] : cursor[j];
   const int lim = send_rowptr[j + 1];
-  // the chunk's edges of this sender form a prefix of [start, lim): find its length
+  vt acc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[r] = (vt)(0.f);
+  auto row = [&](int e, int r) -> vt {
+    const int c = lane + 64 * r;
+    return c < NC ? *(const vt*)(contrib + (sb_i64)(e - e0) * CX + W * c) : (vt)(0.f);
+  };
   int n = 0;
   for (;;) {
+    // the chunk's edges of this sender form a prefix of [start, lim): perm is
+    // increasing along a sender's slots
     const int p = start + n + lane;
-    const bool in = p < lim && send_perm[p] < e1;
-    const unsigned long long m = __ballot(in);
-    const int cnt = __popcll(m);
+    const int pe = p < lim ? send_perm[p] : 0x7fffffff;
+    const int cnt = __popcll(__ballot(pe < e1));
+    int t = 0;
+    for (; t + 4 <= cnt; t += 4) {
+      const int ea = __builtin_amdgcn_readlane(pe, t), eb = __builtin_amdgcn_readlane(pe, t + 1);
+      const int ec = __builtin_amdgcn_readlane(pe, t + 2), ed = __builtin_amdgcn_readlane(pe, t + 3);
+      vt va[R], vb[R], vc[R], vd[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) { va[r] = row(ea, r); vb[r] = row(eb, r); vc[r] = row(ec, r); vd[r] = row(ed, r); }
+#pragma unroll
+      for (int r = 0; r < R; ++r) acc[r] = (((acc[r] + va[r]) + vb[r]) + vc[r]) + vd[r];
+    }
+    for (; t < cnt; ++t) {
+      const int ea = __builtin_amdgcn_readlane(pe, t);
+#pragma unroll
+      for (int r = 0; r < R; ++r) acc[r] += row(ea, r);
+    }
     n += cnt;
     if (cnt < 64) break;
   }
   if (lane == 0) cursor[j] = start + n;
   if (!first && n == 0) return;
-  float* row = gx + (sb_i64)j * CX;
-  if ((CX & 3) == 0) {
-    for (int c = 4 * lane; c < CX; c += 256) {
-      sb_v4 s = first ? (sb_v4){0.f, 0.f, 0.f, 0.f} : *(const sb_v4*)(row + c);
-      for (int t = 0; t < n; ++t) s += sb_ld4(contrib + (sb_i64)(send_perm[start + t] - e0) * CX + c);
-      *(sb_v4*)(row + c) = s;
-    }
-  } else {
-    for (int c = lane; c < CX; c += 64) {
-      float s = first ? 0.f : row[c];
-      for (int t = 0; t < n; ++t) s += contrib[(sb_i64)(send_perm[start + t] - e0) * CX + c];
-      row[c] = s;
+  float* out = gx + (sb_i64)j * CX;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int c = lane + 64 * r;
+    if (c < NC) {
+      vt* o = (vt*)(out + W * c);
+      *o = first ? acc[r] : (*o + acc[r]);
     }
   }
 }

@@ -18,6 +18,7 @@ namespace sobek {
 
 namespace {
 constexpr int kAccMax = 128;        // forward accumulators per lane per wave unit
+constexpr int kFetchRing = 2;       // forward edge-data register sets in flight
 constexpr int kSlabFloats = 10240;  // backward LDS budget for one slab of adjoint state (40 KiB)
 constexpr int kAdjWaves = 2;        // waves per adjoint block
 
@@ -381,27 +382,35 @@ int unit_lsh(const Plan& P, const Unit& u) {
 }
 
 // Forward state (S) or directional state (dS) of one wave unit.  Lane = sub * U + u:
-// ES edges in flight, one input channel u per lane.  The edge loop has the same
-// trip count on every lane (inactive lanes contribute zeros), so the rank-1
-// accumulation S[u, q] += C[u] phi[q] can run on v_mfma_f32_4x4x1_16b_f32 when
-// U and K are multiples of 4: each 4-lane block multiplies its 4 channel values
-// (A) by a quad of radial features (B), and lane 4b + j, register i accumulates
-// S[u = 4b + i][q = 4 qq + j].  Otherwise it runs on the VALU, one channel per lane.
+// ES edges in flight, one input channel u per lane.  Every lane runs the same
+// number of edge iterations: a lane past the receiver's last edge takes that
+// edge again with zero radial features, so the rank-1 accumulation
+// S[u, q] += C[u] phi[q] can run on v_mfma_f32_4x4x1_16b_f32 when U and K are
+// multiples of 4: each 4-lane block multiplies its 4 channel values (A) by a
+// quad of radial features (B), and lane 4b + j, register i accumulates
+// S[u = 4b + i][q = 4 qq + j].  Otherwise it runs on the VALU, one channel per
+// lane.  Edge data is fetched three iterations ahead into a ring of three
+// register sets (the loop is unrolled by three, so no set is ever copied): while
+// one iteration is computed, the loads of the next two are in flight.  The
+// receiver's sender ids are held 64 at a time in one register per lane, the
+// next block already loaded, and handed to the lanes of an edge by a shuffle.
 void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) {
   const Irrep& ri = P.in[u.a];
   const int DA = 2 * ri.l + 1, L = unit_lsh(P, u), NS = (L + 1) * (L + 1);
   const bool mf = (u.U % 4 == 0) && (P.K % 4 == 0);
   const int KQ = P.K / 4;
+  const int NPH = mf ? KQ : P.K;
   o << "template <bool TAN, int FL>\nSB_DEV void sb_fwd_u" << id
     << "(int lane, int il, int beg, int end, const int* __restrict__ sender, const float* __restrict__ evec,"
        " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, sb_i64 ncap,"
-       " const float* __restrict__ xdot, const float* __restrict__ evdot, const float* __restrict__ phidot, int flags) {\n";
+       " const float* __restrict__ xdot, const float* __restrict__ evdot, const float* __restrict__ phidot, int flags,"
+       " int* ids) {\n";
   o << "  const int fl = FL >= 0 ? FL : flags;\n";
   o << "  constexpr int U = " << u.U << ", U0 = " << u.U0 << ", ES = " << u.ES << ", CA = " << ri.mul
-    << ", AOFF = " << ri.off << ", DA = " << DA << ";\n";
+    << ", AOFF = " << ri.off << ", DA = " << DA << ", NPH = " << NPH << ";\n";
   o << "  const int sub = lane / U, u = U0 + lane % U;\n"
-       "  const bool act = (lane < ES * U) && (u < CA);\n"
-       "  const int niter = (end - beg + ES - 1) / ES;\n";
+       "  const int sl = sub < ES ? sub : ES - 1, uu = u < CA ? u : CA - 1;\n"
+       "  const int deg = end - beg;\n";
   for (int t : u.paths) {
     const int DO = 2 * P.paths[t].l_out + 1;
     if (mf)
@@ -410,80 +419,108 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
     else
       o << "  float acc" << t << "[K * " << DO << "] = {};\n";
   }
-  // software pipeline: the receiver's sender ids are loaded 64 at a time and
-  // shared through the wave; the edge data of iteration it + 1 is fetched into
-  // the n* registers before iteration it is computed
-  const int NPH = mf ? KQ : P.K;
-  o << "  int snd = (beg + lane < end) ? sender[beg + lane] : 0;\n"
-       "  float nvx, nvy, nvz, ndx, ndy, ndz, nxv[DA], nxdv[DA], nph[" << NPH << "], nphd[" << NPH << "];\n"
-       "  auto fetch = [&](int itn) {\n"
-       "    const int kb = itn * ES;\n"
-       "    if (itn > 0 && (kb & 63) == 0) snd = (beg + kb + lane < end) ? sender[beg + kb + lane] : 0;\n"
-       "    const int j = __shfl(snd, (kb & 63) + sub);\n"
-       "    const int e = beg + kb + sub;\n"
-       "    const bool ev = act && e < end;\n"
-       "    nvx = 0.f; nvy = 0.f; nvz = 1.f; ndx = 0.f; ndy = 0.f; ndz = 0.f;\n"
-       "#pragma unroll\n    for (int m = 0; m < DA; ++m) { nxv[m] = 0.f; nxdv[m] = 0.f; }\n"
-       "#pragma unroll\n    for (int q = 0; q < " << NPH << "; ++q) { nph[q] = 0.f; nphd[q] = 0.f; }\n"
-       "    if (ev) {\n"
-       "      nvx = evec[3 * (sb_i64)e]; nvy = evec[3 * (sb_i64)e + 1]; nvz = evec[3 * (sb_i64)e + 2];\n"
-       "      const sb_i64 xrow = (sb_i64)j * CXI + AOFF + u;\n"
-       "#pragma unroll\n      for (int m = 0; m < DA; ++m) nxv[m] = x[xrow + m * CA];\n";
-  if (mf)
-    o << "#pragma unroll\n      for (int qq = 0; qq < " << KQ << "; ++qq) nph[qq] = phi[(sb_i64)e * K + 4 * qq + (lane & 3)];\n"
-      << "      if (TAN && (fl & 1)) {\n#pragma unroll\n        for (int qq = 0; qq < " << KQ
-      << "; ++qq) nphd[qq] = phidot[(sb_i64)e * K + 4 * qq + (lane & 3)];\n      }\n";
-  else
-    o << "#pragma unroll\n      for (int q = 0; q < K; ++q) nph[q] = phi[(sb_i64)e * K + q];\n"
-      << "      if (TAN && (fl & 1)) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) nphd[q] = phidot[(sb_i64)e * K + q];\n      }\n";
-  o << "      if (TAN && (fl & 2)) {\n#pragma unroll\n        for (int m = 0; m < DA; ++m) nxdv[m] = xdot[xrow + m * CA];\n      }\n"
-       "      if (TAN && (fl & 4)) { ndx = evdot[3 * (sb_i64)e]; ndy = evdot[3 * (sb_i64)e + 1]; ndz = evdot[3 * (sb_i64)e + 2]; }\n"
-       "    }\n"
-       "  };\n"
-       "  fetch(0);\n"
-       "  for (int it = 0; it < niter; ++it) {\n"
-       "    const float vx = nvx, vy = nvy, vz = nvz, dx = ndx, dy = ndy, dz = ndz;\n"
-    << "    float xv[DA], xdv[DA], " << (mf ? "bq" : "ph") << "[" << NPH << "], " << (mf ? "bqd" : "phd") << "[" << NPH << "];\n"
-    << "#pragma unroll\n    for (int m = 0; m < DA; ++m) { xv[m] = nxv[m]; xdv[m] = nxdv[m]; }\n"
-    << "#pragma unroll\n    for (int q = 0; q < " << NPH << "; ++q) { " << (mf ? "bq" : "ph") << "[q] = nph[q]; "
-    << (mf ? "bqd" : "phd") << "[q] = nphd[q]; }\n"
-    << "    if (it + 1 < niter) fetch(it + 1);\n"
-       "    const float rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
-       "    const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
-    << "    float Y[" << NS << "], Yd[" << NS << "];\n    sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
-    << "    if (TAN && (fl & 4)) sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n";
-  for (int t : u.paths) {
-    const Path& q = P.paths[t];
-    const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
-    o << "    {  // path " << t << "\n"
-      << "      constexpr int DO = " << DO << ";\n"
-      << "      float M[P" << t << "_NP], C[DO], C2[DO];\n"
-      << "      sb_M" << t << "(Y + " << Y0 << ", M);\n"
-      << "      if (!TAN) {\n        sb_C" << t << "(xv, M, C2);\n      } else {\n"
-      << "#pragma unroll\n        for (int m = 0; m < DO; ++m) C2[m] = 0.f;\n"
-      << "        if (fl & 2) { sb_C" << t << "(xdv, M, C); for (int m = 0; m < DO; ++m) C2[m] += C[m]; }\n"
-      << "        if (fl & 4) { float Md[P" << t << "_NP]; sb_M" << t << "(Yd + " << Y0 << ", Md); sb_C" << t
-      << "(xv, Md, C); for (int m = 0; m < DO; ++m) C2[m] += C[m]; }\n"
-      << "        if (fl & 1) sb_C" << t << "(xv, M, C);\n"
-      << "      }\n";
-    if (mf) {
-      o << "#pragma unroll\n      for (int m = 0; m < DO; ++m)\n#pragma unroll\n"
-        << "        for (int qq = 0; qq < " << KQ << "; ++qq) {\n"
-        << "          acc" << t << "[m * " << KQ << " + qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(C2[m], bq[qq], acc" << t
-        << "[m * " << KQ << " + qq], 0, 0, 0);\n"
-        << "          if (TAN && (fl & 1)) acc" << t << "[m * " << KQ << " + qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(C[m], bqd[qq], acc"
-        << t << "[m * " << KQ << " + qq], 0, 0, 0);\n"
+  // The receiver's edges are taken in segments of up to 256.  A segment's
+  // sender ids go to this wave's LDS slice first (clamped addresses: every load
+  // is in bounds); read back with LDS loads, they never make the edge loop wait
+  // on its own global loads.
+  o << "  for (int seg = 0; seg < deg; seg += 256) {\n"
+       "  const int sdeg = min(256, deg - seg), sbeg = beg + seg;\n"
+       "  const int niter = (sdeg + ES - 1) / ES;\n"
+       "#pragma unroll\n  for (int i = 0; i < 4; ++i) ids[64 * i + lane] = sender[sbeg + min(64 * i + lane, sdeg - 1)];\n";
+  const std::string pidx = mf ? "e * K + 4 * q + (lane & 3)" : "e * K + q";
+  // edge data of ring slot r for iteration `itn`; the edge weight w is applied
+  // at use, so nothing here waits for a load
+  auto fetch = [&](int r, const std::string& itn) {
+    const std::string R = std::to_string(r);
+    o << "    {\n"
+         "      const int kb = (" << itn << ") * ES;\n"
+         "      const int k = kb + sl;\n"
+         "      const int kc = k < sdeg ? k : sdeg - 1;\n"
+         "      w" << R << " = k < sdeg ? 1.f : 0.f;\n"
+         "      const int j = ids[kc];\n"
+         "      const sb_i64 e = sbeg + kc;\n"
+         "      vx" << R << " = evec[3 * e]; vy" << R << " = evec[3 * e + 1]; vz" << R << " = evec[3 * e + 2];\n"
+         "      if (TAN && (fl & 4)) { dx" << R << " = evdot[3 * e]; dy" << R << " = evdot[3 * e + 1]; dz" << R
+      << " = evdot[3 * e + 2]; }\n"
+         "#pragma unroll\n      for (int q = 0; q < NPH; ++q) pa" << R << "[q] = phi[" << pidx << "];\n"
+         "      if (TAN && (fl & 1)) {\n"
+         "#pragma unroll\n        for (int q = 0; q < NPH; ++q) pd" << R << "[q] = phidot[" << pidx << "];\n"
+         "      }\n";
+    o << "      const sb_i64 xrow = (sb_i64)j * CXI + AOFF + uu;\n"
+         "#pragma unroll\n      for (int m = 0; m < DA; ++m) xa" << R << "[m] = x[xrow + m * CA];\n"
+         "      if (TAN && (fl & 2)) {\n"
+         "#pragma unroll\n        for (int m = 0; m < DA; ++m) xd" << R << "[m] = xdot[xrow + m * CA];\n"
+         "      }\n"
+         "    }\n";
+  };
+  auto compute = [&](int r) {
+    const std::string R = std::to_string(r);
+    o << "    {\n"
+         "      float ph[NPH], phd[NPH];\n"
+         "#pragma unroll\n      for (int q = 0; q < NPH; ++q) {\n"
+         "        ph[q] = pa" << R << "[q] * w" << R << ";\n"
+         "        phd[q] = (TAN && (fl & 1)) ? pd" << R << "[q] * w" << R << " : 0.f;\n"
+         "      }\n"
+         "      const float rinv = __builtin_amdgcn_rsqf(vx" << R << " * vx" << R << " + vy" << R << " * vy" << R << " + vz" << R
+      << " * vz" << R << ");\n"
+         "      const float ux = vx" << R << " * rinv, uy = vy" << R << " * rinv, uz = vz" << R << " * rinv;\n"
+      << "      float Y[" << NS << "], Yd[" << NS << "];\n      sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
+      << "      if (TAN && (fl & 4)) sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx" << R << ", dy" << R << ", dz" << R
+      << ", Y, Yd);\n";
+    for (int t : u.paths) {
+      const Path& q = P.paths[t];
+      const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
+      o << "      {  // path " << t << "\n"
+        << "        constexpr int DO = " << DO << ";\n"
+        << "        float M[P" << t << "_NP], C[DO], C2[DO];\n"
+        << "        sb_M" << t << "(Y + " << Y0 << ", M);\n"
+        << "        if (!TAN) {\n          sb_C" << t << "(xa" << R << ", M, C2);\n        } else {\n"
+        << "#pragma unroll\n          for (int m = 0; m < DO; ++m) C2[m] = 0.f;\n"
+        << "          if (fl & 2) { sb_C" << t << "(xd" << R << ", M, C); for (int m = 0; m < DO; ++m) C2[m] += C[m]; }\n"
+        << "          if (fl & 4) { float Md[P" << t << "_NP]; sb_M" << t << "(Yd + " << Y0 << ", Md); sb_C" << t
+        << "(xa" << R << ", Md, C); for (int m = 0; m < DO; ++m) C2[m] += C[m]; }\n"
+        << "          if (fl & 1) sb_C" << t << "(xa" << R << ", M, C);\n"
         << "        }\n";
-    } else {
-      o << "#pragma unroll\n      for (int q = 0; q < K; ++q)\n#pragma unroll\n"
-        << "        for (int m = 0; m < DO; ++m) {\n"
-        << "          acc" << t << "[q * DO + m] = fmaf(ph[q], C2[m], acc" << t << "[q * DO + m]);\n"
-        << "          if (TAN && (fl & 1)) acc" << t << "[q * DO + m] = fmaf(phd[q], C[m], acc" << t << "[q * DO + m]);\n"
-        << "        }\n";
+      if (mf) {
+        o << "#pragma unroll\n        for (int m = 0; m < DO; ++m)\n#pragma unroll\n"
+          << "          for (int qq = 0; qq < " << KQ << "; ++qq) {\n"
+          << "            acc" << t << "[m * " << KQ << " + qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(C2[m], ph[qq], acc" << t
+          << "[m * " << KQ << " + qq], 0, 0, 0);\n"
+          << "            if (TAN && (fl & 1)) acc" << t << "[m * " << KQ
+          << " + qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(C[m], phd[qq], acc" << t << "[m * " << KQ << " + qq], 0, 0, 0);\n"
+          << "          }\n";
+      } else {
+        o << "#pragma unroll\n        for (int q = 0; q < K; ++q)\n#pragma unroll\n"
+          << "          for (int m = 0; m < DO; ++m) {\n"
+          << "            acc" << t << "[q * DO + m] = fmaf(ph[q], C2[m], acc" << t << "[q * DO + m]);\n"
+          << "            if (TAN && (fl & 1)) acc" << t << "[q * DO + m] = fmaf(phd[q], C[m], acc" << t << "[q * DO + m]);\n"
+          << "          }\n";
+      }
+      o << "      }\n";
     }
     o << "    }\n";
+  };
+  // ring of register sets: slot r holds iteration it + r; fetches past the last
+  // iteration re-read the last edge with weight 0, which keeps them unconditional
+  // and the number of loads in flight the same on every path
+  const int NR = kFetchRing;
+  o << "  {\n";
+  for (int r = 0; r < NR; ++r)
+    o << "    float vx" << r << ", vy" << r << ", vz" << r << ", dx" << r << " = 0.f, dy" << r << " = 0.f, dz" << r
+      << " = 0.f, w" << r << ", xa" << r << "[DA], xd" << r << "[DA], pa" << r << "[NPH], pd" << r << "[NPH];\n";
+  for (int r = 0; r < NR; ++r) fetch(r, std::to_string(r));
+  o << "    int it = 0;\n    for (; it + " << NR << " <= niter; it += " << NR << ") {\n";
+  for (int r = 0; r < NR; ++r) {
+    compute(r);
+    fetch(r, "it + " + std::to_string(NR + r));
   }
-  o << "  }\n";
+  o << "    }\n";
+  for (int r = 0; r + 1 < NR; ++r) {
+    o << "    if (it + " << r << " < niter) {\n";
+    compute(r);
+    o << "    }\n";
+  }
+  o << "  }\n  }  // segment\n";
   if (u.ES > 1) {
     for (int t : u.paths) {
       const int DO = 2 * P.paths[t].l_out + 1;
@@ -707,7 +744,7 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        "    int zz = 0;\n    asm volatile(\"\" : \"+v\"(zz));\n"
        "    if (ev) {\n"
        "      const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
-       "      rinv = 1.0f / sqrtf(vx * vx + vy * vy + vz * vz);\n"
+       "      rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
        "      ux = vx * rinv; uy = vy * rinv; uz = vz * rinv;\n"
        "#pragma unroll\n      for (int v = 0; v < KQ; ++v) {\n"
        "        const int q = 4 * v + g;\n"
@@ -877,6 +914,14 @@ std::string generate_source(const Plan& P) {
   emit_sh(o, P.lmax);
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
 
+  // x-gradient gather over the sender-sorted view, specialised on the input width
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_sender_reduce(const int* send_rowptr,"
+       " const int* send_perm, const float* contrib, float* gx, int* cursor, int N, int CX, int e0, int e1,"
+       " int first) {\n"
+       "  (void)CX;\n"
+       "  sb_sender_reduce<CXI>(send_rowptr, send_perm, contrib, gx, cursor, N, e0, e1, first);\n"
+       "}\n";
+
   // forward S / dS kernels: one wave per (receiver, unit)
   for (int t = 0; t < (int)P.fwd_units.size(); ++t) emit_fwd_unit(o, P, P.fwd_units[t], t);
   const int NU = (int)P.fwd_units.size();
@@ -890,6 +935,7 @@ std::string generate_source(const Plan& P) {
          " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, int r0, int n_recv,"
          " sb_i64 ncap, const float* __restrict__ xdot, const float* __restrict__ evdot,"
          " const float* __restrict__ phidot, int flags) {\n"
+      << "  __shared__ int sids[4][256];\n"
       << "  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;\n"
       << "  const int il = gw / " << NU << ", t = gw % " << NU << ";\n"
       << "  if (il >= n_recv) return;\n"
@@ -897,7 +943,7 @@ std::string generate_source(const Plan& P) {
          "  switch (t) {\n";
     for (int t = 0; t < NU; ++t)
       o << "    case " << t << ": sb_fwd_u" << t << "<" << (fv.tan ? "true" : "false") << ", " << fv.fl
-        << ">(lane, il, beg, end, sender, evec, phi, x, S, ncap, xdot, evdot, phidot, flags); break;\n";
+        << ">(lane, il, beg, end, sender, evec, phi, x, S, ncap, xdot, evdot, phidot, flags, sids[threadIdx.x >> 6]); break;\n";
     o << "  }\n}\n";
   }
 

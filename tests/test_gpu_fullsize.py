@@ -78,15 +78,18 @@ def test_full_size(gpu, name):
     graph = api.Graph(T(g.rowptr), T(g.sender))
     args = (T(x), T(g.evec), T(g.phi), T(W))
     td = T(rdot)
-    say("  gpu fwd")
-    m = N_(api.conv_fwd(plan, graph, *args, budget=BUDGET))
+    say("  gpu fwd (keeping the receiver state, as the benchmark does)")
+    state = api.new_state(plan, graph)
+    m = N_(api.conv_fwd(plan, graph, *args, budget=BUDGET, state=state))
     say("  gpu bwd / dbwd, dense m_bar")
-    bd = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout), budget=BUDGET)]
+    bd = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout), budget=BUDGET, state=state)]
     dd = [N_(o) for o in api.conv_dbwd(plan, graph, *args, T(gout), t_gevec=td, budget=BUDGET)]
     say("  gpu bwd / dbwd, m_bar restricted to the sampled receivers")
-    bm = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout_m), budget=BUDGET)]
+    bm = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout_m), budget=BUDGET, state=state)]
+    bm_recompute = N_(api.conv_bwd(plan, graph, *args, T(gout_m), need=(False, False, False, True),
+                                   budget=BUDGET)[3])
     dm = [N_(o) for o in api.conv_dbwd(plan, graph, *args, T(gout_m), t_gevec=td, budget=BUDGET)]
-    del args, td, graph
+    del args, td, graph, state
     torch.cuda.empty_cache()
 
     # ---- oracle on the sampled receivers' in-edges ---------------------------------------------
@@ -110,7 +113,8 @@ def test_full_size(gpu, name):
     other = np.ones(g.E, bool)
     other[A] = False
     _check("bwd x_bar (restricted m_bar)", bm[0], b_ref["gx"], BWD_TOL)
-    _check("bwd A_bar (restricted m_bar)", bm[3], b_ref["gW"], BWD_TOL)
+    _check("bwd A_bar (restricted m_bar, retained S)", bm[3], b_ref["gW"], BWD_TOL)
+    _check("bwd A_bar (restricted m_bar, recomputed S)", bm_recompute, b_ref["gW"], BWD_TOL)
     _check("bwd evec_bar (restricted m_bar)", bm[1][A], b_ref["gevec"], BWD_TOL)
     _check("dbwd g_x (restricted m_bar)", dm[1], d_ref["g_x"], BWD_TOL)
     _check("dbwd g_W (restricted m_bar)", dm[4], d_ref["g_W"], BWD_TOL)

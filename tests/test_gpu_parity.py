@@ -181,3 +181,52 @@ def test_autograd_matches_oracle(gpu):
     r = oc.dbwd(*oracle_args(case, prob), case["gout"], t_gevec=2 * _n(gev).astype(np.float64))
     for name, o in zip(("g_x", "g_evec", "g_phi", "g_W"), d):
         assert max_rel(_n(o), r[name]) <= BWD_TOL, name
+
+
+@pytest.mark.parametrize("sig,N,E,seed", [("small", 300, 4000, 11), ("odd", 50, 700, 12), ("medium", 120, 1500, 13)])
+def test_retained_state(gpu, sig, N, E, seed):
+    """Forward that keeps S, and the backward that reads it, against the oracle and the recomputing path."""
+    import torch
+    case = make_case(sig, N, E, seed, isolated=2)
+    api, plan, graph, prob = setup(case)
+    g = case["graph"]
+    args = (_t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]))
+    state = api.new_state(plan, graph)
+    state.fill_(float("nan"))                       # every element the backward reads must be written
+    m = api.conv_fwd(plan, graph, *args, state=state, budget=1 << 20)   # small budget: the state is one chunk anyway
+    assert max_rel(_n(m), oc.fwd(*oracle_args(case, prob))) <= FWD_TOL
+    assert np.array_equal(_n(m), _n(api.conv_fwd(plan, graph, *args)))
+    gout = _t(case["gout"])
+    ref = oc.bwd(*oracle_args(case, prob), case["gout"])
+    for budget in (0, 1 << 20):                     # one chunk, and many chunks for the edge stage
+        outs = api.conv_bwd(plan, graph, *args, gout, state=state, budget=budget)
+        for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
+            err = max_rel(_n(o), ref[name])
+            print(f"bwd (retained S, budget {budget}) {sig} {name}: max rel err {err:.2e}")
+            assert err <= BWD_TOL, name
+    # W does not enter S: a state kept with other weights serves as well
+    m2 = api.conv_fwd(plan, graph, args[0], args[1], args[2], 2 * args[3], state=state)
+    torch.cuda.synchronize()
+    assert torch.isfinite(m2).all()
+    outs = api.conv_bwd(plan, graph, *args, gout, state=state)
+    assert max_rel(_n(outs[3]), ref["gW"]) <= BWD_TOL
+
+
+def test_autograd_retained_state(gpu):
+    import torch
+    case = make_case("small", 80, 900, 14)
+    api, plan, graph, prob = setup(case)
+    g = case["graph"]
+    x = _t(case["x"]).requires_grad_()
+    ev = _t(g.evec).requires_grad_()
+    ph = _t(g.phi).requires_grad_()
+    W = _t(case["W"]).requires_grad_()
+    m = api.tp_conv(plan, graph, x, ev, ph, W, retain_state=True)
+    gx, gev, gph, gW = torch.autograd.grad(m, (x, ev, ph, W), _t(case["gout"]), create_graph=True)
+    ref = oc.bwd(*oracle_args(case, prob), case["gout"])
+    for name, o in zip(("gx", "gevec", "gphi", "gW"), (gx, gev, gph, gW)):
+        assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
+    d = torch.autograd.grad((gev ** 2).sum(), (x, ev, ph, W))
+    r = oc.dbwd(*oracle_args(case, prob), case["gout"], t_gevec=2 * _n(gev).astype(np.float64))
+    for name, o in zip(("g_x", "g_evec", "g_phi", "g_W"), d):
+        assert max_rel(_n(o), r[name]) <= BWD_TOL, name
