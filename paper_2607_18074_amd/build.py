@@ -74,6 +74,17 @@ def prewarm(signatures, jobs=None):
             pass
 
 
+def prune_cache(since):
+    """Delete code objects of the in-tree cache that no compile or cache hit touched since `since`."""
+    import glob
+    removed = 0
+    for f in glob.glob(os.path.join(HERE, "_jitcache", "sobek_*.co")):
+        if os.path.getmtime(f) < since - 1.0:
+            os.remove(f)
+            removed += 1
+    return removed
+
+
 if __name__ == "__main__":
     build_library(verbose=True)
     print("built", LIB)

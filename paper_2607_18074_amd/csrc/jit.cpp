@@ -5,6 +5,7 @@
 #include <hip/hiprtc.h>
 #include <sys/stat.h>
 #include <unistd.h>
+#include <utime.h>
 
 #include <cstdio>
 #include <cstdlib>
@@ -83,7 +84,10 @@ std::vector<char> jit_compile(const std::string& plan_source, std::string* log_o
   const std::string key = jit_key(plan_source);
   const std::string path = cache_dir() + "/sobek_" + key + ".co";
   std::vector<char> code;
-  if (read_file(path, code)) return code;
+  if (read_file(path, code)) {
+    utime(path.c_str(), nullptr);  // a hit marks the entry as in use (build steps prune untouched ones)
+    return code;
+  }
 
   std::string src = full_source(plan_source);
   hiprtcProgram prog;

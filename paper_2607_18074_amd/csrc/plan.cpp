@@ -705,12 +705,16 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
   for (auto& it : sl.items)
     for (int t : it.paths) L = std::max(L, P.paths[t].l_sh);
   const int NS = (L + 1) * (L + 1);
+  auto is_v4 = [&](const AdjItem& it) {
+    const Irrep& ri = P.in[it.a];
+    return ri.mul % 4 == 0 && ri.off % 4 == 0 && P.dim_in % 4 == 0;
+  };
   o << "template <bool DB, int FL>\nSB_DEV void sb_adj_s" << s
     << "(int w, int lane, int ebase, int nb, int e0, const int* __restrict__ sender, const float* __restrict__ evec,"
        " const float* __restrict__ phi, const float* __restrict__ x, const float* __restrict__ xdot,"
        " const float* __restrict__ evdot, const float* __restrict__ phidot, const float* sS, const float* sS2,"
        " float* sacc, float* __restrict__ gphi, float* __restrict__ gevec, float* __restrict__ contrib, int flags,"
-       " bool multi) {\n"
+       " bool multi, int* wids) {\n"
     << "  const int fl = FL >= 0 ? FL : flags;\n"
        "  constexpr bool HAS_GY = !DB || FL < 0 || (FL & 11);\n"
        "  constexpr bool HAS_YB = DB && (FL < 0 || (FL & 4));\n"
@@ -718,77 +722,115 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        "  constexpr int NV = K + (HAS_GY ? NSH : 0) + (HAS_YB ? NSH : 0);\n"
        "  constexpr int KQ = KP / 4;\n"
        "  const int es = lane & 15, g = lane >> 4, l3 = lane & 3;\n"
-       "  const int niter = (nb + 16 * ADJ_W - 1) / (16 * ADJ_W);\n"
-       // sender ids of four iterations per load (lane l -> iteration it + l / 16,
-       // slot l % 16), shared through the wave
-       "  int snd;\n"
-       "  {\n    const int kk = (g * ADJ_W + w) * 16 + es;\n    snd = kk < nb ? sender[ebase + kk] : 0;\n  }\n"
-       "  for (int it = 0; it < niter; ++it) {\n"
-       "    if (it > 0 && (it & 3) == 0) {\n"
-       "      const int kk = ((it + g) * ADJ_W + w) * 16 + es;\n"
-       "      snd = kk < nb ? sender[ebase + kk] : 0;\n"
-       "    }\n"
-       "    const int jsnd = __shfl(snd, ((it & 3) << 4) + es);\n"
-       "    const int k = (it * ADJ_W + w) * 16 + es;\n"
-       "    const bool ev = k < nb;\n"
-       "    const int e = ebase + k;\n"
+       // the batch's edges in segments of up to 256: a segment's sender ids go to
+       // this wave's LDS slice first, so the edge loop never waits on them
+       "  for (int seg = 0; seg < nb; seg += 256) {\n"
+       "  const int sn = min(256, nb - seg), sbase = ebase + seg;\n"
+       "#pragma unroll\n  for (int i = 0; i < 4; ++i) wids[64 * i + lane] = sender[sbase + min(64 * i + lane, sn - 1)];\n"
+       "  const int niter = (sn + 16 * ADJ_W - 1) / (16 * ADJ_W);\n"
+       // edge data and sender rows of the next iteration, loaded one iteration
+       // ahead (clamped to the segment's last edge, masked at use)
+       "  float nvx, nvy, nvz, ndx = 0.f, ndy = 0.f, ndz = 0.f, nph[KQ], nphd[KQ];\n"
+       "  sb_i64 nrow;\n";
+  for (size_t i = 0; i < sl.items.size(); ++i) {
+    const int DA = 2 * P.in[sl.items[i].a].l + 1;
+    if (is_v4(sl.items[i])) o << "  sb_f4 xn" << i << "[" << DA << "];\n";
+    else o << "  float xn" << i << "[4][" << DA << "];\n";
+  }
+  // loads of the next iteration's edge data (and its sender's row offset)
+  auto fetch_edge = [&](const std::string& itn) {
+    o << "    {\n"
+         "      const int kf = ((" << itn << ") * ADJ_W + w) * 16 + es;\n"
+         "      const int kc = kf < sn ? kf : sn - 1;\n"
+         "      const sb_i64 ef = sbase + kc;\n"
+         "      nvx = evec[3 * ef]; nvy = evec[3 * ef + 1]; nvz = evec[3 * ef + 2];\n"
+         "#pragma unroll\n      for (int v = 0; v < KQ; ++v) nph[v] = phi[ef * K + min(4 * v + g, K - 1)];\n"
+         "      if (DB && (fl & 1)) {\n"
+         "#pragma unroll\n        for (int v = 0; v < KQ; ++v) nphd[v] = phidot[ef * K + min(4 * v + g, K - 1)];\n"
+         "      }\n"
+         "      if (DB && (fl & 4)) { ndx = evdot[3 * ef]; ndy = evdot[3 * ef + 1]; ndz = evdot[3 * ef + 2]; }\n"
+         "      nrow = (sb_i64)wids[kc] * CXI;\n"
+         "    }\n";
+  };
+  // loads of item i's sender-row slice at row offset nrow (channel index clamped into the irrep)
+  auto fetch_x = [&](size_t i, const char* ind) {
+    const AdjItem& it = sl.items[i];
+    const Irrep& ri = P.in[it.a];
+    const int DA = 2 * ri.l + 1;
+    if (is_v4(it))
+      o << ind << "{\n" << ind << "  const int uc = min(" << it.u0 << " + 4 * g, " << ri.mul - 4 << ");\n"
+        << "#pragma unroll\n" << ind << "  for (int m = 0; m < " << DA << "; ++m) xn" << i << "[m] = *(const sb_f4*)(x + nrow + "
+        << ri.off << " + m * " << ri.mul << " + uc);\n" << ind << "}\n";
+    else
+      o << "#pragma unroll\n" << ind << "for (int r = 0; r < 4; ++r) {\n"
+        << ind << "  const int uc = min(" << it.u0 << " + 4 * g + r, " << ri.mul - 1 << ");\n"
+        << "#pragma unroll\n" << ind << "  for (int m = 0; m < " << DA << "; ++m) xn" << i << "[r][m] = x[nrow + " << ri.off
+        << " + m * " << ri.mul << " + uc];\n" << ind << "}\n";
+  };
+  fetch_edge("0");
+  for (size_t i = 0; i < sl.items.size(); ++i) fetch_x(i, "  ");
+  o << "  for (int it = 0; it < niter; ++it) {\n"
+       "    const int kl = (it * ADJ_W + w) * 16 + es;\n"
+       "    const int k = seg + kl;\n"
+       "    const bool ev = kl < sn;\n"
+       "    const int e = sbase + kl;\n"
        "    sb_f4 pacc[KQ];\n"
        "#pragma unroll\n    for (int v = 0; v < KQ; ++v) pacc[v] = (sb_f4){0.f, 0.f, 0.f, 0.f};\n"
        "    float gy[NSH], yb[NSH];\n"
        "#pragma unroll\n    for (int v = 0; v < NSH; ++v) { gy[v] = 0.f; yb[v] = 0.f; }\n"
-       "    float ux = 0.f, uy = 0.f, uz = 1.f, rinv = 1.f, dx = 0.f, dy = 0.f, dz = 0.f;\n"
+       "    // this iteration's edge data (masked), then the next iteration's loads\n"
+       "    const float vx = nvx, vy = nvy, vz = nvz;\n"
+       "    const float dx = ev ? ndx : 0.f, dy = ev ? ndy : 0.f, dz = ev ? ndz : 0.f;\n"
        "    float phB[KQ], phdB[KQ];\n"
-       "#pragma unroll\n    for (int v = 0; v < KQ; ++v) { phB[v] = 0.f; phdB[v] = 0.f; }\n"
+       "#pragma unroll\n    for (int v = 0; v < KQ; ++v) {\n"
+       "      const bool ok = ev && 4 * v + g < K;\n"
+       "      phB[v] = ok ? nph[v] : 0.f;\n"
+       "      phdB[v] = (DB && (fl & 1) && ok) ? nphd[v] : 0.f;\n"
+       "    }\n"
+       "    const sb_i64 srow = nrow;\n"
+       "    (void)srow;\n";
+  fetch_edge("it + 1");
+  o << "    const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
+       "    const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
        "    // opaque zero: keeps the adjoint-state reads inside the loop (LDS), instead of\n"
        "    // hoisting the whole slab into registers\n"
        "    int zz = 0;\n    asm volatile(\"\" : \"+v\"(zz));\n"
-       "    if (ev) {\n"
-       "      const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
-       "      rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
-       "      ux = vx * rinv; uy = vy * rinv; uz = vz * rinv;\n"
-       "#pragma unroll\n      for (int v = 0; v < KQ; ++v) {\n"
-       "        const int q = 4 * v + g;\n"
-       "        if (q < K) phB[v] = phi[(sb_i64)e * K + q];\n"
-       "      }\n"
-       "      if (DB && (fl & 1)) {\n"
-       "#pragma unroll\n        for (int v = 0; v < KQ; ++v) {\n"
-       "          const int q = 4 * v + g;\n"
-       "          if (q < K) phdB[v] = phidot[(sb_i64)e * K + q];\n"
-       "        }\n      }\n"
-       "      if (DB && (fl & 4)) { dx = evdot[3 * (sb_i64)e]; dy = evdot[3 * (sb_i64)e + 1]; dz = evdot[3 * (sb_i64)e + 2]; }\n"
-       "    }\n"
     << "    float Y[" << NS << "], Yd[" << NS << "];\n    sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
-    << "    if (DB && (fl & 4)) sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n"
-    << "    const sb_i64 srow = (sb_i64)jsnd * CXI;\n";
-  for (const AdjItem& it : sl.items) {
+    << "    if (DB && (fl & 4)) sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n";
+  for (size_t ii = 0; ii < sl.items.size(); ++ii) {
+    const AdjItem& it = sl.items[ii];
     const Irrep& ri = P.in[it.a];
     const int DA = 2 * ri.l + 1;
-    const bool v4 = ri.mul % 4 == 0 && ri.off % 4 == 0 && P.dim_in % 4 == 0;
+    const bool v4 = is_v4(it);
     o << "    {  // input irrep " << it.a << ", channels " << it.u0 << " .. " << it.u0 + 15 << "\n"
       << "      constexpr int CA = " << ri.mul << ", AOFF = " << ri.off << ", U0 = " << it.u0 << ", DA = " << DA << ";\n"
       << "      const int u = U0 + 4 * g;\n"
-      << "      float xv[4][DA], xdv[4][DA], xc[4][DA];\n"
-      << "#pragma unroll\n      for (int r = 0; r < 4; ++r)\n#pragma unroll\n"
-      << "        for (int m = 0; m < DA; ++m) { xv[r][m] = 0.f; xdv[r][m] = 0.f; xc[r][m] = 0.f; }\n";
+      << "      float xv[4][DA], xdv[4][DA], xc[4][DA];\n";
+    // the prefetched row slice of this iteration (zero for lanes past the edges or past C_in),
+    // then the same slice of the next iteration
     if (v4)
-      o << "      if (ev && u < CA) {\n"
-        << "#pragma unroll\n        for (int m = 0; m < DA; ++m) {\n"
-        << "          const sb_f4 v = *(const sb_f4*)(x + srow + AOFF + m * CA + u);\n"
-        << "          xv[0][m] = v[0]; xv[1][m] = v[1]; xv[2][m] = v[2]; xv[3][m] = v[3];\n"
-        << "        }\n"
-        << "        if (DB && (fl & 2)) {\n"
-        << "#pragma unroll\n          for (int m = 0; m < DA; ++m) {\n"
-        << "            const sb_f4 v = *(const sb_f4*)(xdot + srow + AOFF + m * CA + u);\n"
-        << "            xdv[0][m] = v[0]; xdv[1][m] = v[1]; xdv[2][m] = v[2]; xdv[3][m] = v[3];\n"
-        << "          }\n        }\n      }\n";
+      o << "#pragma unroll\n      for (int m = 0; m < DA; ++m) {\n"
+        << "        const bool ok = ev && u < CA;\n"
+        << "#pragma unroll\n        for (int r = 0; r < 4; ++r) xv[r][m] = ok ? xn" << ii << "[m][r] : 0.f;\n"
+        << "      }\n";
     else
-      o << "      if (ev) {\n"
+      o << "#pragma unroll\n      for (int r = 0; r < 4; ++r)\n#pragma unroll\n"
+        << "        for (int m = 0; m < DA; ++m) xv[r][m] = (ev && u + r < CA) ? xn" << ii << "[r][m] : 0.f;\n";
+    fetch_x(ii, "      ");
+    o << "#pragma unroll\n      for (int r = 0; r < 4; ++r)\n#pragma unroll\n"
+      << "        for (int m = 0; m < DA; ++m) { xdv[r][m] = 0.f; xc[r][m] = 0.f; }\n";
+    if (v4)
+      o << "      if (DB && (fl & 2) && ev && u < CA) {\n"
+        << "#pragma unroll\n        for (int m = 0; m < DA; ++m) {\n"
+        << "          const sb_f4 v = *(const sb_f4*)(xdot + srow + AOFF + m * CA + u);\n"
+        << "          xdv[0][m] = v[0]; xdv[1][m] = v[1]; xdv[2][m] = v[2]; xdv[3][m] = v[3];\n"
+        << "        }\n      }\n";
+    else
+      o << "      if (DB && (fl & 2) && ev) {\n"
         << "#pragma unroll\n        for (int r = 0; r < 4; ++r)\n"
         << "          if (u + r < CA) {\n"
-        << "#pragma unroll\n            for (int m = 0; m < DA; ++m) xv[r][m] = x[srow + AOFF + m * CA + u + r];\n"
-        << "            if (DB && (fl & 2)) {\n"
-        << "#pragma unroll\n              for (int m = 0; m < DA; ++m) xdv[r][m] = xdot[srow + AOFF + m * CA + u + r];\n"
-        << "            }\n          }\n      }\n";
+        << "#pragma unroll\n            for (int m = 0; m < DA; ++m) xdv[r][m] = xdot[srow + AOFF + m * CA + u + r];\n"
+        << "          }\n      }\n";
     for (size_t pi = 0; pi < it.paths.size(); ++pi) emit_adj_path(o, P, it.paths[pi], it.lds_off[pi]);
     o << "      if (contrib && ev) {\n"
       << "        float* cr = contrib + (sb_i64)(e - e0) * CXI + AOFF + u;\n";
@@ -844,7 +886,7 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
          "        gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n"
          "      }\n";
   }
-  o << "    }\n  }\n}\n";
+  o << "    }\n  }\n  }  // segment\n}\n";
 }
 
 // Staging of one slab's adjoint-state slices (and the second slice set when dA
@@ -958,7 +1000,7 @@ std::string generate_source(const Plan& P) {
        " const float* __restrict__ Sb, const float* __restrict__ Sb2, const float* __restrict__ xdot,"
        " const float* __restrict__ evdot, const float* __restrict__ phidot, float* __restrict__ gphi,"
        " float* __restrict__ gevec, float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags,"
-       " float* sS, float* sS2, float* sacc) {\n"
+       " float* sS, float* sS2, float* sacc, int* sids) {\n"
        "  const int il = blockIdx.x;\n"
        "  if (il >= n_recv) return;\n"
        "  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;\n"
@@ -968,7 +1010,7 @@ std::string generate_source(const Plan& P) {
     emit_adj_stage(o, P, 0, "  ");
     o << "  __syncthreads();\n"
          "  sb_adj_s0<DB, FL>(w, lane, beg, end - beg, e0, sender, evec, phi, x, xdot, evdot, phidot, sS, sS2, sacc, gphi,"
-         " gevec, contrib, flags, false);\n";
+         " gevec, contrib, flags, false, sids + 256 * w);\n";
   } else {
     o << "  for (int eb = beg; eb < end; eb += EB) {\n"
          "    const int nb = min(EB, end - eb);\n";
@@ -977,7 +1019,7 @@ std::string generate_source(const Plan& P) {
       emit_adj_stage(o, P, s, "    ");
       o << "    __syncthreads();\n"
         << "    sb_adj_s" << s << "<DB, FL>(w, lane, eb, nb, e0, sender, evec, phi, x, xdot, evdot, phidot, sS, sS2, sacc,"
-           " gphi, gevec, contrib, flags, true);\n";
+           " gphi, gevec, contrib, flags, true, sids + 256 * w);\n";
     }
     o << "  }\n";
   }
@@ -992,14 +1034,15 @@ std::string generate_source(const Plan& P) {
          " const float* __restrict__ Sb2, const float* __restrict__ xdot, const float* __restrict__ evdot,"
          " const float* __restrict__ phidot, float* __restrict__ gphi, float* __restrict__ gevec,"
          " float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags) {\n"
-      << "  __shared__ __attribute__((aligned(16))) float sS[" << LDSF * kv.lds_mult << "];\n";
+      << "  __shared__ __attribute__((aligned(16))) float sS[" << LDSF * kv.lds_mult << "];\n"
+      << "  __shared__ int sids[ADJ_W * 256];  // per-wave sender ids of the current segment\n";
     if (NSL > 1)
       o << "  __shared__ float sacc[EB * SB_ADJ_NV(" << (kv.db ? "true" : "false") << ", " << kv.fl << ")];\n";
     else
       o << "  float* sacc = nullptr;\n";
     o << "  sb_adj_body<" << (kv.db ? "true" : "false") << ", " << kv.fl
       << ">(rowptr, sender, evec, phi, x, Sb, Sb2, xdot, evdot, phidot, gphi, gevec, contrib, r0, n_recv, ncap, e0,"
-         " flags, sS, sS + " << (kv.lds_mult == 2 ? LDSF : 0) << ", sacc);\n}\n";
+         " flags, sS, sS + " << (kv.lds_mult == 2 ? LDSF : 0) << ", sacc, sids);\n}\n";
   }
   return o.str();
 }
