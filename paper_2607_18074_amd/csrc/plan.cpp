@@ -564,7 +564,48 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
 //   C[r] = sum_k x[r][m_i] M_k;  phibar[q] += Sbar[q][m][u_r] C[r]  (4x4x1)
 //   xbar[r][m_i] += M_k G[r];   Ybar[m_y] += c sum_r x[r][m_i] G[r]
 // and the double-backward analogues with the tangents of Y, phi, x and A.
-void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off) {
+// One (path, m_o) block of an adjoint slab: the unit whose adjoint-state
+// operands are loaded from LDS together.
+struct AdjBlock {
+  int t, off, DO, m;
+};
+
+// The blocks of a slab in emission order (items, their paths, output components
+// with a nonzero coupling).
+std::vector<AdjBlock> adj_blocks(const Plan& P, const AdjSlab& sl) {
+  std::vector<AdjBlock> v;
+  for (const AdjItem& it : sl.items)
+    for (size_t pi = 0; pi < it.paths.size(); ++pi) {
+      const Path& q = P.paths[it.paths[pi]];
+      const PathTerms pt = path_terms(q);
+      const int DO = 2 * q.l_out + 1;
+      for (int m = 0; m < DO; ++m) {
+        bool any = false;
+        for (auto& pr : pt.pairs) any = any || pr.second == m;
+        if (any) v.push_back({it.paths[pi], it.lds_off[pi], DO, m});
+      }
+    }
+  return v;
+}
+
+// LDS loads of block b's adjoint-state operands into gA<b> (16x16x4 A operand:
+// Sbar[q = 4v + g][m][u = es]) and pA<b> (4x4x1 A operands: Sbar[q = 4v + l3][m][4g .. 4g + 3]).
+// Backward only: the double-backward kernels keep more per-edge state live and
+// read the operands at use instead.
+void emit_adj_operands(std::ostringstream& o, const std::vector<AdjBlock>& bl, int b, const char* ind) {
+  const AdjBlock& x = bl[b];
+  o << ind << "if (!DB) {\n" << ind << "  const float* Sq = sS + " << x.off << " + zz;\n"
+    << "#pragma unroll\n" << ind << "  for (int v = 0; v < KQ; ++v) {\n"
+    << ind << "    gA" << b << "[v] = Sq[((4 * v + g) * " << x.DO << " + " << x.m << ") * 16 + es];\n"
+    << ind << "    pA" << b << "[v] = *(const sb_f4*)(Sq + ((4 * v + l3) * " << x.DO << " + " << x.m << ") * 16 + 4 * g);\n"
+    << ind << "  }\n" << ind << "}\n";
+}
+
+// Path t of an adjoint item; `bl`/`b` are the slab's blocks and the index of the
+// path's first block, advanced past its blocks.  A block's adjoint-state operands
+// are in registers when it starts (loaded by the previous block, the last block
+// loading the first one's for the next iteration), so no block waits on LDS.
+void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off, const std::vector<AdjBlock>& bl, int& b) {
   const Path& q = P.paths[t];
   const int DO = 2 * q.l_out + 1, Y0 = q.l_sh * q.l_sh;
   const PathTerms pt = path_terms(q);
@@ -582,15 +623,24 @@ void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off) {
   // G tile of component m against radial features `ph` and adjoint state `sp`
   auto gtile = [&](const char* dst, const char* sp, const char* ph, int m) {
     std::ostringstream e;
-    e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) " << dst << " = sb_mfma(" << sp << "[((4 * v + g) * " << DO
-      << " + " << m << ") * 16 + es], " << ph << "[v], " << dst << ");\n";
+    if (std::string(sp) == "Sp")  // registers in the backward; LDS in the double backward (register budget)
+      e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) " << dst << " = sb_mfma(DB ? " << sp
+        << "[((4 * v + g) * " << DO << " + " << m << ") * 16 + es] : gA" << b << "[v], " << ph << "[v], " << dst << ");\n";
+    else
+      e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) " << dst << " = sb_mfma(" << sp << "[((4 * v + g) * " << DO
+        << " + " << m << ") * 16 + es], " << ph << "[v], " << dst << ");\n";
     return e.str();
   };
   // phibar[q] += sum_r Sbar[q][m][u_r] c[r]
   auto ptile = [&](const char* sp, const char* cn, int m) {
     std::ostringstream e;
-    e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) {\n"
-      << "              const sb_f4 a = *(const sb_f4*)(" << sp << " + ((4 * v + l3) * " << DO << " + " << m << ") * 16 + 4 * g);\n"
+    e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) {\n";
+    if (std::string(sp) == "Sp")
+      e << "              const sb_f4 a = DB ? *(const sb_f4*)(" << sp << " + ((4 * v + l3) * " << DO << " + " << m
+        << ") * 16 + 4 * g) : pA" << b << "[v];\n";
+    else
+      e << "              const sb_f4 a = *(const sb_f4*)(" << sp << " + ((4 * v + l3) * " << DO << " + " << m << ") * 16 + 4 * g);\n";
+    e
       << "              pacc[v] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[0], " << cn << "0, pacc[v], 0, 0, 0);\n"
       << "              pacc[v] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[1], " << cn << "1, pacc[v], 0, 0, 0);\n"
       << "              pacc[v] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[2], " << cn << "2, pacc[v], 0, 0, 0);\n"
@@ -679,6 +729,9 @@ void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off) {
         o << "          if (HAS_YB) asm volatile(\"\" : \"+v\"(yb[" << Y0 + my << "]));\n";
       }
     }
+    if (bl[b].t != t || bl[b].m != m) throw std::runtime_error("adjoint block order mismatch");
+    emit_adj_operands(o, bl, (b + 1) % (int)bl.size(), "          ");
+    ++b;
     o << "          __builtin_amdgcn_sched_barrier(0);\n"
       << "        }\n";
   }
@@ -769,6 +822,12 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
   };
   fetch_edge("0");
   for (size_t i = 0; i < sl.items.size(); ++i) fetch_x(i, "  ");
+  const std::vector<AdjBlock> bl = adj_blocks(P, sl);
+  for (size_t bi = 0; bi < bl.size(); ++bi) o << "  float gA" << bi << "[KQ]; sb_f4 pA" << bi << "[KQ];\n";
+  o << "  {\n    int zz = 0;\n    asm volatile(\"\" : \"+v\"(zz));\n";
+  emit_adj_operands(o, bl, 0, "    ");
+  o << "  }\n";
+  int blk = 0;
   o << "  for (int it = 0; it < niter; ++it) {\n"
        "    const int kl = (it * ADJ_W + w) * 16 + es;\n"
        "    const int k = seg + kl;\n"
@@ -831,7 +890,7 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
         << "          if (u + r < CA) {\n"
         << "#pragma unroll\n            for (int m = 0; m < DA; ++m) xdv[r][m] = xdot[srow + AOFF + m * CA + u + r];\n"
         << "          }\n      }\n";
-    for (size_t pi = 0; pi < it.paths.size(); ++pi) emit_adj_path(o, P, it.paths[pi], it.lds_off[pi]);
+    for (size_t pi = 0; pi < it.paths.size(); ++pi) emit_adj_path(o, P, it.paths[pi], it.lds_off[pi], bl, blk);
     o << "      if (contrib && ev) {\n"
       << "        float* cr = contrib + (sb_i64)(e - e0) * CXI + AOFF + u;\n";
     if (v4)
