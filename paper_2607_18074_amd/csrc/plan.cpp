@@ -588,17 +588,22 @@ std::vector<AdjBlock> adj_blocks(const Plan& P, const AdjSlab& sl) {
   return v;
 }
 
-// LDS loads of block b's adjoint-state operands into gA<b> (16x16x4 A operand:
-// Sbar[q = 4v + g][m][u = es]) and pA<b> (4x4x1 A operands: Sbar[q = 4v + l3][m][4g .. 4g + 3]).
-// Backward only: the double-backward kernels keep more per-edge state live and
-// read the operands at use instead.
-void emit_adj_operands(std::ostringstream& o, const std::vector<AdjBlock>& bl, int b, const char* ind) {
+// Backward (DB = false) block pipeline.  Block b's G tile (sum_q phi[q] Sbar[q][m][u],
+// 16x16x4 MFMA) is issued by block b - 1 (by the iteration start for b = 0), from
+// operands gA<b> that block b - 2 loaded from LDS; so each block's VALU work finds
+// its G tile finished and overlaps the next block's MFMAs.  The double-backward
+// kernels keep more per-edge state live and compute G in-block from LDS.
+void emit_adj_gload(std::ostringstream& o, const std::vector<AdjBlock>& bl, int b, const char* ind) {
   const AdjBlock& x = bl[b];
-  o << ind << "if (!DB) {\n" << ind << "  const float* Sq = sS + " << x.off << " + zz;\n"
-    << "#pragma unroll\n" << ind << "  for (int v = 0; v < KQ; ++v) {\n"
-    << ind << "    gA" << b << "[v] = Sq[((4 * v + g) * " << x.DO << " + " << x.m << ") * 16 + es];\n"
-    << ind << "    pA" << b << "[v] = *(const sb_f4*)(Sq + ((4 * v + l3) * " << x.DO << " + " << x.m << ") * 16 + 4 * g);\n"
-    << ind << "  }\n" << ind << "}\n";
+  o << ind << "if (!DB) {\n"
+    << "#pragma unroll\n" << ind << "  for (int v = 0; v < KQ; ++v) gA" << b << "[v] = (sS + " << x.off << " + zz)[((4 * v + g) * "
+    << x.DO << " + " << x.m << ") * 16 + es];\n" << ind << "}\n";
+}
+
+void emit_adj_gtile(std::ostringstream& o, int b, const char* ind) {
+  o << ind << "if (!DB) {\n" << ind << "  G" << b << " = (sb_f4){0.f, 0.f, 0.f, 0.f};\n"
+    << "#pragma unroll\n" << ind << "  for (int v = 0; v < KQ; ++v) G" << b << " = sb_mfma(gA" << b << "[v], phB[v], G" << b
+    << ");\n" << ind << "}\n";
 }
 
 // Path t of an adjoint item; `bl`/`b` are the slab's blocks and the index of the
@@ -623,11 +628,7 @@ void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off, const s
   // G tile of component m against radial features `ph` and adjoint state `sp`
   auto gtile = [&](const char* dst, const char* sp, const char* ph, int m) {
     std::ostringstream e;
-    if (std::string(sp) == "Sp")  // registers in the backward; LDS in the double backward (register budget)
-      e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) " << dst << " = sb_mfma(DB ? " << sp
-        << "[((4 * v + g) * " << DO << " + " << m << ") * 16 + es] : gA" << b << "[v], " << ph << "[v], " << dst << ");\n";
-    else
-      e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) " << dst << " = sb_mfma(" << sp << "[((4 * v + g) * " << DO
+    e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) " << dst << " = sb_mfma(" << sp << "[((4 * v + g) * " << DO
         << " + " << m << ") * 16 + es], " << ph << "[v], " << dst << ");\n";
     return e.str();
   };
@@ -635,9 +636,9 @@ void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off, const s
   auto ptile = [&](const char* sp, const char* cn, int m) {
     std::ostringstream e;
     e << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) {\n";
-    if (std::string(sp) == "Sp")
+    if (std::string(sp) == "Sp")  // the backward loaded this block's operands at its start
       e << "              const sb_f4 a = DB ? *(const sb_f4*)(" << sp << " + ((4 * v + l3) * " << DO << " + " << m
-        << ") * 16 + 4 * g) : pA" << b << "[v];\n";
+        << ") * 16 + 4 * g) : pA[v];\n";
     else
       e << "              const sb_f4 a = *(const sb_f4*)(" << sp << " + ((4 * v + l3) * " << DO << " + " << m << ") * 16 + 4 * g);\n";
     e
@@ -681,9 +682,21 @@ void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off, const s
     for (int k = 0; k < (int)pt.pairs.size(); ++k)
       if (pt.pairs[k].second == m) ks.push_back(k);
     if (ks.empty()) continue;
+    if (bl[b].t != t || bl[b].m != m) throw std::runtime_error("adjoint block order mismatch");
+    const int nbk = (int)bl.size();
     o << "        {  // m_o = " << m << "\n";
+    // backward pipeline: operands two blocks ahead, the next block's G tile, this block's 4x4x1 operands
+    emit_adj_gload(o, bl, (b + 2) % nbk, "          ");
+    if (b + 1 < nbk) emit_adj_gtile(o, b + 1, "          ");
+    o << "          sb_f4 pA[KQ];\n"
+      << "          if (!DB) {\n"
+      << "#pragma unroll\n            for (int v = 0; v < KQ; ++v) pA[v] = *(const sb_f4*)(Sp + ((4 * v + l3) * " << DO << " + "
+      << m << ") * 16 + 4 * g);\n"
+      << "          }\n";
     for (int k : ks) o << "          const float M" << k << " = " << yexpr(pt.terms[k], "Y") << ";\n";
-    o << "          sb_f4 G = (sb_f4){0.f, 0.f, 0.f, 0.f};\n" << "  " << gtile("G", "Sp", "phB", m);
+    o << "          sb_f4 G = (sb_f4){0.f, 0.f, 0.f, 0.f};\n"
+      << "          if (!DB) {\n            G = G" << b << ";\n          } else {\n  " << gtile("G", "Sp", "phB", m)
+      << "          }\n";
     o << "          if (!DB) {\n";
     for (int r = 0; r < 4; ++r) o << "            const float c" << r << " = " << cexpr(ks, "xv", "M", r) << ";\n";
     o << ptile("Sp", "c", m) << xupd(ks, "M", "G") << yupd(ks, "xv", "G", "gy");
@@ -729,8 +742,6 @@ void emit_adj_path(std::ostringstream& o, const Plan& P, int t, int off, const s
         o << "          if (HAS_YB) asm volatile(\"\" : \"+v\"(yb[" << Y0 + my << "]));\n";
       }
     }
-    if (bl[b].t != t || bl[b].m != m) throw std::runtime_error("adjoint block order mismatch");
-    emit_adj_operands(o, bl, (b + 1) % (int)bl.size(), "          ");
     ++b;
     o << "          __builtin_amdgcn_sched_barrier(0);\n"
       << "        }\n";
@@ -780,7 +791,9 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        "  for (int seg = 0; seg < nb; seg += 256) {\n"
        "  const int sn = min(256, nb - seg), sbase = ebase + seg;\n"
        "#pragma unroll\n  for (int i = 0; i < 4; ++i) wids[64 * i + lane] = sender[sbase + min(64 * i + lane, sn - 1)];\n"
-       "  const int niter = (sn + 16 * ADJ_W - 1) / (16 * ADJ_W);\n"
+       // this wave's 16-edge batches are w, w + ADJ_W, ...: a wave whose last batch would
+       // be empty stops one iteration early instead of computing on padding
+       "  const int niter = ((sn + 15) / 16 - w + ADJ_W - 1) / ADJ_W;\n"
        // edge data and sender rows of the next iteration, loaded one iteration
        // ahead (clamped to the segment's last edge, masked at use)
        "  float nvx, nvy, nvz, ndx = 0.f, ndy = 0.f, ndz = 0.f, nph[KQ], nphd[KQ];\n"
@@ -823,9 +836,10 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
   fetch_edge("0");
   for (size_t i = 0; i < sl.items.size(); ++i) fetch_x(i, "  ");
   const std::vector<AdjBlock> bl = adj_blocks(P, sl);
-  for (size_t bi = 0; bi < bl.size(); ++bi) o << "  float gA" << bi << "[KQ]; sb_f4 pA" << bi << "[KQ];\n";
+  for (size_t bi = 0; bi < bl.size(); ++bi) o << "  float gA" << bi << "[KQ]; sb_f4 G" << bi << ";\n";
   o << "  {\n    int zz = 0;\n    asm volatile(\"\" : \"+v\"(zz));\n";
-  emit_adj_operands(o, bl, 0, "    ");
+  emit_adj_gload(o, bl, 0, "    ");
+  if (bl.size() > 1) emit_adj_gload(o, bl, 1, "    ");
   o << "  }\n";
   int blk = 0;
   o << "  for (int it = 0; it < niter; ++it) {\n"
@@ -856,6 +870,7 @@ void emit_adj_slab(std::ostringstream& o, const Plan& P, int s) {
        "    int zz = 0;\n    asm volatile(\"\" : \"+v\"(zz));\n"
     << "    float Y[" << NS << "], Yd[" << NS << "];\n    sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
     << "    if (DB && (fl & 4)) sb_sh_jvp_L" << L << "(ux, uy, uz, rinv, dx, dy, dz, Y, Yd);\n";
+  emit_adj_gtile(o, 0, "    ");
   for (size_t ii = 0; ii < sl.items.size(); ++ii) {
     const AdjItem& it = sl.items[ii];
     const Irrep& ri = P.in[it.a];
