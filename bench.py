@@ -168,7 +168,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="stress")
-    ap.add_argument("--budget", type=float, default=2.0, help="workspace budget per pass, GiB")
+    ap.add_argument("--budget", type=float, default=8.0, help="workspace budget per pass, GiB")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", type=float, default=0.0,

@@ -367,8 +367,8 @@ int run_sbar(const Plan& p, const Chunk& c, const WsPlan& w, const float* M, con
     float* Sg = Sbar + (size_t)w.ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     if (p.vec4)
-      LAUNCH(p.k.gemm_sbar_v, cdiv(nrows, 128), cdiv(D, 64), 1, s, M, nrows, D, W,
-             (const int*)(p.d_ktab + g.ktab_off), Sg, dg, Cg, off, CX, r0);
+      LAUNCH(p.k.gemm_sbar_c.at(g.C), cdiv(nrows, 64), 1, 1, s, M, nrows, D, W, (const int*)(p.d_ktab + g.ktab_off),
+             Sg, dg, off, CX, r0);
     else
       LAUNCH(p.k.gemm_sbar[2], cdiv(nrows, 64), cdiv(D, 64), 1, s, M, nrows, D, W,
              (const int*)(p.d_ktab + g.ktab_off), Sg, dg, Cg, off, CX, r0);
@@ -479,6 +479,14 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
       return rc;
   }
   if ((rc = get(p.k.gemm_sbar_v, "sobek_gemm_sbar_v"))) return rc;
+  if (p.vec4)
+    for (auto& g : p.groups)
+      if (!p.k.gemm_sbar_c.count(g.C)) {
+        std::string nm = "sobek_gemm_sbar_c" + std::to_string(g.C);
+        hipFunction_t f = nullptr;
+        if ((rc = get(f, nm.c_str()))) return rc;
+        p.k.gemm_sbar_c[g.C] = f;
+      }
   HIPCHK(hipMalloc(&p.d_ktab, std::max<size_t>(4, p.ktab.size() * 4)));
   HIPCHK(hipMemcpy(p.d_ktab, p.ktab.data(), p.ktab.size() * 4, hipMemcpyHostToDevice));
   auto blocks = [](const std::vector<sobek::Irrep>& v) {

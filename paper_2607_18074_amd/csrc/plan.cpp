@@ -1030,6 +1030,17 @@ std::string generate_source(const Plan& P) {
   emit_sh(o, P.lmax);
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
 
+  // streaming adjoint-state GEMM, one instantiation per output multiplicity
+  if (P.vec4) {
+    std::vector<int> cgs;
+    for (auto& g : P.groups)
+      if (std::find(cgs.begin(), cgs.end(), g.C) == cgs.end()) cgs.push_back(g.C);
+    for (int C : cgs)
+      o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_gemm_sbar_c" << C
+        << "(const float* M, int nrows, int D, const float* W, const int* ktab, float* Sbar, int dg, int off, int CX,"
+           " int r0) {\n  sb_gemm_sbar_s<" << C << ">(M, nrows, D, W, ktab, Sbar, dg, off, CX, r0);\n}\n";
+  }
+
   // x-gradient gather over the sender-sorted view, specialised on the input width
   o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_sender_reduce(const int* send_rowptr,"
        " const int* send_perm, const float* contrib, float* gx, int* cursor, int N, int CX, int e0, int e1,"

@@ -73,6 +73,7 @@ struct Kernels {
   hipFunction_t bwd_E = nullptr, dbwd_E = nullptr, dbwd_E_r = nullptr;
   hipFunction_t gemm_sa[3] = {}, gemm_sbar[3] = {}, gemm_ga[3] = {};  // BN = 16, 32, 64
   hipFunction_t gemm_sa_v[3] = {}, gemm_ga_v[3] = {}, gemm_sbar_v = nullptr;  // 16-byte aligned operands
+  std::map<int, hipFunction_t> gemm_sbar_c;  // streaming adjoint-state GEMM per output multiplicity
   hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
                 zero = nullptr;
 };

@@ -2,7 +2,7 @@
 
 Each case builds the workload's own graph and tensors (up to 200,000 nodes and
 16.0M edges) and runs the library in the launch configuration the benchmark
-times: a 2 GiB workspace budget per pass, hence several receiver chunks, and
+times: an 8 GiB workspace budget per pass (several receiver chunks on the stress graph), and
 for the double backward an edge-vector-only cotangent (the flag set of the
 benchmark's "sum of squared edge-vector gradients" loss).  The float64 oracle
 cannot run these graphs whole, so the comparison uses outputs it can compute
@@ -31,7 +31,7 @@ from tests.cases import BWD_TOL, FWD_TOL, edge_subgraph, in_edges, max_rel, std_
 
 pytestmark = pytest.mark.gpu
 
-BUDGET = 2 << 30   # workspace bytes per pass, as in the benchmark
+BUDGET = 8 << 30   # workspace bytes per pass, as in the benchmark
 
 # (sampled receivers, sampled senders); the tiny graph is compared whole
 SAMPLES = {"tiny": (None, None), "small": (60, 40), "medium": (32, 20), "wide": (8, 6), "stress": (48, 32)}
