@@ -78,6 +78,98 @@ def flop_model(plan, N, E):
     return dict(SD=SD, NZ=NZ, G=G, per_kernel=per_kernel, passes=passes)
 
 
+def byte_model(plan, N, E):
+    """Algorithmic HBM bytes per pass: inputs read once, outputs written once (fp32)."""
+    K, Nw, Cx, Co = plan.K, plan.n_weights, plan.dim_in, plan.dim_out
+    fwd = 4 * (N * Cx + E * (3 + K + 1) + (N + 1) + K * Nw + N * Co)
+    bwd = fwd + 4 * (N * Cx + E * (K + 3) + K * Nw)
+    dbwd = bwd + 4 * (E * 3 + N * Co)   # edge-vector cotangent read, g_gout written
+    return {"fwd": fwd, "bwd": bwd, "dbwd": dbwd}
+
+
+def time_pass(fn, torch):
+    """The paper's protocol: warm-up of at least 5 calls and 50 ms, then 10-30 event-timed samples
+    totalling at least 250 ms; the median sample."""
+    t0, n = time.perf_counter(), 0
+    while n < 5 or time.perf_counter() - t0 < 0.05:
+        fn()
+        torch.cuda.synchronize()
+        n += 1
+    samples = []
+    while len(samples) < 10 or (sum(samples) < 250.0 and len(samples) < 30):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        torch.cuda.synchronize()
+        samples.append(a.elapsed_time(b))
+    return float(np.median(samples)), len(samples)
+
+
+def sweep(budget_gib, names):
+    """Every workload and pass of the benchmark configurations: one JSON line each, then a table."""
+    import torch
+
+    from paper_2607_18074_amd import api
+    from paper_2607_18074_amd import workloads as wl
+    torch.cuda.set_device(0)
+    budget = int(budget_gib * (1 << 30))
+    rows = []
+    for name in names:
+        cfg = wl.CONFIGS[name]
+        g = wl.config_graph(name)
+        plan = api.Plan(cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"])
+        T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+        graph = api.Graph(T(g.rowptr), T(g.sender))
+        xt = T(wl.node_features(g.N, plan.dim_in, cfg["index"]))
+        Wt = T(wl.weights(plan.K, plan.weight_std(), cfg["index"]))
+        gt = T(wl.out_cotangent(g.N, plan.dim_out, cfg["index"]))
+        ev, ph = T(g.evec), T(g.phi)
+        ws = {}   # one pass's workspace at a time, so each pass's peak counts only what it needs
+        state = api.new_state(plan, graph) if "bwd" in cfg["passes"] else None
+        out = torch.empty(g.N, plan.dim_out, device="cuda")
+        fm, bm = flop_model(plan, g.N, g.E), byte_model(plan, g.N, g.E)
+        fns = {"fwd": lambda: api.conv_fwd(plan, graph, xt, ev, ph, Wt, out=out, ws=ws["fwd"], state=state)}
+        if "bwd" in cfg["passes"]:
+            fns["bwd"] = lambda: api.conv_bwd(plan, graph, xt, ev, ph, Wt, gt, ws=ws["bwd"], state=state)
+        if "dbwd" in cfg["passes"]:
+            fns["dbwd"] = lambda: api.conv_dbwd(plan, graph, xt, ev, ph, Wt, gt, t_gevec=rdot, ws=ws["dbwd"])
+        rdot = None
+        for pname in cfg["passes"]:
+            for k in list(ws):
+                del ws[k]
+            graph._ws.clear()
+            torch.cuda.empty_cache()
+            ws[pname] = graph.workspace(plan, pname, budget)
+            if pname == "bwd":         # the backward reads the state kept by a forward
+                ws["fwd"] = ws["bwd"]
+                fns["fwd"]()
+                del ws["fwd"]
+            if pname == "dbwd":        # loss: sum of squared edge-vector gradients
+                ws["bwd"] = ws["dbwd"]
+                rdot = (2.0 * fns["bwd"]()[1]).contiguous()
+                del ws["bwd"]
+            torch.cuda.synchronize()
+            torch.cuda.reset_peak_memory_stats()
+            ms, n = time_pass(fns[pname], torch)
+            tf = fm["passes"][pname] / (ms * 1e-3) / 1e12
+            gbs = bm[pname] / (ms * 1e-3) / 1e9
+            row = dict(workload=name, pass_=pname, N=g.N, E=g.E, ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3),
+                       tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS, alg_gbs=gbs, frac_hbm=gbs / PEAK_HBM_GBS,
+                       peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9,
+                       workspace_gb=ws[pname].numel() / 1e9,
+                       retained_state_gb=0.0 if state is None else state.numel() * 4 / 1e9)
+            rows.append(row)
+            print(json.dumps({k.rstrip("_"): v for k, v in row.items()}), flush=True)
+        del fns, ws, state, out, xt, Wt, gt, ev, ph, graph, plan
+        torch.cuda.empty_cache()
+    log("| workload | pass | E | ms (median) | edges/s | TFLOP/s | % fp32 | alg. GB/s | peak GB |")
+    log("|---|---|---:|---:|---:|---:|---:|---:|---:|")
+    for r in rows:
+        log(f"| {r['workload']} | {r['pass_']} | {r['E']:,} | {r['ms']:.3f} | {r['edges_per_s'] / 1e6:,.1f} M | "
+            f"{r['tflops']:.1f} | {100 * r['frac_fp32']:.1f} | {r['alg_gbs']:.0f} | {r['peak_mem_gb']:.2f} |")
+
+
 PAPER_CONTEXT = {
     "hardware": "NVIDIA RTX 5090 (32 GiB), fp32 throughout, eager, 128 MiB scratch budget (Section 5.1)",
     "workloads": "fixed 128-node degree-32 graph repeated B times, uvw profiles with K = 16 (Section 5.1, Table 3)",
@@ -171,6 +263,8 @@ def main():
     ap.add_argument("--budget", type=float, default=8.0, help="workspace budget per pass, GiB")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--sweep", default="", help="comma-separated workloads (or 'all'): time every pass of each "
+                    "with the paper's protocol instead of the step benchmark, one JSON line per pass")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
                     help="only run a plain device copy of this many MiB (traffic-counter calibration)")
     args = ap.parse_args()
@@ -188,6 +282,11 @@ def main():
         print("bench.py runs on one GPU only: this build has no multi-GPU path (see DESIGN.md for how it "
               "would shard); rerun with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.sweep:
+        names = ["tiny", "small", "medium", "wide", "stress"] if args.sweep == "all" else args.sweep.split(",")
+        sweep(args.budget, names)
+        return
 
     import torch
 

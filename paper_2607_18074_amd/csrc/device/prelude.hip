@@ -370,20 +370,24 @@ SB_DEV void sb_gemm_sbar_v(const float* __restrict__ M, int nrows, int D, const 
 
 // Sbar[r, k] = sum_w mbar(r, w) A_g[k, w], streaming: a block owns 64 rows and
 // walks all D columns in 64-column tiles.  Its mbar rows stay in LDS (transposed,
-// [w][row]); the A_g tile of the next 64 columns is loaded into registers while
-// the current one is consumed, then swapped into the other LDS buffer, so the
-// block never waits on memory between tiles.  The product is taken transposed,
-// Sbar^T tile = A_g tile x mbar^T (16x16x4 MFMA, A rows = k, B columns = rows),
-// which leaves lane (j + 16 g) with columns 4g .. 4g + 3 of row j: one float4
-// store per 16x16 tile and lane.  CG (the group's multiplicity) is a multiple of 4.
+// [w][row]); A_g is consumed in slices of 64 columns x 32 w, the next slice loaded
+// into registers while the current one is multiplied and then swapped into the
+// other LDS buffer, so the block never waits on memory between slices and its LDS
+// does not grow past one 32-wide slice pair with the multiplicity.  The product is
+// taken transposed, Sbar^T tile = A_g tile x mbar^T (16x16x4 MFMA, A rows = k,
+// B columns = rows), which leaves lane (j + 16 g) with columns 4g .. 4g + 3 of row
+// j: one float4 store per 16x16 tile and lane.  CG (the group's multiplicity) is a
+// multiple of 4.
 template <int CG>
 SB_DEV void sb_gemm_sbar_s(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
                            const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int off, int CX, int r0) {
-  constexpr int PAD = 68;                     // row pitch of the transposed LDS tiles (floats)
-  constexpr int NV = CG / 4;                  // float4 per row of mbar / A_g
-  constexpr int NBL = (64 * NV + 255) / 256;  // float4 loads of an A_g tile per thread
+  constexpr int PAD = 68;                       // row pitch of the transposed LDS tiles (floats)
+  constexpr int NV = CG / 4;                    // float4 per row of mbar
+  constexpr int WC = CG < 32 ? CG : 32;         // w per slice
+  constexpr int NS = (CG + WC - 1) / WC;        // slices per column tile
+  constexpr int NBL = (64 * (WC / 4) + 255) / 256;  // float4 loads of a slice per thread
   __shared__ float sM[CG][PAD];
-  __shared__ float sB[2][CG][PAD];
+  __shared__ float sB[2][WC][PAD];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int j = lane & 15, g = lane >> 4;
   const int rb = blockIdx.x * 64;
@@ -395,20 +399,22 @@ SB_DEV void sb_gemm_sbar_s(const float* __restrict__ M, int nrows, int D, const 
     for (int c = 0; c < 4; ++c) sM[w4 + c][row] = v[c];
   }
   sb_v4 rbv[NBL];
-  auto loadB = [&](int k0) {
+  auto loadB = [&](int sl) {  // slice sl = (column tile, w chunk)
+    const int k0 = (sl / NS) * 64, w0 = (sl % NS) * WC;
 #pragma unroll
     for (int i = 0; i < NBL; ++i) {
       const int idx = tid + 256 * i;
-      const int kc = idx / NV, w4 = 4 * (idx % NV), gk = k0 + kc;
-      rbv[i] = (idx < 64 * NV && gk < D) ? sb_ld4(W + (sb_i64)ktab[gk] + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+      const int kc = idx / (WC / 4), w4 = 4 * (idx % (WC / 4)), gk = k0 + kc;
+      rbv[i] = (idx < 64 * (WC / 4) && gk < D && w0 + w4 < CG) ? sb_ld4(W + (sb_i64)ktab[gk] + w0 + w4)
+                                                                 : (sb_v4){0.f, 0.f, 0.f, 0.f};
     }
   };
   auto storeB = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < NBL; ++i) {
       const int idx = tid + 256 * i;
-      if (idx < 64 * NV) {
-        const int kc = idx / NV, w4 = 4 * (idx % NV);
+      if (idx < 64 * (WC / 4)) {
+        const int kc = idx / (WC / 4), w4 = 4 * (idx % (WC / 4));
 #pragma unroll
         for (int c = 0; c < 4; ++c) sB[buf][w4 + c][kc] = rbv[i][c];
       }
@@ -417,29 +423,31 @@ SB_DEV void sb_gemm_sbar_s(const float* __restrict__ M, int nrows, int D, const 
   loadB(0);
   storeB(0);
   __syncthreads();
-  const int nkt = (D + 63) / 64;
+  const int nsl = (D + 63) / 64 * NS;
   const int row = rb + 16 * wave + j;
   float* out = Sbar + (sb_i64)row * D;
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nkt) loadB((kt + 1) * 64);
-    sb_f4 acc[4];
+  sb_f4 acc[4];
+  for (int sl = 0; sl < nsl; ++sl) {
+    const int buf = sl & 1, w0 = (sl % NS) * WC;
+    if (sl + 1 < nsl) loadB(sl + 1);
+    if (w0 == 0) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < 4; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
-    for (int w = 0; w < CG; w += 4) {
-      const float b = sM[w + g][16 * wave + j];
+    for (int w = 0; w < WC; w += 4) {
+      const float b = sM[w0 + w + g][16 * wave + j];
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = sb_mfma(sB[buf][w + g][16 * t + j], b, acc[t]);
     }
-    if (row < nrows) {
+    if (w0 + WC >= CG && row < nrows) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int k = kt * 64 + 16 * t + 4 * g;
+        const int k = (sl / NS) * 64 + 16 * t + 4 * g;
         if (k < D) *(sb_v4*)(out + k) = acc[t];
       }
     }
-    if (kt + 1 < nkt) storeB(buf ^ 1);
+    if (sl + 1 < nsl) storeB(buf ^ 1);
     __syncthreads();
   }
 }
