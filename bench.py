@@ -11,7 +11,8 @@ other three cotangents zero.  Inputs are resident in HBM before timing.
 The forward keeps the receiver state S of every receiver (node-bounded:
 N * K * SD floats, 7.2 GB for this workload) and the backward's weight
 gradient reads it, as the paper's schedule allows when the state fits; the
-double backward computes its directional state dS from scratch.
+backward keeps the adjoint state Sbar = gout A^T (same size) for the double
+backward, which computes its directional state dS from scratch.
 
 value = E / (seconds per step): whole-step edge throughput on one GPU.
 roofline: the kernel with the largest share of the timed region, its
@@ -74,7 +75,9 @@ def flop_model(plan, N, E):
         "fwd_S": edge_fwd, "fwd_dS": edge_fwd, "bwd_E": edge_adj, "dbwd_E": edge_adj,
         "gemm_sa": gemm, "gemm_sbar": gemm, "gemm_ga": gemm,
     }
-    passes = {"fwd": edge_fwd + gemm, "bwd": 2 * gemm + edge_adj, "dbwd": edge_fwd + 3 * gemm + edge_adj}
+    # fwd: S, m = S A; bwd: Sbar = mbar A^T, A_bar = S^T mbar (S kept by the forward), edge adjoints;
+    # dbwd (edge-vector cotangent): dS, m_dot = dS A, g_A = dS^T mbar (Sbar kept by the backward), edge terms
+    passes = {"fwd": edge_fwd + gemm, "bwd": 2 * gemm + edge_adj, "dbwd": edge_fwd + 2 * gemm + edge_adj}
     return dict(SD=SD, NZ=NZ, G=G, per_kernel=per_kernel, passes=passes)
 
 
@@ -127,13 +130,16 @@ def sweep(budget_gib, names):
         ev, ph = T(g.evec), T(g.phi)
         ws = {}   # one pass's workspace at a time, so each pass's peak counts only what it needs
         state = api.new_state(plan, graph) if "bwd" in cfg["passes"] else None
+        adj = api.new_state(plan, graph) if "dbwd" in cfg["passes"] else None
         out = torch.empty(g.N, plan.dim_out, device="cuda")
         fm, bm = flop_model(plan, g.N, g.E), byte_model(plan, g.N, g.E)
         fns = {"fwd": lambda: api.conv_fwd(plan, graph, xt, ev, ph, Wt, out=out, ws=ws["fwd"], state=state)}
         if "bwd" in cfg["passes"]:
-            fns["bwd"] = lambda: api.conv_bwd(plan, graph, xt, ev, ph, Wt, gt, ws=ws["bwd"], state=state)
+            fns["bwd"] = lambda: api.conv_bwd(plan, graph, xt, ev, ph, Wt, gt, ws=ws["bwd"], state=state,
+                                              adj_state=adj)
         if "dbwd" in cfg["passes"]:
-            fns["dbwd"] = lambda: api.conv_dbwd(plan, graph, xt, ev, ph, Wt, gt, t_gevec=rdot, ws=ws["dbwd"])
+            fns["dbwd"] = lambda: api.conv_dbwd(plan, graph, xt, ev, ph, Wt, gt, t_gevec=rdot, ws=ws["dbwd"],
+                                                adj_state=adj)
         rdot = None
         for pname in cfg["passes"]:
             for k in list(ws):
@@ -158,10 +164,10 @@ def sweep(budget_gib, names):
                        tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS, alg_gbs=gbs, frac_hbm=gbs / PEAK_HBM_GBS,
                        peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9,
                        workspace_gb=ws[pname].numel() / 1e9,
-                       retained_state_gb=0.0 if state is None else state.numel() * 4 / 1e9)
+                       retained_state_gb=sum(t.numel() * 4 / 1e9 for t in (state, adj) if t is not None))
             rows.append(row)
             print(json.dumps({k.rstrip("_"): v for k, v in row.items()}), flush=True)
-        del fns, ws, state, out, xt, Wt, gt, ev, ph, graph, plan
+        del fns, ws, state, adj, out, xt, Wt, gt, ev, ph, graph, plan
         torch.cuda.empty_cache()
     log("| workload | pass | E | ms (median) | edges/s | TFLOP/s | % fp32 | alg. GB/s | peak GB |")
     log("|---|---|---:|---:|---:|---:|---:|---:|---:|")
@@ -310,17 +316,18 @@ def main():
     ws = {p: graph.workspace(plan, p, budget) for p in ("fwd", "bwd", "dbwd")}
     out = torch.empty(g.N, plan.dim_out, device=dev)
     state = api.new_state(plan, graph)     # receiver state kept from the forward for the backward
+    adj = api.new_state(plan, graph)       # adjoint state kept from the backward for the double backward
 
     def fwd():
         return api.conv_fwd(plan, graph, xt, ev, ph, Wt, out=out, ws=ws["fwd"], state=state)
 
     def bwd():
-        return api.conv_bwd(plan, graph, xt, ev, ph, Wt, gt, ws=ws["bwd"], state=state)
+        return api.conv_bwd(plan, graph, xt, ev, ph, Wt, gt, ws=ws["bwd"], state=state, adj_state=adj)
 
     rdot = None
 
     def dbwd():
-        return api.conv_dbwd(plan, graph, xt, ev, ph, Wt, gt, t_gevec=rdot, ws=ws["dbwd"])
+        return api.conv_dbwd(plan, graph, xt, ev, ph, Wt, gt, t_gevec=rdot, ws=ws["dbwd"], adj_state=adj)
 
     # cotangent of L2 = sum |evec_bar|^2
     fwd()
@@ -380,7 +387,7 @@ def main():
     if kind in fm["per_kernel"]:
         per_step = fm["per_kernel"][kind]
         if kind.startswith("gemm"):
-            per_step *= {"gemm_sa": 1, "gemm_sbar": 2, "gemm_ga": 2}[kind]  # launches of this GEMM per step
+            per_step *= {"gemm_sa": 2, "gemm_sbar": 1, "gemm_ga": 2}[kind]  # passes running this GEMM per step
         flops_per_launch = per_step * args.steps / dom_n
         achieved = flops_per_launch / (dom_ms / dom_n * 1e-3) / 1e12
         tr = traffic_record(dom_name, sha, dom_n / args.steps)
@@ -433,7 +440,7 @@ def main():
         "passes": passes,
         "peak_mem_gb": peak_gb,
         "workspace_gb": {p: w.numel() / 1e9 for p, w in ws.items()},
-        "retained_state_gb": state.numel() * 4 / 1e9,
+        "retained_state_gb": (state.numel() + adj.numel()) * 4 / 1e9,
         "paper_context": PAPER_CONTEXT,
         "kernels": kernels,
         "wall_s_timed": wall,

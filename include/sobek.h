@@ -165,21 +165,36 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float *x, const flo
  *
  * sobek_conv_fwd_save is sobek_conv_fwd that also leaves S of every receiver in
  * `state` (caller-owned device memory of sobek_state_size bytes, 16-byte
- * aligned; overwritten).  sobek_conv_bwd_saved is sobek_conv_bwd that reads
- * the weight gradient's S from such a state instead of recomputing it; the
- * state must come from sobek_conv_fwd_save with the same plan, graph, x, evec
- * and phi (W may differ: S does not depend on it).  Both take the workspace
- * of their pass (sobek_workspace_size with SOBEK_PASS_FWD / SOBEK_PASS_BWD);
- * results agree with sobek_conv_fwd / sobek_conv_bwd within rounding (the
- * weight gradient's summation splits differ). */
+ * aligned; overwritten).
+ *
+ * sobek_conv_bwd_saved is sobek_conv_bwd with two optional state buffers of
+ * sobek_state_size bytes each (NULL = not used):
+ *   state      read: the weight gradient takes S from it instead of
+ *              recomputing it; it must come from sobek_conv_fwd_save with the
+ *              same plan, graph, x, evec and phi (W may differ: S does not
+ *              depend on it);
+ *   adj_state  written: the adjoint state Sbar = gout A^T (Section 4.3, eq.
+ *              receiver_adjoint) of every receiver, computed once and kept,
+ *              so that a double backward with the same gout and W need not
+ *              recompute it.
+ * sobek_conv_dbwd_saved is sobek_conv_dbwd that reads Sbar from such an
+ * adj_state (same plan, graph, gout and W) instead of recomputing it.
+ * All take the workspace of their pass (sobek_workspace_size with the pass
+ * constant); results agree with the plain calls within rounding (the weight
+ * gradient's summation splits differ). */
 int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t *bytes);
 int sobek_conv_fwd_save(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
                         const float *phi, const float *W, float *out, float *state, void *ws,
                         size_t ws_bytes, hipStream_t stream);
 int sobek_conv_bwd_saved(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
                          const float *phi, const float *W, const float *gout, const float *state,
-                         float *gx, float *gevec, float *gphi, float *gW, void *ws, size_t ws_bytes,
-                         hipStream_t stream);
+                         float *adj_state, float *gx, float *gevec, float *gphi, float *gW, void *ws,
+                         size_t ws_bytes, hipStream_t stream);
+int sobek_conv_dbwd_saved(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                          const float *phi, const float *W, const float *gout, const float *adj_state,
+                          const float *t_gx, const float *t_gevec, const float *t_gphi, const float *t_gW,
+                          float *g_gout, float *g_x, float *g_evec, float *g_phi, float *g_W, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
 
 /* Double backward (Sections 3.3 and 4.4): vector-Jacobian product of the
  * backward map (gout, x, evec, phi, W) -> (gx, gevec, gphi, gW) with

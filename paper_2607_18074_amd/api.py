@@ -181,11 +181,13 @@ def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=No
     return out
 
 
-def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), ws=None, budget=0, state=None):
+def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), ws=None, budget=0, state=None,
+             adj_state=None):
     """(gx, gevec, gphi, gW); entries not in `need` are None.
 
     `state`: the retained receiver state of conv_fwd(..., state=...) with the same x, evec and phi; the
-    weight gradient then reads it instead of recomputing S.
+    weight gradient then reads it instead of recomputing S.  `adj_state` (from new_state): receives the
+    adjoint state Sbar = gout A^T of every receiver, for conv_dbwd(..., adj_state=...).
     """
     N, E = graph.N, graph.E
     _check_tensor(x, "x", (N, plan.dim_in))
@@ -197,20 +199,24 @@ def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), 
     shapes = [(N, plan.dim_in), (E, 3), (E, plan.K), (plan.K, plan.n_weights)]
     outs = [torch.empty(s, dtype=torch.float32, device=dev) if n else None for s, n in zip(shapes, need)]
     _check_state(plan, graph, state)
+    _check_state(plan, graph, adj_state)
     ws = _ws(plan, graph, "bwd", ws, budget)
-    if state is None:
+    if state is None and adj_state is None:
         check(lib().sobek_conv_bwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(gout),
                                    *[_ptr(o) for o in outs], _ptr(ws), ws.numel(), _stream()))
     else:
         check(lib().sobek_conv_bwd_saved(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W),
-                                         _ptr(gout), _ptr(state), *[_ptr(o) for o in outs], _ptr(ws), ws.numel(),
-                                         _stream()))
+                                         _ptr(gout), _ptr(state), _ptr(adj_state), *[_ptr(o) for o in outs],
+                                         _ptr(ws), ws.numel(), _stream()))
     return tuple(outs)
 
 
 def conv_dbwd(plan, graph, x, evec, phi, W, gout, t_gx=None, t_gevec=None, t_gphi=None, t_gW=None,
-              need=(True, True, True, True, True), ws=None, budget=0):
-    """(g_gout, g_x, g_evec, g_phi, g_W); entries not in `need` are None."""
+              need=(True, True, True, True, True), ws=None, budget=0, adj_state=None):
+    """(g_gout, g_x, g_evec, g_phi, g_W); entries not in `need` are None.
+
+    `adj_state`: the adjoint state kept by conv_bwd(..., adj_state=...) with the same gout and W.
+    """
     N, E = graph.N, graph.E
     _check_tensor(x, "x", (N, plan.dim_in))
     _check_tensor(evec, "evec", (E, 3))
@@ -224,10 +230,16 @@ def conv_dbwd(plan, graph, x, evec, phi, W, gout, t_gx=None, t_gevec=None, t_gph
     dev = x.device
     shapes = [(N, plan.dim_out), (N, plan.dim_in), (E, 3), (E, plan.K), (plan.K, plan.n_weights)]
     outs = [torch.empty(s, dtype=torch.float32, device=dev) if n else None for s, n in zip(shapes, need)]
+    _check_state(plan, graph, adj_state)
     ws = _ws(plan, graph, "dbwd", ws, budget)
-    check(lib().sobek_conv_dbwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(gout),
-                                _ptr(t_gx), _ptr(t_gevec), _ptr(t_gphi), _ptr(t_gW), *[_ptr(o) for o in outs],
-                                _ptr(ws), ws.numel(), _stream()))
+    if adj_state is None:
+        check(lib().sobek_conv_dbwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(gout),
+                                    _ptr(t_gx), _ptr(t_gevec), _ptr(t_gphi), _ptr(t_gW), *[_ptr(o) for o in outs],
+                                    _ptr(ws), ws.numel(), _stream()))
+    else:
+        check(lib().sobek_conv_dbwd_saved(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W),
+                                          _ptr(gout), _ptr(adj_state), _ptr(t_gx), _ptr(t_gevec), _ptr(t_gphi),
+                                          _ptr(t_gW), *[_ptr(o) for o in outs], _ptr(ws), ws.numel(), _stream()))
     return tuple(outs)
 
 
@@ -244,13 +256,15 @@ class _TPConvBackward(torch.autograd.Function):
     def forward(ctx, x, evec, phi, W, gout, plan, graph, state):
         ctx.plan, ctx.graph = plan, graph
         ctx.save_for_backward(x, evec, phi, W, gout)
-        return conv_bwd(plan, graph, x, evec, phi, W, gout, state=state)
+        # with retention, the adjoint state is kept for the double backward as well
+        ctx.adj_state = new_state(plan, graph, x.device) if state is not None else None
+        return conv_bwd(plan, graph, x, evec, phi, W, gout, state=state, adj_state=ctx.adj_state)
 
     @staticmethod
     def backward(ctx, t_gx, t_gevec, t_gphi, t_gW):
         x, evec, phi, W, gout = ctx.saved_tensors
         g_gout, g_x, g_evec, g_phi, g_W = conv_dbwd(ctx.plan, ctx.graph, x, evec, phi, W, gout, _c(t_gx),
-                                                    _c(t_gevec), _c(t_gphi), _c(t_gW))
+                                                    _c(t_gevec), _c(t_gphi), _c(t_gW), adj_state=ctx.adj_state)
         return g_x, g_evec, g_phi, g_W, g_gout, None, None, None
 
 
@@ -273,6 +287,7 @@ class TPConv(torch.autograd.Function):
 
 
 def tp_conv(plan, graph, x, evec, phi, W, retain_state=False):
-    """Differentiable convolution.  retain_state=True keeps S of every receiver from the forward (memory
-    N * sobek_state_size / N) so that the backward's weight gradient does not recompute it."""
+    """Differentiable convolution.  retain_state=True keeps S of every receiver from the forward, and Sbar of
+    every receiver from the backward (each sobek_state_size bytes, node-bounded), so that neither the
+    backward's weight gradient nor the double backward recomputes them."""
     return TPConv.apply(x, evec, phi, W, plan, graph, bool(retain_state))

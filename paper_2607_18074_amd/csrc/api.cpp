@@ -252,13 +252,14 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
   if (need > ws_bytes) {
     size_t partial_max = align_up(partial_floats(p, std::max<int64_t>(1, N)) * 4) + 2 * kAlign;
     if (ws_bytes <= w.fixed + partial_max) {
-      w.ncap = 1;
+      w.ncap = per_recv ? 1 : std::max<int64_t>(1, N);
       w.ecap = std::max<int64_t>(1, G.max_deg);
     } else {
       size_t rem = ws_bytes - w.fixed - partial_max - 2 * kAlign;
       double wr = (double)N * per_recv, we = (double)E * per_edge;
       double frac = (wr + we) > 0 ? wr / (wr + we) : 1.0;
-      w.ncap = std::max<int64_t>(1, (int64_t)(rem * frac / std::max<size_t>(per_recv, 1)));
+      // no per-receiver cost (every state kept by the caller): chunks are bounded by their edges alone
+      w.ncap = per_recv ? std::max<int64_t>(1, (int64_t)(rem * frac / per_recv)) : std::max<int64_t>(1, N);
       w.ncap = std::min<int64_t>(w.ncap, std::max<int64_t>(1, N));
       if (per_edge) {
         w.ecap = (int64_t)((rem - std::min(rem, (size_t)w.ncap * per_recv)) / per_edge);
@@ -361,10 +362,12 @@ int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, const float* S, cons
 }
 
 // Sbar_g = mbar_g A_g^T for every group
-int run_sbar(const Plan& p, const Chunk& c, const WsPlan& w, const float* M, const float* W, float* Sbar,
+// Sbar of receivers [c.r0, c.r0 + c.n) at row 0 of each group block, group blocks
+// s_ncap receivers apart (the chunk slot, or a state kept for every receiver)
+int run_sbar(const Plan& p, const Chunk& c, int64_t s_ncap, const float* M, const float* W, float* Sbar,
              hipStream_t s) {
   for (auto& g : p.groups) {
-    float* Sg = Sbar + (size_t)w.ncap * g.s_off;
+    float* Sg = Sbar + (size_t)s_ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     if (p.vec4)
       LAUNCH(p.k.gemm_sbar_c.at(g.C), cdiv(nrows, 64), 1, 1, s, M, nrows, D, W, (const int*)(p.d_ktab + g.ktab_off),
@@ -750,9 +753,12 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
 
 // Backward; with `state` non-NULL (the retained state of conv_fwd_impl) the weight
 // gradient reads it in one pass instead of recomputing S chunk by chunk.
+// With `adj_state` non-NULL the adjoint state Sbar = mbar A^T of every receiver is
+// computed into it in one pass (and kept for a double backward); the edge kernel
+// then reads each chunk's rows from it.
 int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
-                  const float* W, const float* gout, const float* state, float* gx, float* gevec, float* gphi,
-                  float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
+                  const float* W, const float* gout, const float* state, float* adj_state, float* gx, float* gevec,
+                  float* gphi, float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
   int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
   if (rc) return rc;
   if (!gout && graph->N) return fail(SOBEK_E_INVALID, "gout is NULL");
@@ -760,8 +766,11 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     if (q && !aligned16(q)) return fail(SOBEK_E_ALIGN, "pointer %p is not 16-byte aligned", q);
   const Plan& p = plan->p;
   const sobek_graph_s& G = *graph;
+  if (adj_state && !aligned16(adj_state)) return fail(SOBEK_E_ALIGN, "adj_state is not 16-byte aligned");
   WsPlan w;
-  if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false))) return rc;
+  // the state slot holds S (weight gradient without a kept state) and Sbar (without a kept adjoint state)
+  const bool need_slot = (gW && !state) || (!adj_state && (gx || gevec || gphi));
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false, need_slot ? 1 : 0))) return rc;
   if (gW) { if ((rc = fill_zero(p, gW, (int64_t)p.K * p.n_w, stream))) return rc; }
   if (G.N == 0) return SOBEK_OK;
   const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
@@ -779,10 +788,11 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   float* Sb = S;  // the same slot: S is consumed by the weight-gradient GEMM first
   float* contrib = gx ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = gx || gevec || gphi;
+  const Chunk all{0, (int)G.N, 0, G.E};
   if (gW && state) {
-    const Chunk all{0, (int)G.N, 0, G.E};
     if ((rc = run_ga(p, all, w, ws, state, G.N, gk, gW, true, true, stream))) return rc;
   }
+  if (adj_state && (rc = run_sbar(p, all, G.N, gk, W, adj_state, stream))) return rc;
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
     if (gW && !state) {
@@ -790,12 +800,13 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
       if ((rc = run_ga(p, c, w, ws, S, w.ncap, gk, gW, ci == 0, ci + 1 == w.chunks.size(), stream))) return rc;
     }
     if (edge) {
-      if ((rc = run_sbar(p, c, w, gk, W, Sb, stream))) return rc;
+      if (!adj_state && (rc = run_sbar(p, c, w.ncap, gk, W, Sb, stream))) return rc;
       int r0 = c.r0, n = c.n, e0 = (int)c.e0, flags = 0;
-      long long ncap = w.ncap;
+      long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
+      int sb_r0 = adj_state ? c.r0 : 0;
       LAUNCH_N(p.k.bwd_E, 64 * p.adj_waves, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
-             (const float*)Sb, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
-             (const float*)nullptr, gphi, gevec, contrib, r0, n, ncap, e0, flags);
+             (const float*)(adj_state ? adj_state : Sb), (const float*)nullptr, (const float*)nullptr,
+             (const float*)nullptr, (const float*)nullptr, gphi, gevec, contrib, r0, n, ncap, e0, flags, sb_ncap, sb_r0);
       if (gx && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
     }
   }
@@ -827,22 +838,31 @@ int sobek_conv_fwd_save(sobek_plan plan, sobek_graph graph, const float* x, cons
 int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
                    const float* W, const float* gout, float* gx, float* gevec, float* gphi, float* gW, void* ws,
                    size_t ws_bytes, hipStream_t stream) {
-  return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, nullptr, gx, gevec, gphi, gW, ws, ws_bytes, stream);
+  return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, nullptr, nullptr, gx, gevec, gphi, gW, ws, ws_bytes,
+                       stream);
 }
 
 int sobek_conv_bwd_saved(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
-                         const float* W, const float* gout, const float* state, float* gx, float* gevec, float* gphi,
-                         float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!state && graph && graph->N) return fail(SOBEK_E_INVALID, "state is NULL");
+                         const float* W, const float* gout, const float* state, float* adj_state, float* gx,
+                         float* gevec, float* gphi, float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (state && !aligned16(state)) return fail(SOBEK_E_ALIGN, "state is not 16-byte aligned");
-  return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, state, gx, gevec, gphi, gW, ws, ws_bytes, stream);
+  return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, state, adj_state, gx, gevec, gphi, gW, ws, ws_bytes,
+                       stream);
 }
 
-int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
-                    const float* W, const float* gout, const float* t_gx, const float* t_gevec, const float* t_gphi,
-                    const float* t_gW, float* g_gout, float* g_x, float* g_evec, float* g_phi, float* g_W, void* ws,
-                    size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Double backward; with `adj_state` non-NULL (the adjoint state kept by
+// sobek_conv_bwd_saved for the same gout and W) Sbar is read from it instead of
+// being recomputed chunk by chunk.
+int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                   const float* W, const float* gout, const float* adj_state, const float* t_gx, const float* t_gevec,
+                   const float* t_gphi, const float* t_gW, float* g_gout, float* g_x, float* g_evec, float* g_phi,
+                   float* g_W, void* ws, size_t ws_bytes, hipStream_t stream) {
   int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
+  if (adj_state && !aligned16(adj_state)) return fail(SOBEK_E_ALIGN, "adj_state is not 16-byte aligned");
   if (rc) return rc;
   if (!gout && graph->N) return fail(SOBEK_E_INVALID, "gout is NULL");
   for (const void* q : {(const void*)gout, (const void*)t_gx, (const void*)t_gevec, (const void*)t_gphi,
@@ -895,13 +915,15 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const fl
       if ((rc = run_mix(p, c, w, S, t_gW, ggk, tan ? 1 : 0, stream))) return rc;
     }
     if (edge) {
-      if ((rc = run_sbar(p, c, w, gk, W, Sb, stream))) return rc;
-      if (t_gW && (rc = run_sbar(p, c, w, gk, t_gW, Sb2, stream))) return rc;
+      if (!adj_state && (rc = run_sbar(p, c, w.ncap, gk, W, Sb, stream))) return rc;
+      if (t_gW && (rc = run_sbar(p, c, w.ncap, gk, t_gW, Sb2, stream))) return rc;
       int r0 = c.r0, n = c.n, e0 = (int)c.e0;
-      long long ncap = w.ncap;
+      long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
+      int sb_r0 = adj_state ? c.r0 : 0;
       int fl = flags;
-      LAUNCH_N(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, 64 * p.adj_waves, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
-             (const float*)Sb, (const float*)Sb2, txk, t_gevec, t_gphi, g_phi, g_evec, contrib, r0, n, ncap, e0, fl);
+      LAUNCH_N(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, 64 * p.adj_waves, n, 1, 1, stream, (const int*)G.rowptr,
+               (const int*)G.sender, evec, phi, xk, (const float*)(adj_state ? adj_state : Sb), (const float*)Sb2, txk,
+               t_gevec, t_gphi, g_phi, g_evec, contrib, r0, n, ncap, e0, fl, sb_ncap, sb_r0);
       if (g_x && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
     }
   }
@@ -911,6 +933,26 @@ int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const fl
     if (g_x && (rc = transpose(p, gxk, g_x, G.N, true, 1, stream))) return rc;
   }
   return SOBEK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sobek_conv_dbwd(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                    const float* W, const float* gout, const float* t_gx, const float* t_gevec, const float* t_gphi,
+                    const float* t_gW, float* g_gout, float* g_x, float* g_evec, float* g_phi, float* g_W, void* ws,
+                    size_t ws_bytes, hipStream_t stream) {
+  return conv_dbwd_impl(plan, graph, x, evec, phi, W, gout, nullptr, t_gx, t_gevec, t_gphi, t_gW, g_gout, g_x, g_evec,
+                        g_phi, g_W, ws, ws_bytes, stream);
+}
+
+int sobek_conv_dbwd_saved(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                          const float* W, const float* gout, const float* adj_state, const float* t_gx,
+                          const float* t_gevec, const float* t_gphi, const float* t_gW, float* g_gout, float* g_x,
+                          float* g_evec, float* g_phi, float* g_W, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return conv_dbwd_impl(plan, graph, x, evec, phi, W, gout, adj_state, t_gx, t_gevec, t_gphi, t_gW, g_gout, g_x,
+                        g_evec, g_phi, g_W, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -979,14 +979,17 @@ void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* ind
       sls.push_back({&q, &P.groups[q.group], it.u0, it.lds_off[pi], 2 * q.l_out + 1});
     }
   const int W = P.vec4 ? 4 : 1;  // floats per copy unit
-  auto src_expr = [&](const Sl& x, const std::string& t) {
+  // Sbar: group blocks sb_ncap receivers apart, this receiver at row sb_r0 + il (a
+  // workspace chunk slot, or a state kept for every receiver); Sbar': the chunk slot
+  auto src_expr = [&](const Sl& x, const std::string& t, int pass) {
     std::ostringstream e;
     const int per_q = x.DO * 16 / W;   // copy units per q row
     e << "const int q = " << t << " / " << per_q << ", r = " << t << " % " << per_q << ", m = r / " << 16 / W
       << ", uc = " << x.u0 << " + " << W << " * (r % " << 16 / W << ");\n"
       << indent << "    const bool ok = q < K && uc < " << x.q->c_in << ";\n"
-      << indent << "    const sb_i64 src = ncap * " << x.g->s_off << "LL + ((sb_i64)il * " << x.g->d << " + m) * " << x.g->D
-      << "LL + " << x.q->koff << " + q * " << x.q->c_in << " + uc;\n";
+      << indent << "    const sb_i64 src = " << (pass ? "ncap" : "sb_ncap") << " * " << x.g->s_off << "LL + ((sb_i64)"
+      << (pass ? "il" : "(sb_r0 + il)") << " * " << x.g->d << " + m) * " << x.g->D << "LL + " << x.q->koff << " + q * "
+      << x.q->c_in << " + uc;\n";
     return e.str();
   };
   const char* T = W == 4 ? "sb_f4" : "float";
@@ -1004,7 +1007,7 @@ void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* ind
         o << indent << "  " << T << " v" << reg << " = " << Z << ";\n"
           << indent << "  const int " << t << " = tid + " << j * NT << ";\n"
           << indent << "  if (" << t << " < " << n << ") {\n"
-          << indent << "    " << src_expr(x, t)
+          << indent << "    " << src_expr(x, t, pass)
           << indent << "    if (ok) v" << reg << " = " << (W == 4 ? "*(const sb_f4*)(" : "*(") << src << " + src);\n"
           << indent << "  }\n";
         stores << indent << "  if (" << t << " < " << n << ") *(" << T << "*)(" << dst << " + " << x.off << " + " << W
@@ -1085,7 +1088,7 @@ std::string generate_source(const Plan& P) {
        " const float* __restrict__ Sb, const float* __restrict__ Sb2, const float* __restrict__ xdot,"
        " const float* __restrict__ evdot, const float* __restrict__ phidot, float* __restrict__ gphi,"
        " float* __restrict__ gevec, float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags,"
-       " float* sS, float* sS2, float* sacc, int* sids) {\n"
+       " sb_i64 sb_ncap, int sb_r0, float* sS, float* sS2, float* sacc, int* sids) {\n"
        "  const int il = blockIdx.x;\n"
        "  if (il >= n_recv) return;\n"
        "  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;\n"
@@ -1118,7 +1121,8 @@ std::string generate_source(const Plan& P) {
          " const float* __restrict__ phi, const float* __restrict__ x, const float* __restrict__ Sb,"
          " const float* __restrict__ Sb2, const float* __restrict__ xdot, const float* __restrict__ evdot,"
          " const float* __restrict__ phidot, float* __restrict__ gphi, float* __restrict__ gevec,"
-         " float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags) {\n"
+         " float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags, sb_i64 sb_ncap,"
+         " int sb_r0) {\n"
       << "  __shared__ __attribute__((aligned(16))) float sS[" << LDSF * kv.lds_mult << "];\n"
       << "  __shared__ int sids[ADJ_W * 256];  // per-wave sender ids of the current segment\n";
     if (NSL > 1)
@@ -1127,7 +1131,7 @@ std::string generate_source(const Plan& P) {
       o << "  float* sacc = nullptr;\n";
     o << "  sb_adj_body<" << (kv.db ? "true" : "false") << ", " << kv.fl
       << ">(rowptr, sender, evec, phi, x, Sb, Sb2, xdot, evdot, phidot, gphi, gevec, contrib, r0, n_recv, ncap, e0,"
-         " flags, sS, sS + " << (kv.lds_mult == 2 ? LDSF : 0) << ", sacc, sids);\n}\n";
+         " flags, sb_ncap, sb_r0, sS, sS + " << (kv.lds_mult == 2 ? LDSF : 0) << ", sacc, sids);\n}\n";
   }
   return o.str();
 }

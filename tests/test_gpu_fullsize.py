@@ -81,15 +81,18 @@ def test_full_size(gpu, name):
     say("  gpu fwd (keeping the receiver state, as the benchmark does)")
     state = api.new_state(plan, graph)
     m = N_(api.conv_fwd(plan, graph, *args, budget=BUDGET, state=state))
-    say("  gpu bwd / dbwd, dense m_bar")
-    bd = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout), budget=BUDGET, state=state)]
-    dd = [N_(o) for o in api.conv_dbwd(plan, graph, *args, T(gout), t_gevec=td, budget=BUDGET)]
+    say("  gpu bwd / dbwd, dense m_bar (the adjoint state kept by the backward serves the double backward)")
+    adj = api.new_state(plan, graph)
+    bd = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout), budget=BUDGET, state=state, adj_state=adj)]
+    dd = [N_(o) for o in api.conv_dbwd(plan, graph, *args, T(gout), t_gevec=td, budget=BUDGET, adj_state=adj)]
     say("  gpu bwd / dbwd, m_bar restricted to the sampled receivers")
-    bm = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout_m), budget=BUDGET, state=state)]
+    bm = [N_(o) for o in api.conv_bwd(plan, graph, *args, T(gout_m), budget=BUDGET, state=state, adj_state=adj)]
     bm_recompute = N_(api.conv_bwd(plan, graph, *args, T(gout_m), need=(False, False, False, True),
                                    budget=BUDGET)[3])
-    dm = [N_(o) for o in api.conv_dbwd(plan, graph, *args, T(gout_m), t_gevec=td, budget=BUDGET)]
-    del args, td, graph, state
+    dm = [N_(o) for o in api.conv_dbwd(plan, graph, *args, T(gout_m), t_gevec=td, budget=BUDGET, adj_state=adj)]
+    dm_recompute = N_(api.conv_dbwd(plan, graph, *args, T(gout_m), t_gevec=td, budget=BUDGET,
+                                    need=(False, True, False, False, False))[1])
+    del args, td, graph, state, adj
     torch.cuda.empty_cache()
 
     # ---- oracle on the sampled receivers' in-edges ---------------------------------------------
@@ -116,7 +119,8 @@ def test_full_size(gpu, name):
     _check("bwd A_bar (restricted m_bar, retained S)", bm[3], b_ref["gW"], BWD_TOL)
     _check("bwd A_bar (restricted m_bar, recomputed S)", bm_recompute, b_ref["gW"], BWD_TOL)
     _check("bwd evec_bar (restricted m_bar)", bm[1][A], b_ref["gevec"], BWD_TOL)
-    _check("dbwd g_x (restricted m_bar)", dm[1], d_ref["g_x"], BWD_TOL)
+    _check("dbwd g_x (restricted m_bar, kept Sbar)", dm[1], d_ref["g_x"], BWD_TOL)
+    _check("dbwd g_x (restricted m_bar, recomputed Sbar)", dm_recompute, d_ref["g_x"], BWD_TOL)
     _check("dbwd g_W (restricted m_bar)", dm[4], d_ref["g_W"], BWD_TOL)
     _check("dbwd g_phi (restricted m_bar)", dm[3][A], d_ref["g_phi"], BWD_TOL)
     for nm, t in (("evec_bar", bm[1]), ("phi_bar", bm[2]), ("g_evec", dm[2]), ("g_phi", dm[3])):

@@ -204,6 +204,27 @@ def test_retained_state(gpu, sig, N, E, seed):
             err = max_rel(_n(o), ref[name])
             print(f"bwd (retained S, budget {budget}) {sig} {name}: max rel err {err:.2e}")
             assert err <= BWD_TOL, name
+    # the adjoint state kept by the backward serves the double backward (all four cotangents and edge-only)
+    adj = api.new_state(plan, graph)
+    adj.fill_(float("nan"))
+    outs = api.conv_bwd(plan, graph, *args, gout, state=state, adj_state=adj)
+    for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
+        assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
+    c = case["cot"]
+    for keep in (("x", "evec", "phi", "W"), ("evec",)):
+        t = {k: (v if k in keep else None) for k, v in c.items()}
+        for budget in (0, 1 << 20):
+            outs = api.conv_dbwd(plan, graph, *args, gout, _t(t["x"]), _t(t["evec"]), _t(t["phi"]), _t(t["W"]),
+                                 adj_state=adj, budget=budget)
+            r = oc.dbwd(*oracle_args(case, prob), case["gout"], t_gx=t["x"], t_gevec=t["evec"], t_gphi=t["phi"],
+                        t_gW=t["W"])
+            for name, o in zip(("g_gout", "g_x", "g_evec", "g_phi", "g_W"), outs):
+                if np.abs(r[name]).max() == 0:
+                    assert np.abs(_n(o)).max() == 0, name
+                    continue
+                err = max_rel(_n(o), r[name])
+                print(f"dbwd (kept Sbar, {keep}, budget {budget}) {sig} {name}: max rel err {err:.2e}")
+                assert err <= BWD_TOL, name
     # W does not enter S: a state kept with other weights serves as well
     m2 = api.conv_fwd(plan, graph, args[0], args[1], args[2], 2 * args[3], state=state)
     torch.cuda.synchronize()
