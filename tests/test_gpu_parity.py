@@ -251,3 +251,28 @@ def test_autograd_retained_state(gpu):
     r = oc.dbwd(*oracle_args(case, prob), case["gout"], t_gevec=2 * _n(gev).astype(np.float64))
     for name, o in zip(("g_x", "g_evec", "g_phi", "g_W"), d):
         assert max_rel(_n(o), r[name]) <= BWD_TOL, name
+
+
+def test_kept_states_chunk_by_edges_only(gpu):
+    """With S and Sbar both kept the backward needs no per-receiver workspace: its chunks are bounded by the
+    per-edge x-gradient contributions alone (a regression test for chunks of one receiver each)."""
+    from paper_2607_18074_amd import _lib
+    case = make_case("small", 300, 4000, 15)
+    api, plan, graph, prob = setup(case)
+    g = case["graph"]
+    args = (_t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]))
+    state, adj = api.new_state(plan, graph), api.new_state(plan, graph)
+    api.conv_fwd(plan, graph, *args, state=state)
+    budget = 2 << 20      # contributions of 4000 edges x 288 floats = 4.6 MB: a few chunks
+    ws = graph.workspace(plan, "bwd", budget)
+    _lib.profile_reset()
+    _lib.profile_enable(True)
+    outs = api.conv_bwd(plan, graph, *args, _t(case["gout"]), state=state, adj_state=adj, ws=ws)
+    prof = _lib.profile_read()
+    _lib.profile_enable(False)
+    n_edge = prof["sobek_bwd_E"][0]
+    print("bwd_E launches", n_edge, "workspace", ws.numel())
+    assert 2 <= n_edge <= 10
+    ref = oc.bwd(*oracle_args(case, prob), case["gout"])
+    for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
+        assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
