@@ -176,6 +176,69 @@ def sweep(budget_gib, names):
             f"{r['tflops']:.1f} | {100 * r['frac_fp32']:.1f} | {r['alg_gbs']:.0f} | {r['peak_mem_gb']:.2f} |")
 
 
+def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd")):
+    """The paper's scaling regimes: degree scaling (2,048 nodes, mean degree 4..1,023) and graph-count
+    scaling (B copies of a 128-node degree-32 graph, B = 2..511) on its representative profiles, every
+    pass timed with the paper's protocol; one JSON line per point, a table at the end."""
+    import torch
+
+    from paper_2607_18074_amd import api
+    from paper_2607_18074_amd import workloads as wl
+    torch.cuda.set_device(0)
+    budget = int(budget_gib * (1 << 30))
+    rows = []
+    for prof in profiles:
+        spec, lmax = wl.profile_irreps(prof)
+        plan = api.Plan(spec, lmax, spec, wl.REGIME_K)
+        W = torch.from_numpy(wl.weights(plan.K, plan.weight_std(), 7)).cuda()
+        points = [("degree", d) for d in wl.DEGREE_GRID if "degree" in kinds] + \
+                 [("count", b) for b in wl.GRAPH_COUNT_GRID if "count" in kinds]
+        for kind, v in points:
+            g = wl.degree_graph(v)[0] if kind == "degree" else wl.graph_count_graph(v)
+            T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+            graph = api.Graph(T(g.rowptr), T(g.sender))
+            xt, ev, ph = T(wl.node_features(g.N, plan.dim_in, 7)), T(g.evec), T(g.phi)
+            gt = T(wl.out_cotangent(g.N, plan.dim_out, 7))
+            state = api.new_state(plan, graph) if retain else None
+            adj = api.new_state(plan, graph) if retain else None
+            fm = flop_model(plan, g.N, g.E)
+            rdot = None
+            for pname in passes:
+                graph._ws.clear()
+                torch.cuda.empty_cache()
+                ws = graph.workspace(plan, pname, budget)
+                if pname == "fwd":
+                    fn = lambda: api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)  # noqa: E731
+                elif pname == "bwd":
+                    if retain:
+                        api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)
+                    fn = lambda: api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,  # noqa: E731
+                                              adj_state=adj)
+                else:
+                    rdot = (2.0 * api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,
+                                               adj_state=adj)[1]).contiguous()
+                    fn = lambda: api.conv_dbwd(plan, graph, xt, ev, ph, W, gt, t_gevec=rdot, ws=ws,  # noqa: E731
+                                               adj_state=adj)
+                torch.cuda.synchronize()
+                torch.cuda.reset_peak_memory_stats()
+                ms, n = time_pass(fn, torch)
+                tf = fm["passes"][pname] / (ms * 1e-3) / 1e12
+                row = dict(profile=prof, regime=kind, value=v, N=g.N, E=g.E, mean_degree=g.E / g.N, pass_=pname,
+                           ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3), tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS,
+                           peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9, workspace_gb=ws.numel() / 1e9)
+                rows.append(row)
+                print(json.dumps({k.rstrip("_"): x for k, x in row.items()}), flush=True)
+                del ws, fn
+            del graph, xt, ev, ph, gt, state, adj, rdot
+            torch.cuda.empty_cache()
+        del plan, W
+    log("| profile | regime | N | E | pass | edges/s | % fp32 | peak GB |")
+    log("|---|---|---:|---:|---|---:|---:|---:|")
+    for r in rows:
+        log(f"| {r['profile']} | {r['regime']} {r['value']} | {r['N']:,} | {r['E']:,} | {r['pass_']} | "
+            f"{r['edges_per_s'] / 1e6:,.2f} M | {100 * r['frac_fp32']:.1f} | {r['peak_mem_gb']:.2f} |")
+
+
 PAPER_CONTEXT = {
     "hardware": "NVIDIA RTX 5090 (32 GiB), fp32 throughout, eager, 128 MiB scratch budget (Section 5.1)",
     "workloads": "fixed 128-node degree-32 graph repeated B times, uvw profiles with K = 16 (Section 5.1, Table 3)",
@@ -271,6 +334,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", default="", help="comma-separated workloads (or 'all'): time every pass of each "
                     "with the paper's protocol instead of the step benchmark, one JSON line per pass")
+    ap.add_argument("--regimes", default="", help="'degree', 'count' or 'all': the paper's scaling regimes on its "
+                    "profiles (--profiles), one JSON line per point and pass")
+    ap.add_argument("--profiles", default="128/64,128/64/64,128/64/64/64")
+    ap.add_argument("--retain", action="store_true", help="regimes: keep S and Sbar across passes (default: the "
+                    "paper's setting, recompute within the workspace budget)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
                     help="only run a plain device copy of this many MiB (traffic-counter calibration)")
     args = ap.parse_args()
@@ -289,6 +357,10 @@ def main():
               "would shard); rerun with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    if args.regimes:
+        kinds = ("degree", "count") if args.regimes == "all" else tuple(args.regimes.split(","))
+        regimes(kinds, args.profiles.split(","), args.budget, args.retain)
+        return
     if args.sweep:
         names = ["tiny", "small", "medium", "wide", "stress"] if args.sweep == "all" else args.sweep.split(",")
         sweep(args.budget, names)

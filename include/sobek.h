@@ -137,9 +137,10 @@ int sobek_graph_destroy(sobek_graph graph);
 /* Number of nodes and edges of a prepared graph (either pointer may be NULL). */
 int sobek_graph_info(sobek_graph graph, int64_t *N, int64_t *E);
 
-/* Workspace for one pass: the smallest size that allows receiver chunks of at
- * least one receiver, grown up to `budget` bytes (budget 0 = the default of
- * 1 GiB).  The bytes never scale with E * n_weights or E * dim_out: receiver
+/* Workspace for one pass: the bytes of a single chunk over every receiver when
+ * that fits in `budget` (budget 0 = the default of 1 GiB), else `budget` itself
+ * (or the minimum for chunks of one receiver, if larger), so that a call given
+ * exactly the reported bytes chunks as finely as the budget requires and no finer.  The bytes never scale with E * n_weights or E * dim_out: receiver
  * state is bounded by the chunk size, per-edge x-gradient contributions by the
  * chunk's edges.  conv_* derive their chunking from ws_bytes. */
 int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t budget, size_t *bytes);

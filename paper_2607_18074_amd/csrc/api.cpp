@@ -177,7 +177,8 @@ struct Chunk {
 struct WsPlan {
   // byte offsets
   size_t off_x = 0, off_gout = 0, off_tgx = 0, off_out = 0, off_gx = 0, off_cursor = 0, off_P = 0, off_state = 0,
-         off_contrib = 0;
+         off_contrib = 0, off_K = 0;
+  size_t kfloats = 0;  // split-K partials of the state GEMM (forward and double backward)
   size_t fixed = 0;
   int nstate = 0;
   int64_t ncap = 0, ecap = 0;
@@ -203,6 +204,34 @@ size_t partial_floats(const Plan& p, int64_t ncap) {
   size_t m = 0;
   for (auto& g : p.groups) m += (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C;
   return m;
+}
+
+// Split-K of the state GEMM m_g = S_g A_g: a chunk of few receivers gives few row
+// tiles against a long reduction (K times the summed input multiplicities), so the
+// reduction is split until about kSaTarget blocks run; partial tiles are summed in
+// split order by sobek_sa_reduce.  The partials of one group at a time live in a
+// region of at most kSaSplitCap floats.
+constexpr int kSaTarget = 512, kSaMaxSplit = 16;
+constexpr size_t kSaSplitCap = (size_t)4 << 20;
+
+size_t sa_split_floats(const Plan& p, int pass, int64_t ncap) {
+  if (pass == SOBEK_PASS_BWD || !p.vec4) return 0;
+  size_t m = 0;
+  for (auto& g : p.groups) m = std::max(m, (size_t)g.d * g.C);
+  return std::min(kSaSplitCap, (size_t)kSaMaxSplit * (size_t)std::max<int64_t>(1, ncap) * m);
+}
+
+// splits of one state-GEMM launch over nrows rows (1 = no split); kper = reduction per split
+int sa_nsplit(const sobek::Group& g, int64_t nrows, size_t kfloats, int& kper) {
+  const int bn = gemm_bn(g.C);
+  const int64_t blocks = (int64_t)cdiv(nrows, 128) * cdiv(g.C, bn);
+  kper = (int)g.D;
+  if (blocks * 2 > kSaTarget || nrows <= 0) return 1;
+  int64_t ns = std::min<int64_t>({(kSaTarget + blocks - 1) / blocks, (int64_t)kSaMaxSplit,
+                                  (int64_t)(kfloats / ((size_t)nrows * g.C)), (int64_t)g.D / (4 * 32)});
+  if (ns < 2) return 1;
+  kper = (int)(cdiv(cdiv(g.D, ns), 32) * 32);
+  return (int)cdiv(g.D, kper);
 }
 
 // fixed part + per-receiver + per-edge bytes of a pass
@@ -231,6 +260,8 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, int nstate, WsP
 size_t layout_total(const Plan& p, WsPlan& w, int pass) {
   size_t o = w.fixed;
   if (pass != SOBEK_PASS_FWD) o = align_up(o + partial_floats(p, w.ncap) * 4);
+  w.off_K = o;  // w.kfloats is set by the planner
+  o = align_up(o + w.kfloats * 4);
   w.off_state = o;
   o = align_up(o + (size_t)w.nstate * w.ncap * p.srow * 4);
   w.off_contrib = o;
@@ -245,36 +276,119 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
   size_t per_recv, per_edge;
   pass_costs(p, G, pass, nstate, w, per_recv, per_edge);
   const int64_t N = G.N, E = G.E;
+  // The state-GEMM split-K region only adds blocks: give it what the budget leaves
+  // once the chunk capacities are fixed, down to nothing (no split).
+  auto fit_split = [&]() -> size_t {
+    w.kfloats = sa_split_floats(p, pass, w.ncap);
+    size_t t = layout_total(p, w, pass);
+    if (t <= ws_bytes || !w.kfloats) return t;
+    w.kfloats = 0;
+    const size_t bare = layout_total(p, w, pass);
+    if (bare >= ws_bytes) return bare;
+    w.kfloats = std::min(sa_split_floats(p, pass, w.ncap), (ws_bytes - bare) / kAlign * kAlign / 4);
+    return layout_total(p, w, pass);
+  };
   // try a single chunk, else split the remaining bytes between state and contributions
   w.ncap = std::max<int64_t>(1, N);
   w.ecap = std::max<int64_t>(G.max_deg, E);
+  w.kfloats = 0;
   size_t need = layout_total(p, w, pass);
-  if (need > ws_bytes) {
-    size_t partial_max = align_up(partial_floats(p, std::max<int64_t>(1, N)) * 4) + 2 * kAlign;
-    if (ws_bytes <= w.fixed + partial_max) {
-      w.ncap = per_recv ? 1 : std::max<int64_t>(1, N);
-      w.ecap = std::max<int64_t>(1, G.max_deg);
-    } else {
-      size_t rem = ws_bytes - w.fixed - partial_max - 2 * kAlign;
-      double wr = (double)N * per_recv, we = (double)E * per_edge;
-      double frac = (wr + we) > 0 ? wr / (wr + we) : 1.0;
-      // no per-receiver cost (every state kept by the caller): chunks are bounded by their edges alone
-      w.ncap = per_recv ? std::max<int64_t>(1, (int64_t)(rem * frac / per_recv)) : std::max<int64_t>(1, N);
-      w.ncap = std::min<int64_t>(w.ncap, std::max<int64_t>(1, N));
-      if (per_edge) {
-        w.ecap = (int64_t)((rem - std::min(rem, (size_t)w.ncap * per_recv)) / per_edge);
-        if (w.ecap < G.max_deg) {
-          w.ecap = std::max<int64_t>(1, G.max_deg);
-          size_t left = rem > (size_t)w.ecap * per_edge ? rem - (size_t)w.ecap * per_edge : 0;
-          w.ncap = std::max<int64_t>(1, std::min<int64_t>(w.ncap, (int64_t)(left / std::max<size_t>(per_recv, 1))));
-        }
+  if (need <= ws_bytes) {
+    need = fit_split();
+    w.total = need;
+  } else {
+    // GEMM partials (weight-gradient splits, state-GEMM split-K) of chunks of nc receivers
+    auto partial_bytes = [&](int64_t nc) -> size_t {
+      nc = std::max<int64_t>(1, nc);
+      return (pass != SOBEK_PASS_FWD ? align_up(partial_floats(p, nc) * 4) + kAlign : 0) +
+             align_up(sa_split_floats(p, pass, nc) * 4) + kAlign;
+    };
+    auto total_at = [&](int64_t nc, int64_t ec, size_t kf) {
+      w.ncap = nc;
+      w.ecap = ec;
+      w.kfloats = kf;
+      return layout_total(p, w, pass);
+    };
+    const int64_t emin = std::max<int64_t>(1, G.max_deg), eall = std::max<int64_t>(G.max_deg, E);
+    const int64_t ec0 = per_edge ? emin : eall;
+    // A capacity nc of receivers leaves, after the fixed part, the partials, the state of nc
+    // receivers and the split-K region (what fits of it), every byte to the per-edge
+    // contributions.  Among candidate capacities keep the one with the fewest chunks
+    // (about max(N / nc, E / ec)), ties to the larger nc.
+    // The split-K region is reserved whole (strict) unless no capacity fits with it.
+    struct Cand { int64_t nc = 0, ec = 0; size_t kf = 0, need = 0, score = 0; };
+    bool strict = true;
+    auto eval = [&](int64_t nc) {
+      Cand c;
+      c.nc = nc;
+      if (strict) {
+        c.kf = sa_split_floats(p, pass, nc);
+        c.need = total_at(nc, ec0, c.kf);
+        if (c.need > ws_bytes) return c;  // infeasible: score 0
       } else {
-        w.ecap = std::max<int64_t>(1, G.max_deg);
+        if (total_at(nc, ec0, 0) > ws_bytes) return c;
+        w.ncap = nc;
+        w.ecap = ec0;
+        c.need = fit_split();
+        c.kf = w.kfloats;
+      }
+      c.ec = ec0;
+      if (per_edge) {
+        int64_t ec = std::min<int64_t>(eall, ec0 + (int64_t)((ws_bytes - c.need) / per_edge));
+        while (ec > ec0 && total_at(nc, ec, c.kf) > ws_bytes) ec = std::max<int64_t>(ec0, ec - 64);
+        c.ec = ec;
+        c.need = total_at(nc, ec, c.kf);
+      }
+      c.score = std::max<size_t>(cdiv(N, nc), per_edge ? cdiv(std::max<int64_t>(1, E), c.ec) : 1);
+      return c;
+    };
+    std::vector<int64_t> cands;
+    for (int64_t nc = std::max<int64_t>(1, N); nc >= 1; nc /= 2) cands.push_back(nc);
+    if (per_recv) {
+      // the bytes left after the fixed part and the partials, split between receiver state and
+      // contributions in proportion to their totals (a few rounds: the partials shrink with nc)
+      const double wr = (double)N * per_recv, we = (double)E * per_edge;
+      int64_t nc = std::max<int64_t>(1, N);
+      for (int iter = 0; iter < 4; ++iter) {
+        const size_t aux = partial_bytes(nc);
+        if (ws_bytes <= w.fixed + aux) break;
+        const double rem = (double)(ws_bytes - w.fixed - aux);
+        nc = std::min<int64_t>(std::max<int64_t>(1, (int64_t)(rem * (wr / (wr + we)) / per_recv)), N);
+        cands.push_back(nc);
       }
     }
-    need = layout_total(p, w, pass);
+    Cand best;
+    for (int pass_strict = 1; pass_strict >= 0 && !best.score; --pass_strict) {
+      strict = pass_strict;
+      for (int64_t nc : cands) {
+        Cand c = eval(nc);
+        if (c.score && (!best.score || c.score < best.score || (c.score == best.score && c.nc > best.nc))) best = c;
+      }
+    }
+    if (best.score && best.nc < std::max<int64_t>(1, N)) {
+      // refine: the largest capacity with the same chunk count (bisection above the best)
+      int64_t lo = best.nc, hi = std::min<int64_t>(N, 2 * best.nc);
+      while (hi - lo > 1) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        Cand c = eval(mid);
+        if (c.score && c.score <= best.score) {
+          best = c;
+          lo = mid;
+        } else {
+          hi = mid;
+        }
+      }
+    }
+    if (best.score) {
+      total_at(best.nc, best.ec, best.kf);
+      need = best.need;
+    } else {
+      need = total_at(1, ec0, 0);  // not even one receiver fits: report the minimum
+    }
+    // A chunked pass plans from ws_bytes alone: report the whole budget so that a call
+    // given exactly the reported bytes reproduces these chunk capacities.
+    w.total = std::max(need, ws_bytes);
   }
-  w.total = need;
   if (sizing_only) return SOBEK_OK;
   if (need > ws_bytes)
     return fail(SOBEK_E_WORKSPACE, "workspace of %zu bytes is below the minimum %zu for this pass", ws_bytes, need);
@@ -345,18 +459,25 @@ int run_state(const Plan& p, const sobek_graph_s& G, const Chunk& c, const WsPla
 }
 
 // out(i, m_o, w) (+)= S_g A_g for every group
-int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, const float* S, const float* W, float* out, int acc,
-            hipStream_t s) {
+int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float* S, const float* W, float* out,
+            int acc, hipStream_t s) {
+  float* K = (float*)((char*)ws + w.off_K);
   for (auto& g : p.groups) {
     const float* Sg = S + (size_t)w.ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     int bn = gemm_bn(g.C);
-    if (p.vec4)
-      LAUNCH(p.k.gemm_sa_v[bn_index(bn)], cdiv(nrows, 128), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
-             (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
-    else
+    if (p.vec4) {
+      int kper = D;
+      const int ns = sa_nsplit(g, nrows, w.kfloats, kper);
+      LAUNCH(p.k.gemm_sa_v[bn_index(bn)], cdiv(nrows, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, W,
+             (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc, K, kper);
+      if (ns > 1)
+        LAUNCH(p.k.sa_reduce, cdiv((int64_t)nrows * (Cg / 4), 256), 1, 1, s, (const float*)K, ns, nrows, Cg, out, dg,
+               off, CX, r0, acc);
+    } else {
       LAUNCH(p.k.gemm_sa[bn_index(bn)], cdiv(nrows, 64), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
              (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
+    }
   }
   return SOBEK_OK;
 }
@@ -370,8 +491,14 @@ int run_sbar(const Plan& p, const Chunk& c, int64_t s_ncap, const float* M, cons
     float* Sg = Sbar + (size_t)s_ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     if (p.vec4)
-      LAUNCH(p.k.gemm_sbar_c.at(g.C), cdiv(nrows, 64), 1, 1, s, M, nrows, D, W, (const int*)(p.d_ktab + g.ktab_off),
-             Sg, dg, off, CX, r0);
+    {
+      // spread the 64-wide column tiles over blockIdx.y until about kSaTarget blocks run,
+      // keeping at least four tiles per block
+      const int rows = cdiv(nrows, 64), ntile = cdiv(D, 64);
+      const int gy = std::max(1, std::min((int)cdiv(kSaTarget, rows), ntile / 4));
+      LAUNCH(p.k.gemm_sbar_c.at(g.C), rows, gy, 1, s, M, nrows, D, W, (const int*)(p.d_ktab + g.ktab_off), Sg, dg,
+             off, CX, r0);
+    }
     else
       LAUNCH(p.k.gemm_sbar[2], cdiv(nrows, 64), cdiv(D, 64), 1, s, M, nrows, D, W,
              (const int*)(p.d_ktab + g.ktab_off), Sg, dg, Cg, off, CX, r0);
@@ -470,7 +597,7 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
       (rc = get(p.k.dbwd_E, "sobek_dbwd_E")) || (rc = get(p.k.dbwd_E_r, "sobek_dbwd_E_r")) ||
       (rc = get(p.k.ga_reduce, "sobek_ga_reduce")) || (rc = get(p.k.sender_reduce, "sobek_sender_reduce")) ||
       (rc = get(p.k.transpose, "sobek_transpose")) || (rc = get(p.k.fill_cols, "sobek_fill_cols")) ||
-      (rc = get(p.k.zero, "sobek_zero")))
+      (rc = get(p.k.zero, "sobek_zero")) || (rc = get(p.k.sa_reduce, "sobek_sa_reduce")))
     return rc;
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
@@ -744,7 +871,7 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   float* S = state ? state : state_ptr(w, ws, p, 0);  // a retained state is one chunk of all N receivers
   for (auto& c : w.chunks) {
     if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
-    if ((rc = run_mix(p, c, w, S, W, ok, 0, stream))) return rc;
+    if ((rc = run_mix(p, c, w, ws, S, W, ok, 0, stream))) return rc;
   }
   if ((rc = zero_dead_out(p, ok, G.N, stream))) return rc;
   if (mulir && (rc = transpose(p, ok, out, G.N, false, 1, stream))) return rc;
@@ -906,13 +1033,13 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
     const Chunk& c = w.chunks[ci];
     if (tan && (g_gout || g_W)) {
       if ((rc = run_state(p, G, c, w, dS, true, xk, evec, phi, txk, t_gevec, t_gphi, flags & 7, stream))) return rc;
-      if (g_gout && (rc = run_mix(p, c, w, dS, W, ggk, 0, stream))) return rc;
+      if (g_gout && (rc = run_mix(p, c, w, ws, dS, W, ggk, 0, stream))) return rc;
       if (g_W && (rc = run_ga(p, c, w, ws, dS, w.ncap, gk, g_W, ci == 0, ci + 1 == w.chunks.size(), stream)))
         return rc;
     }
     if (t_gW && g_gout) {  // S reuses the slot once dS has been consumed
       if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
-      if ((rc = run_mix(p, c, w, S, t_gW, ggk, tan ? 1 : 0, stream))) return rc;
+      if ((rc = run_mix(p, c, w, ws, S, t_gW, ggk, tan ? 1 : 0, stream))) return rc;
     }
     if (edge) {
       if (!adj_state && (rc = run_sbar(p, c, w.ncap, gk, W, Sb, stream))) return rc;

@@ -210,12 +210,14 @@ SB_DEV sb_v4 sb_ld4(const float* p) { return *(const sb_v4*)p; }
 template <int BN>
 SB_DEV void sb_gemm_sa_v(const float* __restrict__ S, int nrows, int D, const float* __restrict__ W,
                          const int* __restrict__ ktab, float* __restrict__ out, int dg, int Cg, int off, int CX,
-                         int r0, int accumulate) {
+                         int r0, int accumulate, float* __restrict__ P, int kper) {
   __shared__ float sA[SB_VK][SB_VM + 4];
   __shared__ float sB[SB_VK][BN + 4];
   constexpr int NB = (SB_VK * BN / 4 + 255) / 256;  // float4 loads of B per thread
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int rb = blockIdx.x * SB_VM, cb = blockIdx.y * BN;
+  // split z of a split-K launch takes k in [kbeg, kend) (kper a multiple of SB_VK)
+  const int kbeg = blockIdx.z * kper, kend = min(D, kbeg + kper);
   sb_f4 acc[2][BN / 16];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -227,14 +229,14 @@ SB_DEV void sb_gemm_sa_v(const float* __restrict__ S, int nrows, int D, const fl
     for (int i = 0; i < 4; ++i) {
       const int row = (tid >> 3) + 32 * i, k = k0 + 4 * (tid & 7);
       const int gr = rb + row;
-      ra[i] = (gr < nrows && k < D) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+      ra[i] = (gr < nrows && k < kend) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int idx = tid + 256 * i;
       const int kk = idx / (BN / 4), c = 4 * (idx % (BN / 4));
       const int gk = k0 + kk;
-      rbv[i] = (idx < SB_VK * BN / 4 && gk < D && cb + c < Cg) ? sb_ld4(W + (sb_i64)ktab[gk] + cb + c)
+      rbv[i] = (idx < SB_VK * BN / 4 && gk < kend && cb + c < Cg) ? sb_ld4(W + (sb_i64)ktab[gk] + cb + c)
                                                                 : (sb_v4){0.f, 0.f, 0.f, 0.f};
     }
   };
@@ -251,11 +253,11 @@ SB_DEV void sb_gemm_sa_v(const float* __restrict__ S, int nrows, int D, const fl
       if (idx < SB_VK * BN / 4) *(sb_v4*)&sB[idx / (BN / 4)][4 * (idx % (BN / 4))] = rbv[i];
     }
   };
-  load(0);
+  load(kbeg);
   store();
   __syncthreads();
-  for (int k0 = 0; k0 < D; k0 += SB_VK) {
-    const bool more = k0 + SB_VK < D;
+  for (int k0 = kbeg; k0 < kend; k0 += SB_VK) {
+    const bool more = k0 + SB_VK < kend;
     if (more) load(k0 + SB_VK);
 #pragma unroll
     for (int kk = 0; kk < SB_VK; kk += 4) {
@@ -283,10 +285,30 @@ SB_DEV void sb_gemm_sa_v(const float* __restrict__ S, int nrows, int D, const fl
         const int row = rb + 32 * wave + 16 * i + 4 * (lane >> 4) + r;
         const int col = cb + 16 * t + (lane & 15);
         if (row < nrows && col < Cg) {
-          float* o = out + sb_row_addr(row, dg, Cg, off, CX, r0) + col;
-          *o = accumulate ? (*o + acc[i][t][r]) : acc[i][t][r];
+          if (gridDim.z > 1) {  // partial of this split: P[z][row][col], summed by sobek_sa_reduce
+            P[((sb_i64)blockIdx.z * nrows + row) * Cg + col] = acc[i][t][r];
+          } else {
+            float* o = out + sb_row_addr(row, dg, Cg, off, CX, r0) + col;
+            *o = accumulate ? (*o + acc[i][t][r]) : acc[i][t][r];
+          }
         }
       }
+}
+
+// out rows (r0 + r / dg, r % dg) (+)= sum_{z < nsplit} P[z][r][:], splits added in order
+extern "C" __global__ __launch_bounds__(256) void sobek_sa_reduce(const float* __restrict__ P, int nsplit, int nrows,
+                                                                  int Cg, float* __restrict__ out, int dg, int off,
+                                                                  int CX, int r0, int accumulate) {
+  const int nq = Cg / 4;
+  const sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (sb_i64)nrows * nq) return;
+  const int row = (int)(t / nq), c = 4 * (int)(t % nq);
+  const sb_i64 stride = (sb_i64)nrows * Cg;
+  const float* src = P + (sb_i64)row * Cg + c;
+  sb_v4 v = sb_ld4(src);
+  for (int z = 1; z < nsplit; ++z) v += sb_ld4(src + z * stride);
+  sb_v4* o = (sb_v4*)(out + sb_row_addr(row, dg, Cg, off, CX, r0) + c);
+  *o = accumulate ? (*o + v) : v;
 }
 
 // Sbar[r, k] = sum_w mbar(r, w) A_g[k, w]; 128 rows x 64 k-columns per block, reduction over w
@@ -420,15 +442,17 @@ SB_DEV void sb_gemm_sbar_s(const float* __restrict__ M, int nrows, int D, const 
       }
     }
   };
-  loadB(0);
+  // blockIdx.y takes a contiguous range of 64-wide column tiles
+  const int ntile = (D + 63) / 64, tpb = (ntile + gridDim.y - 1) / gridDim.y;
+  const int sl0 = blockIdx.y * tpb * NS, nsl = min(ntile, (int)(blockIdx.y + 1) * tpb) * NS;
+  loadB(sl0);
   storeB(0);
   __syncthreads();
-  const int nsl = (D + 63) / 64 * NS;
   const int row = rb + 16 * wave + j;
   float* out = Sbar + (sb_i64)row * D;
   sb_f4 acc[4];
-  for (int sl = 0; sl < nsl; ++sl) {
-    const int buf = sl & 1, w0 = (sl % NS) * WC;
+  for (int sl = sl0; sl < nsl; ++sl) {
+    const int buf = (sl - sl0) & 1, w0 = (sl % NS) * WC;
     if (sl + 1 < nsl) loadB(sl + 1);
     if (w0 == 0) {
 #pragma unroll
@@ -542,8 +566,8 @@ SB_DEV void sb_gemm_ga_v(const float* __restrict__ S, int nrows, int D, const fl
 #define SB_GEMM_V_ENTRY(BN)                                                                          \
   extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sa_v##BN(                            \
       const float* S, int nrows, int D, const float* W, const int* ktab, float* out, int dg,       \
-      int Cg, int off, int CX, int r0, int accumulate) {                                           \
-    sb_gemm_sa_v<BN>(S, nrows, D, W, ktab, out, dg, Cg, off, CX, r0, accumulate);                  \
+      int Cg, int off, int CX, int r0, int accumulate, float* P, int kper) {                       \
+    sb_gemm_sa_v<BN>(S, nrows, D, W, ktab, out, dg, Cg, off, CX, r0, accumulate, P, kper);         \
   }                                                                                                \
   extern "C" __global__ __launch_bounds__(256) void sobek_gemm_ga_v##BN(                            \
       const float* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \

@@ -75,7 +75,7 @@ struct Kernels {
   hipFunction_t gemm_sa_v[3] = {}, gemm_ga_v[3] = {}, gemm_sbar_v = nullptr;  // 16-byte aligned operands
   std::map<int, hipFunction_t> gemm_sbar_c;  // streaming adjoint-state GEMM per output multiplicity
   hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
-                zero = nullptr;
+                zero = nullptr, sa_reduce = nullptr;
 };
 
 struct Plan {

@@ -131,6 +131,65 @@ def cube_graph(N, degree, r_c, seed, K):
     return Graph(N, rowptr, send, evec.astype(np.float32), bessel_basis(d, K, r_c).astype(np.float32))
 
 
+# ---------------------------------------------------------------------------
+# Scaling regimes (the paper's degree and graph-count grids, its Appendix on
+# benchmark regimes).  The paper's position set is unpublished: uniform points
+# in a cube stand in for it, so the realized degree spread differs from its
+# table while the node counts, mean degrees and graph counts match.
+# ---------------------------------------------------------------------------
+
+REGIME_PROFILES = {   # multiplicities per l = 0, 1, ... (equal input and output, parity alternating), K = 16
+    "128/64": (128, 64),
+    "128/64/64": (128, 64, 64),
+    "128/64/64/64": (128, 64, 64, 64),
+}
+DEGREE_GRID = (4, 6, 8, 12, 16, 24, 32, 48, 64, 96, 128, 192, 256, 384, 512, 768, 1023)
+GRAPH_COUNT_GRID = (2, 3, 5, 8, 13, 23, 38, 64, 108, 181, 304, 511)
+REGIME_K = 16
+
+
+def profile_irreps(name):
+    """'128/64/64' -> ('128x0e+64x1o+64x2e', lmax 2): one irrep per l, parity (-1)^l, SH up to the same l."""
+    muls = REGIME_PROFILES[name]
+    spec = "+".join(f"{m}x{l}{'e' if l % 2 == 0 else 'o'}" for l, m in enumerate(muls))
+    return spec, len(muls) - 1
+
+
+def _radius_graph(pos, r_c, K, r_basis):
+    from scipy.spatial import cKDTree
+    N = pos.shape[0]
+    pairs = cKDTree(pos).query_pairs(r_c, output_type="ndarray").astype(np.int64)
+    recv = np.concatenate([pairs[:, 0], pairs[:, 1]])
+    send = np.concatenate([pairs[:, 1], pairs[:, 0]])
+    evec = pos[send] - pos[recv]
+    rowptr, send, evec = _csr(N, recv, send, evec)
+    d = np.linalg.norm(evec, axis=1)
+    return Graph(N, rowptr, send, evec.astype(np.float32), bessel_basis(d, K, r_basis).astype(np.float32))
+
+
+def degree_graph(degree, N=2048, seed=100, K=REGIME_K, side=20.0):
+    """One fixed set of N uniform points in a cube of side `side`; the cutoff is found by bisection on
+    the realized pair distances so that the mean receiver degree is `degree` (ties aside, exactly)."""
+    from scipy.spatial.distance import pdist
+    rng = np.random.default_rng(np.random.SeedSequence(seed).spawn(6)[0])
+    pos = rng.uniform(0.0, side, size=(N, 3))
+    dist = np.sort(pdist(pos))
+    n_pairs = int(round(degree * N / 2))          # unordered pairs for the target mean degree
+    r_c = float(0.5 * (dist[n_pairs - 1] + dist[n_pairs])) if n_pairs < len(dist) else float(dist[-1] * 1.0001)
+    return _radius_graph(pos, r_c, K, r_c), r_c
+
+
+def graph_count_graph(B, nodes=128, degree=32.0, r_c=5.0, seed=101, K=REGIME_K):
+    """B copies of one nodes-node radius graph of mean degree about `degree` (a block-diagonal batch):
+    copy b's node ids are offset by b * nodes, its edges are the base graph's."""
+    base = cube_graph(nodes, degree, r_c, seed, K)
+    Eb = base.E
+    rowptr = np.concatenate([[0], (base.rowptr[1:][None, :] + Eb * np.arange(B)[:, None]).reshape(-1)])
+    sender = (base.sender[None, :] + nodes * np.arange(B)[:, None]).reshape(-1)
+    return Graph(nodes * B, rowptr.astype(np.int32), sender.astype(np.int32), np.tile(base.evec, (B, 1)),
+                 np.tile(base.phi, (B, 1)))
+
+
 def config_graph(name):
     c = CONFIGS[name]
     if c["kind"] == "tiny":

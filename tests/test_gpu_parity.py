@@ -195,7 +195,8 @@ def test_retained_state(gpu, sig, N, E, seed):
     state.fill_(float("nan"))                       # every element the backward reads must be written
     m = api.conv_fwd(plan, graph, *args, state=state, budget=1 << 20)   # small budget: the state is one chunk anyway
     assert max_rel(_n(m), oc.fwd(*oracle_args(case, prob))) <= FWD_TOL
-    assert np.array_equal(_n(m), _n(api.conv_fwd(plan, graph, *args)))
+    # the state GEMM's split-K depends on the chunk size, so budgets differ only in summation order
+    assert max_rel(_n(m), _n(api.conv_fwd(plan, graph, *args))) <= 1e-5
     gout = _t(case["gout"])
     ref = oc.bwd(*oracle_args(case, prob), case["gout"])
     for budget in (0, 1 << 20):                     # one chunk, and many chunks for the edge stage
