@@ -309,12 +309,14 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
       w.kfloats = kf;
       return layout_total(p, w, pass);
     };
-    const int64_t emin = std::max<int64_t>(1, G.max_deg), eall = std::max<int64_t>(G.max_deg, E);
-    const int64_t ec0 = per_edge ? emin : eall;
+    const int64_t eall = std::max<int64_t>(G.max_deg, E);
+    const int64_t ec0 = per_edge ? 1 : eall;
     // A capacity nc of receivers leaves, after the fixed part, the partials, the state of nc
     // receivers and the split-K region (what fits of it), every byte to the per-edge
-    // contributions.  Among candidate capacities keep the one with the fewest chunks
-    // (about max(N / nc, E / ec)), ties to the larger nc.
+    // contributions, whose windows of ec edges need not follow receiver boundaries.  Among
+    // candidate capacities keep the cheapest, counting a receiver chunk (state, GEMMs, the
+    // per-group launches) as four edge windows (one edge kernel and one sender reduction),
+    // ties to the larger nc.
     // The split-K region is reserved whole (strict) unless no capacity fits with it.
     struct Cand { int64_t nc = 0, ec = 0; size_t kf = 0, need = 0, score = 0; };
     bool strict = true;
@@ -339,7 +341,7 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
         c.ec = ec;
         c.need = total_at(nc, ec, c.kf);
       }
-      c.score = std::max<size_t>(cdiv(N, nc), per_edge ? cdiv(std::max<int64_t>(1, E), c.ec) : 1);
+      c.score = 4 * (size_t)cdiv(N, nc) + (per_edge ? cdiv(std::max<int64_t>(1, E), c.ec) : 0);
       return c;
     };
     std::vector<int64_t> cands;
@@ -366,7 +368,7 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
       }
     }
     if (best.score && best.nc < std::max<int64_t>(1, N)) {
-      // refine: the largest capacity with the same chunk count (bisection above the best)
+      // refine: the largest capacity with no higher cost (bisection above the best)
       int64_t lo = best.nc, hi = std::min<int64_t>(N, 2 * best.nc);
       while (hi - lo > 1) {
         const int64_t mid = lo + (hi - lo) / 2;
@@ -392,18 +394,12 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
   if (sizing_only) return SOBEK_OK;
   if (need > ws_bytes)
     return fail(SOBEK_E_WORKSPACE, "workspace of %zu bytes is below the minimum %zu for this pass", ws_bytes, need);
-  // greedy receiver chunks under both capacities
+  // receiver chunks of ncap receivers; the edge kernels walk each chunk's edges in
+  // windows of ecap edges
   w.chunks.clear();
-  int64_t r = 0;
-  while (r < N) {
-    int64_t n = 0, e0 = G.h_rowptr[r];
-    while (r + n < N && n < w.ncap) {
-      int64_t e_next = G.h_rowptr[r + n + 1];
-      if (per_edge && n > 0 && e_next - e0 > w.ecap) break;
-      ++n;
-    }
-    w.chunks.push_back({(int)r, (int)n, e0, (int64_t)G.h_rowptr[r + n]});
-    r += n;
+  for (int64_t r = 0; r < N; r += w.ncap) {
+    const int64_t n = std::min<int64_t>(w.ncap, N - r);
+    w.chunks.push_back({(int)r, (int)n, (int64_t)G.h_rowptr[r], (int64_t)G.h_rowptr[r + n]});
   }
   return SOBEK_OK;
 }
@@ -537,13 +533,37 @@ int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float
   return SOBEK_OK;
 }
 
-int run_sender_reduce(const Plan& p, const sobek_graph_s& G, const Chunk& c, const WsPlan& w, void* ws,
+int run_sender_reduce(const Plan& p, const sobek_graph_s& G, int64_t ea, int64_t eb, const WsPlan& w, void* ws,
                       const float* contrib, float* gx, int first, hipStream_t s) {
-  int N = (int)G.N, CX = p.dim_in, e0 = (int)c.e0, e1 = (int)c.e1;
+  int N = (int)G.N, CX = p.dim_in, e0 = (int)ea, e1 = (int)eb;
   int* cursor = (int*)((char*)ws + w.off_cursor);
   LAUNCH(p.k.sender_reduce, cdiv(G.N, 4), 1, 1, s, (const int*)G.send_rowptr, (const int*)G.send_perm, contrib, gx,
          cursor, N, CX, e0, e1, first);
   return SOBEK_OK;
+}
+
+// Edge windows of a receiver chunk for the edge-owned adjoint kernels: consecutive
+// ranges of at most w.ecap edges (the x-gradient contribution buffer), each handed
+// to f(ea, eb, ra, nr) with the receivers [ra, ra + nr) that own its edges.
+template <class F>
+int for_edge_windows(const sobek_graph_s& G, const Chunk& c, const WsPlan& w, F&& f) {
+  const int32_t* rp = G.h_rowptr.data();
+  const int64_t step = std::max<int64_t>(1, w.ecap);
+  for (int64_t ea = c.e0; ea < c.e1; ea += step) {
+    const int64_t eb = std::min<int64_t>(c.e1, ea + step);
+    const int ra = (int)(std::upper_bound(rp + c.r0, rp + c.r0 + c.n + 1, (int32_t)ea) - rp) - 1;
+    const int rb = (int)(std::lower_bound(rp + c.r0, rp + c.r0 + c.n + 1, (int32_t)eb) - rp);
+    if (int rc = f(ea, eb, ra, rb - ra)) return rc;
+  }
+  return SOBEK_OK;
+}
+
+// blockIdx.y split of the adjoint edge kernels: spread the window's receivers' edges
+// until about 512 blocks run, at least 16 edges per wave of a block
+int adj_edge_split(const Plan& p, int nr, int64_t ne) {
+  const int64_t per_block = 16 * p.adj_waves;
+  const int64_t by_work = std::max<int64_t>(1, ne / std::max(1, nr) / per_block);
+  return (int)std::max<int64_t>(1, std::min<int64_t>({cdiv(512, std::max(1, nr)), by_work, 64}));
 }
 
 int check_common(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
@@ -920,6 +940,7 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     if ((rc = run_ga(p, all, w, ws, state, G.N, gk, gW, true, true, stream))) return rc;
   }
   if (adj_state && (rc = run_sbar(p, all, G.N, gk, W, adj_state, stream))) return rc;
+  bool first_win = true;  // the first edge window overall initialises the sender cursors and x-gradient rows
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
     if (gW && !state) {
@@ -928,15 +949,22 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     }
     if (edge) {
       if (!adj_state && (rc = run_sbar(p, c, w.ncap, gk, W, Sb, stream))) return rc;
-      int r0 = c.r0, n = c.n, e0 = (int)c.e0, flags = 0;
-      long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
-      int sb_r0 = adj_state ? c.r0 : 0;
-      LAUNCH_N(p.k.bwd_E, 64 * p.adj_waves, n, 1, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
-             (const float*)(adj_state ? adj_state : Sb), (const float*)nullptr, (const float*)nullptr,
-             (const float*)nullptr, (const float*)nullptr, gphi, gevec, contrib, r0, n, ncap, e0, flags, sb_ncap, sb_r0);
-      if (gx && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
+      rc = for_edge_windows(G, c, w, [&](int64_t ea, int64_t eb, int ra, int nr) -> int {
+        int e0 = (int)ea, e1 = (int)eb, flags = 0, sub_off = ra - c.r0;
+        long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
+        int sb_r0 = adj_state ? ra : sub_off;
+        LAUNCH_N(p.k.bwd_E, 64 * p.adj_waves, nr, adj_edge_split(p, nr, eb - ea), 1, stream, (const int*)G.rowptr,
+                 (const int*)G.sender, evec, phi, xk, (const float*)(adj_state ? adj_state : Sb), (const float*)nullptr,
+                 (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, gphi, gevec, contrib, ra, nr, ncap,
+                 e0, flags, sb_ncap, sb_r0, e0, e1, sub_off);
+        const int first = first_win;
+        first_win = false;
+        return gx ? run_sender_reduce(p, G, ea, eb, w, ws, contrib, gxk, first, stream) : SOBEK_OK;
+      });
+      if (rc) return rc;
     }
   }
+  if (gx && first_win && (rc = fill_zero(p, gxk, G.N * p.dim_in, stream))) return rc;  // no edges at all
   if (mulir && gx && (rc = transpose(p, gxk, gx, G.N, true, 1, stream))) return rc;
   return SOBEK_OK;
 }
@@ -1029,6 +1057,7 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
   float* Sb2 = state_ptr(w, ws, p, 1);
   float* contrib = g_x ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = g_x || g_evec || g_phi;
+  bool first_win = true;  // the first edge window overall initialises the sender cursors and x-gradient rows
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
     if (tan && (g_gout || g_W)) {
@@ -1044,16 +1073,22 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
     if (edge) {
       if (!adj_state && (rc = run_sbar(p, c, w.ncap, gk, W, Sb, stream))) return rc;
       if (t_gW && (rc = run_sbar(p, c, w.ncap, gk, t_gW, Sb2, stream))) return rc;
-      int r0 = c.r0, n = c.n, e0 = (int)c.e0;
-      long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
-      int sb_r0 = adj_state ? c.r0 : 0;
-      int fl = flags;
-      LAUNCH_N(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, 64 * p.adj_waves, n, 1, 1, stream, (const int*)G.rowptr,
-               (const int*)G.sender, evec, phi, xk, (const float*)(adj_state ? adj_state : Sb), (const float*)Sb2, txk,
-               t_gevec, t_gphi, g_phi, g_evec, contrib, r0, n, ncap, e0, fl, sb_ncap, sb_r0);
-      if (g_x && (rc = run_sender_reduce(p, G, c, w, ws, contrib, gxk, ci == 0, stream))) return rc;
+      rc = for_edge_windows(G, c, w, [&](int64_t ea, int64_t eb, int ra, int nr) -> int {
+        int e0 = (int)ea, e1 = (int)eb, fl = flags, sub_off = ra - c.r0;
+        long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
+        int sb_r0 = adj_state ? ra : sub_off;
+        LAUNCH_N(flags == 4 ? p.k.dbwd_E_r : p.k.dbwd_E, 64 * p.adj_waves, nr, adj_edge_split(p, nr, eb - ea), 1,
+                 stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi, xk,
+                 (const float*)(adj_state ? adj_state : Sb), (const float*)Sb2, txk, t_gevec, t_gphi, g_phi, g_evec,
+                 contrib, ra, nr, ncap, e0, fl, sb_ncap, sb_r0, e0, e1, sub_off);
+        const int first = first_win;
+        first_win = false;
+        return g_x ? run_sender_reduce(p, G, ea, eb, w, ws, contrib, gxk, first, stream) : SOBEK_OK;
+      });
+      if (rc) return rc;
     }
   }
+  if (g_x && first_win && (rc = fill_zero(p, gxk, G.N * p.dim_in, stream))) return rc;  // no edges at all
   if (g_gout && (rc = zero_dead_out(p, ggk, G.N, stream))) return rc;
   if (mulir) {
     if (g_gout && (rc = transpose(p, ggk, g_gout, G.N, false, 1, stream))) return rc;

@@ -980,7 +980,8 @@ void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* ind
     }
   const int W = P.vec4 ? 4 : 1;  // floats per copy unit
   // Sbar: group blocks sb_ncap receivers apart, this receiver at row sb_r0 + il (a
-  // workspace chunk slot, or a state kept for every receiver); Sbar': the chunk slot
+  // workspace chunk slot, or a state kept for every receiver); Sbar': the chunk slot,
+  // row sub_off + il
   auto src_expr = [&](const Sl& x, const std::string& t, int pass) {
     std::ostringstream e;
     const int per_q = x.DO * 16 / W;   // copy units per q row
@@ -988,7 +989,7 @@ void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* ind
       << ", uc = " << x.u0 << " + " << W << " * (r % " << 16 / W << ");\n"
       << indent << "    const bool ok = q < K && uc < " << x.q->c_in << ";\n"
       << indent << "    const sb_i64 src = " << (pass ? "ncap" : "sb_ncap") << " * " << x.g->s_off << "LL + ((sb_i64)"
-      << (pass ? "il" : "(sb_r0 + il)") << " * " << x.g->d << " + m) * " << x.g->D << "LL + " << x.q->koff << " + q * "
+      << (pass ? "(sub_off + il)" : "(sb_r0 + il)") << " * " << x.g->d << " + m) * " << x.g->D << "LL + " << x.q->koff << " + q * "
       << x.q->c_in << " + uc;\n";
     return e.str();
   };
@@ -1077,9 +1078,9 @@ std::string generate_source(const Plan& P) {
     o << "  }\n}\n";
   }
 
-  // adjoint edge kernels: one block of ADJ_W waves per receiver, adjoint state
-  // staged in LDS slab by slab, every wave owning a disjoint set of the
-  // receiver's edges
+  // adjoint edge kernels: blocks of ADJ_W waves over (receiver, share of its edges),
+  // adjoint state staged in LDS slab by slab, every wave owning a disjoint set of
+  // the block's edges
   for (int s = 0; s < (int)P.slabs.size(); ++s) emit_adj_slab(o, P, s);
   const int LDSF = std::max(1, P.bwd_lds_max);
   const int NSL = (int)P.slabs.size();
@@ -1088,12 +1089,17 @@ std::string generate_source(const Plan& P) {
        " const float* __restrict__ Sb, const float* __restrict__ Sb2, const float* __restrict__ xdot,"
        " const float* __restrict__ evdot, const float* __restrict__ phidot, float* __restrict__ gphi,"
        " float* __restrict__ gevec, float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags,"
-       " sb_i64 sb_ncap, int sb_r0, float* sS, float* sS2, float* sacc, int* sids) {\n"
+       " sb_i64 sb_ncap, int sb_r0, int win0, int win1, int sub_off, float* sS, float* sS2, float* sacc, int* sids) {\n"
        "  const int il = blockIdx.x;\n"
        "  if (il >= n_recv) return;\n"
        "  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;\n"
        "  const int fl = FL >= 0 ? FL : flags;\n"
-       "  const int beg = rowptr[r0 + il], end = rowptr[r0 + il + 1];\n";
+       // the receiver's edges inside the launch's edge window [win0, win1), split evenly over
+       // blockIdx.y in whole 16-edge batches of every wave (edge outputs need no reduction)
+       "  const int wb = max(rowptr[r0 + il], win0), we = min(rowptr[r0 + il + 1], win1);\n"
+       "  const int span = ((we - wb + (int)gridDim.y - 1) / (int)gridDim.y + 16 * ADJ_W - 1) / (16 * ADJ_W) * (16 * ADJ_W);\n"
+       "  const int beg = wb + (int)blockIdx.y * span, end = min(we, beg + span);\n"
+       "  if (beg >= end) return;\n";
   if (NSL == 1) {
     emit_adj_stage(o, P, 0, "  ");
     o << "  __syncthreads();\n"
@@ -1122,7 +1128,7 @@ std::string generate_source(const Plan& P) {
          " const float* __restrict__ Sb2, const float* __restrict__ xdot, const float* __restrict__ evdot,"
          " const float* __restrict__ phidot, float* __restrict__ gphi, float* __restrict__ gevec,"
          " float* __restrict__ contrib, int r0, int n_recv, sb_i64 ncap, int e0, int flags, sb_i64 sb_ncap,"
-         " int sb_r0) {\n"
+         " int sb_r0, int win0, int win1, int sub_off) {\n"
       << "  __shared__ __attribute__((aligned(16))) float sS[" << LDSF * kv.lds_mult << "];\n"
       << "  __shared__ int sids[ADJ_W * 256];  // per-wave sender ids of the current segment\n";
     if (NSL > 1)
@@ -1131,7 +1137,7 @@ std::string generate_source(const Plan& P) {
       o << "  float* sacc = nullptr;\n";
     o << "  sb_adj_body<" << (kv.db ? "true" : "false") << ", " << kv.fl
       << ">(rowptr, sender, evec, phi, x, Sb, Sb2, xdot, evdot, phidot, gphi, gevec, contrib, r0, n_recv, ncap, e0,"
-         " flags, sb_ncap, sb_r0, sS, sS + " << (kv.lds_mult == 2 ? LDSF : 0) << ", sacc, sids);\n}\n";
+         " flags, sb_ncap, sb_r0, win0, win1, sub_off, sS, sS + " << (kv.lds_mult == 2 ? LDSF : 0) << ", sacc, sids);\n}\n";
   }
   return o.str();
 }
