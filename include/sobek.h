@@ -71,6 +71,7 @@ typedef enum sobek_status {
 enum { SOBEK_LAYOUT_IR_MUL = 0, SOBEK_LAYOUT_MUL_IR = 1 };
 enum { SOBEK_DTYPE_F32 = 0 };
 enum { SOBEK_NORM_NONE = 0, SOBEK_NORM_FAN_IN = 1 };
+enum { SOBEK_MODE_UVW = 0, SOBEK_MODE_UVU = 1 };
 enum { SOBEK_PASS_FWD = 0, SOBEK_PASS_BWD = 1, SOBEK_PASS_DBWD = 2 };
 
 /* One irreducible representation: multiplicity, order l >= 0, parity +1 ('e') or -1 ('o'). */
@@ -87,26 +88,34 @@ int sobek_version(void);
 /* Plan: paths, tables and kernels for one operator signature.
  *   in[n_in], out[n_out]: input and output irreps (mul >= 1, 0 <= l <= 3).
  *   lmax: spherical harmonics 1x0e + 1x1o + ... up to lmax (<= 3), parity (-1)^l.
- *   K: radial width (1..64).  layout: SOBEK_LAYOUT_*.  dtype: SOBEK_DTYPE_F32.
+ *   K: radial width (1..64).
+ *   mode: SOBEK_MODE_UVW, fully connected channel mixing (eq. uvw_connection):
+ *         a path owns C_in*C_out weights, W[q][w_off + u*C_out + w];
+ *         SOBEK_MODE_UVU, channelwise (eq. uvu_connection): every path needs
+ *         C_out = C_in (else SOBEK_E_INVALID) and owns C_in weights,
+ *         W[q][w_off + u], output channel u = input channel u.
+ *   layout: SOBEK_LAYOUT_*.  dtype: SOBEK_DTYPE_F32.
  *   path_norm: SOBEK_NORM_NONE (alpha = 1) or SOBEK_NORM_FAN_IN
- *   (alpha = 1/sqrt(sum of C_in over the paths into the same output irrep)).
+ *   (alpha = 1/sqrt(fan_in), fan_in = number of terms summed into one output
+ *   channel: the sum of C_in over the paths into the same output irrep for
+ *   uvw, the number of such paths for uvu).
  * Paths are every (input, SH, output) triple allowed by the selection rules
- * of Section 2.2 (eq. cg_selection_rules), in lexicographic index order; each
- * owns C_in*C_out weights (eq. num_weights).  Kernels are generated for the
- * signature and compiled with hipRTC for gfx950 (cached on disk).  The plan
- * must be destroyed with sobek_plan_destroy. */
+ * of Section 2.2 (eq. cg_selection_rules), in lexicographic index order, with
+ * weight offsets w_off in that order (eq. num_weights).  Kernels are generated
+ * for the signature and compiled with hipRTC for gfx950 (cached on disk).  The
+ * plan must be destroyed with sobek_plan_destroy. */
 int sobek_plan_create(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out,
-                      int K, int layout, int dtype, int path_norm, sobek_plan *plan);
+                      int K, int mode, int layout, int dtype, int path_norm, sobek_plan *plan);
 int sobek_plan_destroy(sobek_plan plan);
 /* Generate and compile (hipRTC, gfx950) the kernels of a signature into the
  * on-disk code-object cache without touching a GPU; arguments as in
  * sobek_plan_create.  Lets a build step prepare kernels ahead of a GPU run. */
 int sobek_jit_compile(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out, int K,
-                      int layout, int dtype, int path_norm);
+                      int mode, int layout, int dtype, int path_norm);
 /* Full HIP source generated for a signature (prelude + plan code), NUL-terminated
  * into buf when buf_bytes allows; *needed gets the size including the NUL. */
 int sobek_plan_source(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out, int K,
-                      int layout, int dtype, int path_norm, char *buf, size_t buf_bytes, size_t *needed);
+                      int mode, int layout, int dtype, int path_norm, char *buf, size_t buf_bytes, size_t *needed);
 /* Sizes of the plan; any output pointer may be NULL. */
 int sobek_plan_info(sobek_plan plan, int64_t *n_paths, int64_t *n_weights, int64_t *dim_in,
                     int64_t *dim_out, int64_t *dim_sh);

@@ -102,11 +102,16 @@ def real_cg(l1, l2, l3):
     return Q
 
 
-def path_coefficients(paths, normalization="none"):
-    """c^pi = alpha_pi Q^(l_in, l_sh, l_out) for every path (eq. angular_path_contraction)."""
+def path_coefficients(paths, normalization="none", mode="uvw"):
+    """c^pi = alpha_pi Q^(l_in, l_sh, l_out) for every path (eq. angular_path_contraction).
+
+    With "fan_in" normalisation alpha = 1/sqrt(fan_in), fan_in being the number of
+    terms summed into one output channel: C_in per path into the output irrep for
+    fully connected mixing, one per path for channelwise mixing.
+    """
     fan = {}
     for p in paths:
-        fan[p["i_out"]] = fan.get(p["i_out"], 0) + p["c_in"]
+        fan[p["i_out"]] = fan.get(p["i_out"], 0) + (1 if mode == "uvu" else p["c_in"])
     out = []
     for p in paths:
         Q = real_cg(p["l_in"], p["l_sh"], p["l_out"])

@@ -35,6 +35,12 @@ vectors rather than Y, the edge-vector gradient has one extra chain term the
 paper's Y-input operator does not have:
     g_evec = J^T g_Y + sum_m Y_bar_m Hess(Y_m) evec_dot.
 
+Channel modes (§2.3): fully connected ``uvw`` (eq. ``uvw_connection``) mixes
+every input channel u into every output channel w of a path with the C_in x
+C_out block W_e[pi, u, w]; channelwise ``uvu`` (eq. ``uvu_connection``) ties
+output channel u to input channel u with one weight W_e[pi, u] (C_out = C_in).
+Only the per-path mixing (``_apply`` and its two transposes) depends on the mode.
+
 Receiver route (cross-check of the reassociation)
 -------------------------------------------------
 §4.2-§4.4: S_i = sum_e phi_e (x) C_e (eq. ``receiver_state``), m = S A (eq.
@@ -65,6 +71,7 @@ class Problem:
     K: int
     normalization: str = "none"
     layout: str = "ir_mul"
+    mode: str = "uvw"           # "uvw": eq. uvw_connection; "uvu": eq. uvu_connection
     paths: list = field(init=False)
     coeffs: list = field(init=False)
     irreps_sh: list = field(init=False)
@@ -74,8 +81,8 @@ class Problem:
         self.irreps_in = _ir.parse_irreps(self.irreps_in)
         self.irreps_out = _ir.parse_irreps(self.irreps_out)
         self.irreps_sh = _ir.sh_irreps(self.lmax)
-        self.paths = _ir.enumerate_paths(self.irreps_in, self.irreps_sh, self.irreps_out)
-        self.coeffs = _cg.path_coefficients(self.paths, self.normalization)
+        self.paths = _ir.enumerate_paths(self.irreps_in, self.irreps_sh, self.irreps_out, self.mode)
+        self.coeffs = _cg.path_coefficients(self.paths, self.normalization, self.mode)
         self.n_w = _ir.num_weights(self.paths)
 
     @property
@@ -120,6 +127,34 @@ def _prepare(prob, x, rowptr, sender):
 
 
 # ---------------------------------------------------------------------------
+# channel mixing of one path (§2.3): fully connected, eq. uvw_connection,
+# z_w = sum_u W[u, w] T_u; channelwise, eq. uvu_connection, z_u = W[u] T_u
+# ---------------------------------------------------------------------------
+
+def _w_path(prob, We, p):
+    """Per-edge weights of path p: [e, C_in, C_out] (uvw) or [e, C_in] (uvu)."""
+    sl = We[:, p["w_off"]:p["w_off"] + p["n_w"]]
+    return sl.reshape(len(We), p["c_in"], p["c_out"]) if prob.mode == "uvw" else sl
+
+
+def _apply(prob, Wp, T):
+    """Message [e, C_out, d_out] of path weights Wp on unweighted contractions T [e, C_in, d_out]."""
+    return np.matmul(np.swapaxes(Wp, 1, 2), T) if prob.mode == "uvw" else Wp[:, :, None] * T
+
+
+def _apply_T(prob, Wp, G):
+    """Transpose of _apply in T: D [e, C_in, d_out] from a message-shaped G [e, C_out, d_out]."""
+    return np.matmul(Wp, G) if prob.mode == "uvw" else Wp[:, :, None] * G
+
+
+def _weight_adj(prob, T, G):
+    """Transpose of _apply in the weights: h [e, n_w of the path] = d<G, _apply(W, T)>/dW."""
+    if prob.mode == "uvw":
+        return np.matmul(T, np.swapaxes(G, 1, 2)).reshape(len(T), -1)
+    return np.einsum("eum,eum->eu", T, G)
+
+
+# ---------------------------------------------------------------------------
 # materialised route
 # ---------------------------------------------------------------------------
 
@@ -133,10 +168,10 @@ def fwd(prob, x, evec, phi, W, rowptr, sender):
         Y = _sh.sh(prob.lmax, evec[s:t])
         We = phi[s:t] @ W                                  # edge weights, eq. radial_projection_background
         for p, c in zip(prob.paths, prob.coeffs):
-            Wp = We[:, p["w_off"]:p["w_off"] + p["n_w"]].reshape(t - s, p["c_in"], p["c_out"])
+            Wp = _w_path(prob, We, p)
             xs = xb[p["i_in"]][send[s:t]]                    # [e, C_in, d_in]
             Ct = np.matmul(xs, _contract_y(c, _sh_slice(Y, p["l_sh"])))   # [e, C_in, d_out]
-            msg = np.matmul(np.swapaxes(Wp, 1, 2), Ct)     # [e, C_out, d_out]
+            msg = _apply(prob, Wp, Ct)                     # [e, C_out, d_out]
             np.add.at(mb[p["i_out"]], recv[s:t], msg)
     return _ir.blocks_to_flat(mb, prob.irreps_out, prob.layout)
 
@@ -161,16 +196,16 @@ def bwd(prob, x, evec, phi, W, rowptr, sender, gout):
         h = np.zeros((e, prob.n_w))
         gY = np.zeros((e, nsh))
         for p, c in zip(prob.paths, prob.coeffs):
-            Wp = We[:, p["w_off"]:p["w_off"] + p["n_w"]].reshape(e, p["c_in"], p["c_out"])
+            Wp = _w_path(prob, We, p)
             Yb = _sh_slice(Y, p["l_sh"])
             M = _contract_y(c, Yb)
             xs = xb[p["i_in"]][send[s:t]]
             Ct = np.matmul(xs, M)                          # T(x_j, Y) unweighted
             gr = gb[p["i_out"]][recv[s:t]]                 # m_bar of the receiver [e, C_out, d_out]
             # h[e, u, w] = <m_bar_i, T_{pi,(u,w)}>      (eq. streamed_weight_adjoint)
-            h[:, p["w_off"]:p["w_off"] + p["n_w"]] = np.matmul(Ct, np.swapaxes(gr, 1, 2)).reshape(e, -1)
+            h[:, p["w_off"]:p["w_off"] + p["n_w"]] = _weight_adj(prob, Ct, gr)
             # D[e, u, m_o] = sum_w W_e[u, w] m_bar[w, m_o]
-            D = np.matmul(Wp, gr)
+            D = _apply_T(prob, Wp, gr)
             # x_bar_j += D_x T^* : sum_{m_y, m_o} c Y D        (eq. streamed_operand_adjoints)
             np.add.at(gxb[p["i_in"]], send[s:t], np.matmul(D, np.swapaxes(M, 1, 2)))
             # Y_bar += D_Y T^* : sum_{m_i, m_o, u} c x D
@@ -219,8 +254,8 @@ def dbwd(prob, x, evec, phi, W, rowptr, sender, gout,
         Ybar = np.zeros((e, nsh))
         for p, c in zip(prob.paths, prob.coeffs):
             sl = slice(p["w_off"], p["w_off"] + p["n_w"])
-            Wp = We[:, sl].reshape(e, p["c_in"], p["c_out"])
-            Wdp = Wed[:, sl].reshape(e, p["c_in"], p["c_out"])
+            Wp = _w_path(prob, We, p)
+            Wdp = _w_path(prob, Wed, p)
             l = p["l_sh"]
             M = _contract_y(c, _sh_slice(Y, l))
             Md = _contract_y(c, _sh_slice(Yd, l))
@@ -230,12 +265,12 @@ def dbwd(prob, x, evec, phi, W, rowptr, sender, gout,
             Ctd = np.matmul(xds, M) + np.matmul(xs, Md)               # T_dot = T(x_dot, Y) + T(x, Y_dot)
             gr = gb[p["i_out"]][recv[s:t]]
             # tangent output m_dot = sum (w_dot T + w T_dot)  -> gradient for m_bar
-            msg = np.matmul(np.swapaxes(Wdp, 1, 2), Ct) + np.matmul(np.swapaxes(Wp, 1, 2), Ctd)
+            msg = _apply(prob, Wdp, Ct) + _apply(prob, Wp, Ctd)
             np.add.at(out_m[p["i_out"]], recv[s:t], msg)
-            h[:, sl] = np.matmul(Ct, np.swapaxes(gr, 1, 2)).reshape(e, -1)
-            hd[:, sl] = np.matmul(Ctd, np.swapaxes(gr, 1, 2)).reshape(e, -1)   # h_dot = <m_bar, T_dot>
-            D = np.matmul(Wp, gr)
-            Dd = np.matmul(Wdp, gr)
+            h[:, sl] = _weight_adj(prob, Ct, gr)
+            hd[:, sl] = _weight_adj(prob, Ctd, gr)                    # h_dot = <m_bar, T_dot>
+            D = _apply_T(prob, Wp, gr)
+            Dd = _apply_T(prob, Wdp, gr)
             # x_bar_dot = sum (w_dot B^x + w B_dot^x), B_dot^x = D_x T(., Y_dot)^* m_bar
             np.add.at(g_xb[p["i_in"]], send[s:t],
                       np.matmul(Dd, np.swapaxes(M, 1, 2)) + np.matmul(D, np.swapaxes(Md, 1, 2)))
@@ -277,15 +312,34 @@ def _receiver_state(prob, phi, Cs, recv, N):
 
 
 def _A(prob, W, p):
-    """A_pi = [K, C_in, C_out] view of the flattened weights."""
-    return W[:, p["w_off"]:p["w_off"] + p["n_w"]].reshape(prob.K, p["c_in"], p["c_out"])
+    """A_pi: [K, C_in, C_out] (uvw) or [K, C_in] (uvu) view of the flattened weights."""
+    Wp = W[:, p["w_off"]:p["w_off"] + p["n_w"]]
+    return Wp.reshape(prob.K, p["c_in"], p["c_out"]) if prob.mode == "uvw" else Wp
+
+
+def _state_times_A(prob, Sp, A):
+    """Receiver mixing of one path: m[n, w, m_o] = sum_{q, u} S[n, q, u, m_o] A[q, u, w] (uvw);
+    m[n, u, m_o] = sum_q S[n, q, u, m_o] A[q, u] (uvu)."""
+    return np.einsum("nqum,quw->nwm", Sp, A) if prob.mode == "uvw" else np.einsum("nqum,qu->num", Sp, A)
+
+
+def _adjoint_state(prob, A, g):
+    """S_bar[n, q, u, m_o] = m_bar A^T of one path (eq. receiver_adjoint)."""
+    return np.einsum("quw,nwm->nqum", A, g) if prob.mode == "uvw" else np.einsum("qu,num->nqum", A, g)
+
+
+def _state_T_mbar(prob, Sp, g):
+    """A_bar = S^T m_bar of one path, flattened like its weights (eq. receiver_adjoint)."""
+    if prob.mode == "uvw":
+        return np.einsum("nqum,nwm->quw", Sp, g).reshape(prob.K, -1)
+    return np.einsum("nqum,num->qu", Sp, g)
 
 
 def _mix(prob, S, W, N):
     """m = S A per output group  (eqs. receiver_mixing / receiver_matrix_product)."""
     mb = [np.zeros((N, mul, 2 * l + 1)) for (mul, l, _p) in prob.irreps_out]
     for p, Sp in zip(prob.paths, S):
-        mb[p["i_out"]] += np.einsum("nqum,quw->nwm", Sp, _A(prob, W, p))
+        mb[p["i_out"]] += _state_times_A(prob, Sp, _A(prob, W, p))
     return mb
 
 
@@ -329,8 +383,8 @@ def bwd_receiver(prob, x, evec, phi, W, rowptr, sender, gout):
     for p, Sp in zip(prob.paths, S):
         A = _A(prob, W, p)
         g = gb[p["i_out"]]
-        Sbar.append(np.einsum("quw,nwm->nqum", A, g))         # S_bar = m_bar A^T   (eq. receiver_adjoint)
-        gW[:, p["w_off"]:p["w_off"] + p["n_w"]] = np.einsum("nqum,nwm->quw", Sp, g).reshape(prob.K, -1)
+        Sbar.append(_adjoint_state(prob, A, g))              # S_bar = m_bar A^T   (eq. receiver_adjoint)
+        gW[:, p["w_off"]:p["w_off"] + p["n_w"]] = _state_T_mbar(prob, Sp, g)
     gphi, gY, gxb = _edge_adjoints(prob, xb, Y, send, recv, phi, Sbar, N)
     return dict(gx=_ir.blocks_to_flat(gxb, prob.irreps_in, prob.layout),
                 gevec=np.einsum("ej,ejk->ek", gY, J), gphi=gphi, gW=gW)
@@ -366,9 +420,9 @@ def dbwd_receiver(prob, x, evec, phi, W, rowptr, sender, gout,
     g_xb = [np.zeros_like(b) for b in xb]
     for p, c, Ct, Ctd, dSp in zip(prob.paths, prob.coeffs, C, Cd, dS):
         A, Ad, g = _A(prob, W, p), _A(prob, Wd, p), gb[p["i_out"]]
-        Sb = np.einsum("quw,nwm->nqum", A, g)[recv]           # S_bar  = m_bar A^T
-        Sbp = np.einsum("quw,nwm->nqum", Ad, g)[recv]         # S_bar' = m_bar dA^T
-        g_W[:, p["w_off"]:p["w_off"] + p["n_w"]] = np.einsum("nqum,nwm->quw", dSp, g).reshape(prob.K, -1)
+        Sb = _adjoint_state(prob, A, g)[recv]                 # S_bar  = m_bar A^T
+        Sbp = _adjoint_state(prob, Ad, g)[recv]               # S_bar' = m_bar dA^T
+        g_W[:, p["w_off"]:p["w_off"] + p["n_w"]] = _state_T_mbar(prob, dSp, g)
         G = np.einsum("eq,equm->eum", phi, Sb)
         Gd = np.einsum("eq,equm->eum", phid, Sb) + np.einsum("eq,equm->eum", phi, Sbp)
         g_phi += np.einsum("equm,eum->eq", Sb, Ctd) + np.einsum("equm,eum->eq", Sbp, Ct)

@@ -67,12 +67,15 @@ def offsets(irreps):
     return offs
 
 
-def enumerate_paths(irreps_in, irreps_sh, irreps_out):
+def enumerate_paths(irreps_in, irreps_sh, irreps_out, mode="uvw"):
     """All paths allowed by eq. cg_selection_rules, lexicographic order.
 
     Returns dicts with the irrep indices, orders, multiplicities, the path's
-    weight count n = C_in C_out (eq. num_weights) and its offset in the
-    flattened weight axis.
+    weight count and its offset in the flattened weight axis.  The count is
+    C_in C_out for fully connected mixing (eq. uvw_connection, eq. num_weights)
+    and C_in for channelwise mixing (eq. uvu_connection), which ties the output
+    multiplicity to the input one: a channelwise path with C_out != C_in is an
+    error.
     """
     paths, off = [], 0
     for ia, (ca, la, pa) in enumerate(irreps_in):
@@ -84,7 +87,14 @@ def enumerate_paths(irreps_in, irreps_sh, irreps_out):
                     continue
                 if pc != pa * pb:
                     continue
-                n = ca * cc
+                if mode == "uvu":
+                    if cc != ca:
+                        raise ValueError(f"uvu path {ia}->{ic} needs C_out = C_in, got {ca} and {cc}")
+                    n = ca
+                elif mode == "uvw":
+                    n = ca * cc
+                else:
+                    raise ValueError(mode)
                 paths.append(dict(i_in=ia, i_sh=ib, i_out=ic, l_in=la, l_sh=lb,
                                   l_out=lc, c_in=ca, c_out=cc, n_w=n, w_off=off))
                 off += n
@@ -92,7 +102,7 @@ def enumerate_paths(irreps_in, irreps_sh, irreps_out):
 
 
 def num_weights(paths):
-    """N_w = sum over paths of C_in C_out  (eq. num_weights)."""
+    """N_w = sum over paths of their weight counts (C_in C_out each for uvw, eq. num_weights; C_in for uvu)."""
     return sum(p["n_w"] for p in paths)
 
 

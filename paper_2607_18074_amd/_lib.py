@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libsobek_hip.so")
 
 LAYOUTS = {"ir_mul": 0, "mul_ir": 1}
 NORMS = {"none": 0, "fan_in": 1}
+MODES = {"uvw": 0, "uvu": 1}
 PASSES = {"fwd": 0, "bwd": 1, "dbwd": 2}
 STATUS = {0: "OK", -1: "INVALID", -2: "UNSUPPORTED", -3: "SHAPE", -4: "ALIGN", -5: "WORKSPACE",
           -6: "HIP", -7: "INTERNAL", -8: "COMPILE"}
@@ -40,11 +41,11 @@ _SIGNATURES = {
     "sobek_last_error": (ctypes.c_char_p, []),
     "sobek_version": (_INT, []),
     "sobek_plan_create": (_INT, [ctypes.POINTER(Irrep), _INT, _INT, ctypes.POINTER(Irrep), _INT, _INT, _INT, _INT,
-                                 _INT, ctypes.POINTER(_P)]),
+                                 _INT, _INT, ctypes.POINTER(_P)]),
     "sobek_jit_compile": (_INT, [ctypes.POINTER(Irrep), _INT, _INT, ctypes.POINTER(Irrep), _INT, _INT, _INT, _INT,
-                                 _INT]),
+                                 _INT, _INT]),
     "sobek_plan_source": (_INT, [ctypes.POINTER(Irrep), _INT, _INT, ctypes.POINTER(Irrep), _INT, _INT, _INT, _INT,
-                                 _INT, ctypes.c_char_p, _SZ, ctypes.POINTER(_SZ)]),
+                                 _INT, _INT, ctypes.c_char_p, _SZ, ctypes.POINTER(_SZ)]),
     "sobek_plan_destroy": (_INT, [_P]),
     "sobek_plan_info": (_INT, [_P] + [ctypes.POINTER(_I64)] * 5),
     "sobek_plan_paths": (_INT, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
@@ -119,20 +120,20 @@ def irrep_array(spec):
     return arr, len(v)
 
 
-def _sig_args(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none"):
+def _sig_args(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
     a, na = irrep_array(irreps_in)
     b, nb = irrep_array(irreps_out)
-    return (a, na, int(lmax), b, nb, int(K), LAYOUTS[layout], 0, NORMS[normalization])
+    return (a, na, int(lmax), b, nb, int(K), MODES[mode], LAYOUTS[layout], 0, NORMS[normalization])
 
 
-def jit_compile(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none"):
+def jit_compile(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
     """Generate and compile the kernels of a signature into the code-object cache (no GPU needed)."""
-    check(lib().sobek_jit_compile(*_sig_args(irreps_in, lmax, irreps_out, K, layout, normalization)))
+    check(lib().sobek_jit_compile(*_sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode)))
 
 
-def plan_source(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none"):
+def plan_source(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
     """The full HIP source compiled for a signature."""
-    args = _sig_args(irreps_in, lmax, irreps_out, K, layout, normalization)
+    args = _sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode)
     need = _SZ(0)
     check(lib().sobek_plan_source(*args, None, 0, ctypes.byref(need)))
     buf = ctypes.create_string_buffer(need.value)

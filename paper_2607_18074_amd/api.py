@@ -40,13 +40,15 @@ def _check_tensor(t, name, shape, dtype=torch.float32):
 
 
 class Plan:
-    """Operator signature: irreps, spherical-harmonic order, radial width."""
+    """Operator signature: irreps, spherical-harmonic order, radial width, channel mode ("uvw" fully
+    connected, "uvu" channelwise)."""
 
-    def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none"):
+    def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
         self.irreps_in = _lib.parse_irreps(irreps_in)
         self.irreps_out = _lib.parse_irreps(irreps_out)
         self.lmax, self.K, self.layout, self.normalization = int(lmax), int(K), layout, normalization
-        args = _lib._sig_args(irreps_in, lmax, irreps_out, K, layout, normalization)
+        self.mode = mode
+        args = _lib._sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode)
         h = _P()
         check(lib().sobek_plan_create(*args, ctypes.byref(h)))
         self._h = h
@@ -73,14 +75,16 @@ class Plan:
         return np.array(buf).reshape(2 * li + 1, 2 * ls + 1, 2 * lo + 1)
 
     def weight_std(self):
-        """Per-column std 1/sqrt(K * fan_in) of the weight init (fan_in = sum of C_in into the output irrep)."""
+        """Per-column std 1/sqrt(K * fan_in) of the weight init (fan_in = terms summed into one output
+        channel: the sum of C_in over the paths into the output irrep for uvw, their number for uvu)."""
         fan = {}
         paths = self.paths()
+        uvu = self.mode == "uvu"
         for (a, _b, c, _w) in paths:
-            fan[c] = fan.get(c, 0) + self.irreps_in[a][0]
+            fan[c] = fan.get(c, 0) + (1 if uvu else self.irreps_in[a][0])
         std = np.zeros(self.n_weights)
         for (a, _b, c, w) in paths:
-            n = self.irreps_in[a][0] * self.irreps_out[c][0]
+            n = self.irreps_in[a][0] * (1 if uvu else self.irreps_out[c][0])
             std[w:w + n] = 1.0 / np.sqrt(self.K * fan[c])
         return std
 

@@ -140,8 +140,8 @@ int validate_irreps(const sobek_irrep* v, int n, std::vector<sobek::Irrep>& out,
   return SOBEK_OK;
 }
 
-int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
-                    int dtype, int norm, Plan& p) {
+int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int mode,
+                    int layout, int dtype, int norm, Plan& p) {
   int rc;
   if ((rc = validate_irreps(in, n_in, p.in, "input")) != SOBEK_OK) return rc;
   if ((rc = validate_irreps(out, n_out, p.out, "output")) != SOBEK_OK) return rc;
@@ -151,9 +151,12 @@ int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep
   if (layout != SOBEK_LAYOUT_IR_MUL && layout != SOBEK_LAYOUT_MUL_IR) return fail(SOBEK_E_INVALID, "bad layout");
   if (dtype != SOBEK_DTYPE_F32) return fail(SOBEK_E_UNSUPPORTED, "only SOBEK_DTYPE_F32 is implemented");
   if (norm != SOBEK_NORM_NONE && norm != SOBEK_NORM_FAN_IN) return fail(SOBEK_E_INVALID, "bad path normalisation");
-  p.lmax = lmax; p.K = K; p.layout = layout; p.dtype = dtype; p.norm = norm;
+  if (mode != SOBEK_MODE_UVW && mode != SOBEK_MODE_UVU) return fail(SOBEK_E_INVALID, "bad mode");
+  p.lmax = lmax; p.K = K; p.layout = layout; p.dtype = dtype; p.norm = norm; p.mode = mode;
   try {
     sobek::build_plan(p);
+  } catch (const std::invalid_argument& ex) {
+    return fail(SOBEK_E_INVALID, "plan: %s", ex.what());
   } catch (const std::exception& ex) {
     return fail(SOBEK_E_UNSUPPORTED, "plan: %s", ex.what());
   }
@@ -461,6 +464,11 @@ int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const floa
   for (auto& g : p.groups) {
     const float* Sg = S + (size_t)w.ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
+    if (p.mode == SOBEK_MODE_UVU) {
+      LAUNCH(p.k.uvu_mix, cdiv((int64_t)nrows * Cg, 256), 1, 1, s, Sg, nrows, D, Cg, W,
+             (const int*)(p.d_ktab + g.ktab_off), out, dg, off, CX, r0, acc);
+      continue;
+    }
     int bn = gemm_bn(g.C);
     if (p.vec4) {
       int kper = D;
@@ -486,7 +494,10 @@ int run_sbar(const Plan& p, const Chunk& c, int64_t s_ncap, const float* M, cons
   for (auto& g : p.groups) {
     float* Sg = Sbar + (size_t)s_ncap * g.s_off;
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
-    if (p.vec4)
+    if (p.mode == SOBEK_MODE_UVU)
+      LAUNCH(p.k.uvu_sbar, cdiv((int64_t)nrows * D, 256), 1, 1, s, M, nrows, D, Cg, W,
+             (const int*)(p.d_ktab + g.ktab_off), Sg, dg, off, CX, r0);
+    else if (p.vec4)
     {
       // spread the 64-wide column tiles over blockIdx.y until about kSaTarget blocks run,
       // keeping at least four tiles per block
@@ -517,6 +528,17 @@ int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float
     int rps = (int)(((int64_t)cdiv(nrows, ns) + 31) / 32 * 32);
     int bn = gemm_bn(g.C);
     int acc = first_chunk ? 0 : 1;
+    if (p.mode == SOBEK_MODE_UVU) {
+      // channelwise: one weight per column k of S (P[split][k]); the region holds ns * D * C floats
+      LAUNCH(p.k.uvu_ga, cdiv(D, 256), 1, ns, s, Sg, nrows, D, Cg, M, P, dg, off, CX, r0, rps, acc);
+      if (last_chunk) {
+        int one = 1, ncol = 1;
+        LAUNCH(p.k.ga_reduce, cdiv((int64_t)D, 256), 1, 1, s, (const float*)P, ns, D, ncol,
+               (const int*)(p.d_ktab + g.ktab_off), gW, one);
+      }
+      P += (size_t)ns * g.D * g.C;
+      continue;
+    }
     if (p.vec4)
       LAUNCH(p.k.gemm_ga_v[bn_index(bn)], cdiv(D, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
              rps, acc);
@@ -589,13 +611,13 @@ extern "C" {
 const char* sobek_last_error(void) { return g_err.c_str(); }
 int sobek_version(void) { return 1; }
 
-int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
-                      int dtype, int path_norm, sobek_plan* plan) {
+int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int mode,
+                      int layout, int dtype, int path_norm, sobek_plan* plan) {
   if (!plan) return fail(SOBEK_E_INVALID, "plan output pointer is NULL");
   *plan = nullptr;
   std::unique_ptr<sobek_plan_s> h(new sobek_plan_s());
   Plan& p = h->p;
-  int rc = build_signature(in, n_in, lmax, out, n_out, K, layout, dtype, path_norm, p);
+  int rc = build_signature(in, n_in, lmax, out, n_out, K, mode, layout, dtype, path_norm, p);
   if (rc != SOBEK_OK) return rc;
   std::vector<char> code;
   try {
@@ -617,7 +639,9 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
       (rc = get(p.k.dbwd_E, "sobek_dbwd_E")) || (rc = get(p.k.dbwd_E_r, "sobek_dbwd_E_r")) ||
       (rc = get(p.k.ga_reduce, "sobek_ga_reduce")) || (rc = get(p.k.sender_reduce, "sobek_sender_reduce")) ||
       (rc = get(p.k.transpose, "sobek_transpose")) || (rc = get(p.k.fill_cols, "sobek_fill_cols")) ||
-      (rc = get(p.k.zero, "sobek_zero")) || (rc = get(p.k.sa_reduce, "sobek_sa_reduce")))
+      (rc = get(p.k.zero, "sobek_zero")) || (rc = get(p.k.sa_reduce, "sobek_sa_reduce")) ||
+      (rc = get(p.k.uvu_mix, "sobek_uvu_mix")) || (rc = get(p.k.uvu_sbar, "sobek_uvu_sbar")) ||
+      (rc = get(p.k.uvu_ga, "sobek_uvu_ga")))
     return rc;
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
@@ -657,10 +681,10 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   return SOBEK_OK;
 }
 
-int sobek_jit_compile(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
-                      int dtype, int path_norm) {
+int sobek_jit_compile(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int mode,
+                      int layout, int dtype, int path_norm) {
   Plan p;
-  int rc = build_signature(in, n_in, lmax, out, n_out, K, layout, dtype, path_norm, p);
+  int rc = build_signature(in, n_in, lmax, out, n_out, K, mode, layout, dtype, path_norm, p);
   if (rc != SOBEK_OK) return rc;
   try {
     sobek::jit_compile(p.source);
@@ -670,10 +694,10 @@ int sobek_jit_compile(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   return SOBEK_OK;
 }
 
-int sobek_plan_source(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int layout,
-                      int dtype, int path_norm, char* buf, size_t buf_bytes, size_t* needed) {
+int sobek_plan_source(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int mode,
+                      int layout, int dtype, int path_norm, char* buf, size_t buf_bytes, size_t* needed) {
   Plan p;
-  int rc = build_signature(in, n_in, lmax, out, n_out, K, layout, dtype, path_norm, p);
+  int rc = build_signature(in, n_in, lmax, out, n_out, K, mode, layout, dtype, path_norm, p);
   if (rc != SOBEK_OK) return rc;
   std::string s = sobek::full_source(p.source);
   if (needed) *needed = s.size() + 1;

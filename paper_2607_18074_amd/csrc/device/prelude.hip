@@ -585,6 +585,56 @@ extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sbar_v(const float*
   sb_gemm_sbar_v(M, nrows, D, W, ktab, Sbar, dg, Cg, off, CX, r0);
 }
 
+// ---------------------------------------------------------------------------
+// Channelwise (uvu) mixing, eq. uvu_connection in receiver form: a path's
+// weights A[q, path, u] pair state column k = koff + q*C + u with output
+// channel u only, so the three channel products are elementwise in u and
+// reduce over (path, q) or over rows; ktab[k] is the W offset of column k.
+// Memory bound: one pass over the state (or its adjoint) per launch.
+// ---------------------------------------------------------------------------
+
+// out rows (r0 + r / dg, r % dg), channel u (+)= sum_j W[ktab[j*C + u]] S[r, j*C + u]
+extern "C" __global__ __launch_bounds__(256) void sobek_uvu_mix(const float* __restrict__ S, int nrows, int D, int C,
+                                                                const float* __restrict__ W,
+                                                                const int* __restrict__ ktab, float* __restrict__ out,
+                                                                int dg, int off, int CX, int r0, int accumulate) {
+  const sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (sb_i64)nrows * C) return;
+  const int r = (int)(t / C), u = (int)(t % C);
+  const float* s = S + (sb_i64)r * D + u;
+  float acc = 0.f;
+  for (int k = 0; k < D; k += C) acc += W[ktab[k + u]] * s[k];
+  float* o = out + sb_row_addr(r, dg, C, off, CX, r0) + u;
+  *o = accumulate ? (*o + acc) : acc;
+}
+
+// Sbar[r, k] = mbar(row r, channel k % C) W[ktab[k]]
+extern "C" __global__ __launch_bounds__(256) void sobek_uvu_sbar(const float* __restrict__ M, int nrows, int D, int C,
+                                                                 const float* __restrict__ W,
+                                                                 const int* __restrict__ ktab,
+                                                                 float* __restrict__ Sbar, int dg, int off, int CX,
+                                                                 int r0) {
+  const sb_i64 t = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (sb_i64)nrows * D) return;
+  const int r = (int)(t / D), k = (int)(t % D);
+  Sbar[t] = M[sb_row_addr(r, dg, C, off, CX, r0) + k % C] * W[ktab[k]];
+}
+
+// P[split, k] (+)= sum over the split's rows r of S[r, k] mbar(row r, channel k % C)
+extern "C" __global__ __launch_bounds__(256) void sobek_uvu_ga(const float* __restrict__ S, int nrows, int D, int C,
+                                                               const float* __restrict__ M, float* __restrict__ P,
+                                                               int dg, int off, int CX, int r0, int rows_per_split,
+                                                               int accumulate) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= D) return;
+  const int rbeg = blockIdx.z * rows_per_split, rend = min(nrows, rbeg + rows_per_split);
+  const int u = k % C;
+  float acc = 0.f;
+  for (int r = rbeg; r < rend; ++r) acc += S[(sb_i64)r * D + k] * M[sb_row_addr(r, dg, C, off, CX, r0) + u];
+  float* o = P + (sb_i64)blockIdx.z * D + k;
+  *o = accumulate ? (*o + acc) : acc;
+}
+
 // gW[ktab[k] + w] = (first ? 0 : gW[..]) + sum_{s < nsplit} P[s, k, w]   (fixed split order)
 extern "C" __global__ __launch_bounds__(256) void sobek_ga_reduce(const float* P, int nsplit, int D, int Cg,
                                                                   const int* ktab, float* gW, int first) {

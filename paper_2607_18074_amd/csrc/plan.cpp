@@ -59,12 +59,15 @@ void build_plan(Plan& p) {
         int psh = (b % 2) ? -1 : 1;
         if (ro.l < std::abs(ri.l - b) || ro.l > ri.l + b) continue;
         if (ro.p != ri.p * psh) continue;
+        if (p.mode == 1 && ro.mul != ri.mul)
+          throw std::invalid_argument("uvu path " + std::to_string(a) + " -> " + std::to_string(c) +
+                                      " needs equal input and output multiplicities");
         Path q;
         q.i_in = a; q.i_sh = b; q.i_out = c;
         q.l_in = ri.l; q.l_sh = b; q.l_out = ro.l;
         q.c_in = ri.mul; q.c_out = ro.mul;
         q.w_off = woff;
-        woff += (int64_t)ri.mul * ro.mul;
+        woff += p.mode == 1 ? (int64_t)ri.mul : (int64_t)ri.mul * ro.mul;
         p.paths.push_back(q);
       }
   p.n_w = woff;
@@ -81,7 +84,7 @@ void build_plan(Plan& p) {
     g.i_out = c; g.l = p.out[c].l; g.d = 2 * g.l + 1; g.C = p.out[c].mul; g.off = p.out[c].off;
     g.paths = ps;
     int64_t fan = 0, k = 0;
-    for (int t : ps) fan += p.paths[t].c_in;
+    for (int t : ps) fan += p.mode == 1 ? 1 : p.paths[t].c_in;  // terms summed into one output channel
     for (int t : ps) {
       Path& q = p.paths[t];
       q.alpha = (p.norm == 1) ? 1.0 / std::sqrt((double)fan) : 1.0;
@@ -103,7 +106,8 @@ void build_plan(Plan& p) {
     for (int t : g.paths) {
       const Path& q = p.paths[t];
       for (int qq = 0; qq < p.K; ++qq)
-        for (int u = 0; u < q.c_in; ++u) p.ktab.push_back((int32_t)(qq * p.n_w + q.w_off + (int64_t)u * q.c_out));
+        for (int u = 0; u < q.c_in; ++u)  // W row of (q, path, u): uvw mixes C_out columns from it, uvu reads one
+          p.ktab.push_back((int32_t)(qq * p.n_w + q.w_off + (int64_t)u * (p.mode == 1 ? 1 : q.c_out)));
     }
   }
   p.srow = soff;

@@ -76,11 +76,13 @@ struct Kernels {
   std::map<int, hipFunction_t> gemm_sbar_c;  // streaming adjoint-state GEMM per output multiplicity
   hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
                 zero = nullptr, sa_reduce = nullptr;
+  hipFunction_t uvu_mix = nullptr, uvu_sbar = nullptr, uvu_ga = nullptr;  // channelwise mixing
 };
 
 struct Plan {
   std::vector<Irrep> in, out;
   int lmax = 0, K = 0, layout = 0, dtype = 0, norm = 0;
+  int mode = 0;                 // 0: uvw (fully connected mixing), 1: uvu (channelwise)
   int dim_in = 0, dim_out = 0, nsh = 0;
   int64_t n_w = 0;
   std::vector<Path> paths;

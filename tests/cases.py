@@ -17,6 +17,10 @@ SIGS = {
     "wide": ("128x0e+128x1o+128x2e+64x3o", 3, "128x0e+128x1o+128x2e+64x3o", 16),
     # odd multiplicities, a dead input irrep (0o reaches nothing) and a dead output irrep (3e)
     "odd": ("3x0e+5x1o+2x2e+1x0o", 1, "4x0e+3x1o+2x2e+1x3e", 4),
+    # channelwise (uvu) signatures: equal multiplicities along every path
+    "uvu_small": ("16x0e+16x1o+16x2e", 2, "16x0e+16x1o+16x2e", 8),
+    "uvu_l3": ("8x0e+8x1o+8x2e+8x3o", 3, "8x0e+8x1o+8x2e+8x3o", 16),
+    "uvu_odd": ("3x0e+3x1o+3x1e+3x2e", 1, "3x0e+3x1o+3x1e+3x2e+1x3e", 4),   # 3e: dead output
 }
 
 
@@ -27,20 +31,21 @@ def max_rel(a, b):
     return float(np.abs(a - b).max() / den) if den > 0 else float(np.abs(a).max())
 
 
-def std_for(irr_in, irr_out, lmax, K):
-    """Per-weight-column std 1/sqrt(K fan_in) from an independent path count."""
+def std_for(irr_in, irr_out, lmax, K, mode="uvw"):
+    """Per-weight-column std 1/sqrt(K fan_in) from an independent path count (fan_in: terms summed
+    into one output channel, C_in per path for uvw and one per path for uvu)."""
     from oracle import irreps as ir
-    paths = ir.enumerate_paths(ir.parse_irreps(irr_in), ir.sh_irreps(lmax), ir.parse_irreps(irr_out))
+    paths = ir.enumerate_paths(ir.parse_irreps(irr_in), ir.sh_irreps(lmax), ir.parse_irreps(irr_out), mode)
     fan = {}
     for p in paths:
-        fan[p["i_out"]] = fan.get(p["i_out"], 0) + p["c_in"]
+        fan[p["i_out"]] = fan.get(p["i_out"], 0) + (1 if mode == "uvu" else p["c_in"])
     std = np.zeros(ir.num_weights(paths))
     for p in paths:
         std[p["w_off"]:p["w_off"] + p["n_w"]] = 1.0 / np.sqrt(K * fan[p["i_out"]])
     return std
 
 
-def make_case(sig, N, E, seed, isolated=0):
+def make_case(sig, N, E, seed, isolated=0, mode="uvw"):
     """Random receiver-sorted graph (last `isolated` nodes receive nothing) plus all tensors."""
     irr_in, lmax, irr_out, K = SIGS[sig] if isinstance(sig, str) else sig
     from oracle import irreps as ir
@@ -55,12 +60,13 @@ def make_case(sig, N, E, seed, isolated=0):
         recv, send, ev, ph = recv[order], g.sender[order], g.evec[order], g.phi[order]
         rowptr = np.concatenate([[0], np.cumsum(np.bincount(recv, minlength=N))]).astype(np.int32)
         g = wl.Graph(N, rowptr, send.astype(np.int32), ev, ph)
-    std = std_for(irr_in, irr_out, lmax, K)
+    std = std_for(irr_in, irr_out, lmax, K, mode)
     x = wl.node_features(N, din, seed)
     W = wl.weights(K, std, seed)
     gout = wl.out_cotangent(N, dout, seed)
     cot = wl.cotangents(N, g.E, K, din, len(std), seed)
-    return dict(sig=(irr_in, lmax, irr_out, K), graph=g, x=x, W=W, gout=gout, cot=cot, dim_in=din, dim_out=dout)
+    return dict(sig=(irr_in, lmax, irr_out, K), graph=g, x=x, W=W, gout=gout, cot=cot, dim_in=din, dim_out=dout,
+                mode=mode)
 
 
 def edge_subgraph(g, edges):

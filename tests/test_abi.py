@@ -75,6 +75,9 @@ def test_error_codes():
         _lib.plan_source("8x0e", 1, "8x1o", 0)            # K = 0
     assert e.value.code == -1
     with pytest.raises(_lib.SobekError) as e:
+        _lib.plan_source("8x0e+4x1o", 1, "8x0e+4x1o", 4, mode="uvu")   # uvu path 0e x 1o -> 1o joins 8 and 4
+    assert e.value.code == -1
+    with pytest.raises(_lib.SobekError) as e:
         _lib.cg_table(1, 1, 3)                            # triangle rule
     assert e.value.code == -1
     import ctypes
@@ -96,6 +99,16 @@ def test_generated_source_reflects_paths():
     assert "v_pk_" not in src
 
 
+def test_uvu_source_carries_channelwise_normalisation():
+    # fan_in counts paths for uvu (3 paths reach 0e here) and C_in for uvw (3 * 8)
+    su = _lib.plan_source("8x0e+8x1o+8x2e", 2, "8x0e+8x1o+8x2e", 4, "ir_mul", "fan_in", "uvu")
+    sw = _lib.plan_source("8x0e+8x1o+8x2e", 2, "8x0e+8x1o+8x2e", 4, "ir_mul", "fan_in", "uvw")
+    assert "alpha=%g" % (1 / np.sqrt(3)) in su and "alpha=%g" % (1 / np.sqrt(24)) in sw
+    for kname in ("sobek_uvu_mix", "sobek_uvu_sbar", "sobek_uvu_ga"):
+        assert kname in su
+
+
 def test_jit_compiles_for_gfx950():
     _lib.jit_compile("8x0e+8x1o", 1, "8x0e+8x1o", 8)
+    _lib.jit_compile("8x0e+8x1o", 1, "8x0e+8x1o", 8, "ir_mul", "fan_in", "uvu")
     _lib.jit_compile("3x0e+5x1o+2x2e+1x0o", 1, "4x0e+3x1o+2x2e+1x3e", 4, "mul_ir", "fan_in")
