@@ -67,7 +67,7 @@ def flop_model(plan, N, E):
         nnz = int(np.count_nonzero(plan.cg(t)))
         SD += cin * (2 * lo + 1)
         NZ += cin * nnz
-        G += cin * (2 * lo + 1) * cout
+        G += cin * (2 * lo + 1) * (1 if getattr(plan, "mode", "uvw") == "uvu" else cout)  # uvu: elementwise
     edge_fwd = E * (2 * K * SD + 2 * NZ)
     edge_adj = E * (4 * K * SD + 6 * NZ)
     gemm = N * 2 * K * G
@@ -176,6 +176,86 @@ def sweep(budget_gib, names):
             f"{r['tflops']:.1f} | {100 * r['frac_fp32']:.1f} | {r['alg_gbs']:.0f} | {r['peak_mem_gb']:.2f} |")
 
 
+def time_graph_passes(plan, W, g, passes, budget, retain):
+    """Time each pass of `passes` on graph g with the paper's protocol; one dict per pass."""
+    import torch
+
+    from paper_2607_18074_amd import api
+    from paper_2607_18074_amd import workloads as wl
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    graph = api.Graph(T(g.rowptr), T(g.sender))
+    xt, ev, ph = T(wl.node_features(g.N, plan.dim_in, 7)), T(g.evec), T(g.phi)
+    gt = T(wl.out_cotangent(g.N, plan.dim_out, 7))
+    state = api.new_state(plan, graph) if retain else None
+    adj = api.new_state(plan, graph) if retain else None
+    fm = flop_model(plan, g.N, g.E)
+    out = []
+    for pname in passes:
+        graph._ws.clear()
+        torch.cuda.empty_cache()
+        ws = graph.workspace(plan, pname, budget)
+        if pname == "fwd":
+            fn = lambda: api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)  # noqa: E731
+        elif pname == "bwd":
+            if retain:
+                api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)
+            fn = lambda: api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,  # noqa: E731
+                                      adj_state=adj)
+        else:
+            rdot = (2.0 * api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,
+                                       adj_state=adj)[1]).contiguous()
+            fn = lambda: api.conv_dbwd(plan, graph, xt, ev, ph, W, gt, t_gevec=rdot, ws=ws,  # noqa: E731
+                                       adj_state=adj)
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        ms, n = time_pass(fn, torch)
+        tf = fm["passes"][pname] / (ms * 1e-3) / 1e12
+        out.append(dict(N=g.N, E=g.E, mean_degree=g.E / g.N, pass_=pname, ms=ms, samples=n,
+                        edges_per_s=g.E / (ms * 1e-3), tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS,
+                        peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9, workspace_gb=ws.numel() / 1e9))
+        del ws, fn
+    del graph, xt, ev, ph, gt, state, adj
+    torch.cuda.empty_cache()
+    return out
+
+
+def tables(which, budget_gib, retain):
+    """The paper's capacity-matched grids (Section 5.4, Tables 3 and 4): every profile and pass on B copies
+    of the fixed 128-node degree-32 graph, B the paper's graph count for that pass, timed with its protocol;
+    the paper's own M edges/s (another GPU) printed beside ours for context."""
+    import torch
+
+    from paper_2607_18074_amd import api
+    from paper_2607_18074_amd import workloads as wl
+    torch.cuda.set_device(0)
+    budget = int(budget_gib * (1 << 30))
+    grids = []
+    if which in ("uvw", "all"):
+        grids.append(("uvw", wl.PAPER_TABLE3_UVW))
+    if which in ("uvu", "all"):
+        grids.append(("uvu", wl.PAPER_TABLE4_UVU))
+    rows = []
+    for mode, grid in grids:
+        for prof, (n_w, Bs, paper) in grid.items():
+            spec, lmax = wl.profile_irreps(prof)
+            plan = api.Plan(spec, lmax, spec, wl.REGIME_K, mode=mode)
+            assert plan.n_weights == n_w, (prof, plan.n_weights, n_w)
+            W = torch.from_numpy(wl.weights(plan.K, plan.weight_std(), 7)).cuda()
+            for pi, pname in enumerate(("fwd", "bwd", "dbwd")):
+                g = wl.graph_count_graph(Bs[pi])
+                r = time_graph_passes(plan, W, g, (pname,), budget, retain)[0]
+                r.update(mode=mode, profile=prof, graphs=Bs[pi], paper_medges_per_s=paper[pi])
+                rows.append(r)
+                print(json.dumps({k.rstrip("_"): x for k, x in r.items()}), flush=True)
+            del plan, W
+    log("| mode | profile | pass | graphs B | E | M edges/s | paper's (RTX 5090) | % fp32 | peak GB |")
+    log("|---|---|---|---:|---:|---:|---:|---:|---:|")
+    for r in rows:
+        log(f"| {r['mode']} | {r['profile']} | {r['pass_']} | {r['graphs']} | {r['E']:,} | "
+            f"{r['edges_per_s'] / 1e6:,.1f} | {r['paper_medges_per_s']:,.1f} | {100 * r['frac_fp32']:.1f} | "
+            f"{r['peak_mem_gb']:.2f} |")
+
+
 def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd")):
     """The paper's scaling regimes: degree scaling (2,048 nodes, mean degree 4..1,023) and graph-count
     scaling (B copies of a 128-node degree-32 graph, B = 2..511) on its representative profiles, every
@@ -195,42 +275,10 @@ def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd")):
                  [("count", b) for b in wl.GRAPH_COUNT_GRID if "count" in kinds]
         for kind, v in points:
             g = wl.degree_graph(v)[0] if kind == "degree" else wl.graph_count_graph(v)
-            T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
-            graph = api.Graph(T(g.rowptr), T(g.sender))
-            xt, ev, ph = T(wl.node_features(g.N, plan.dim_in, 7)), T(g.evec), T(g.phi)
-            gt = T(wl.out_cotangent(g.N, plan.dim_out, 7))
-            state = api.new_state(plan, graph) if retain else None
-            adj = api.new_state(plan, graph) if retain else None
-            fm = flop_model(plan, g.N, g.E)
-            rdot = None
-            for pname in passes:
-                graph._ws.clear()
-                torch.cuda.empty_cache()
-                ws = graph.workspace(plan, pname, budget)
-                if pname == "fwd":
-                    fn = lambda: api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)  # noqa: E731
-                elif pname == "bwd":
-                    if retain:
-                        api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)
-                    fn = lambda: api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,  # noqa: E731
-                                              adj_state=adj)
-                else:
-                    rdot = (2.0 * api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,
-                                               adj_state=adj)[1]).contiguous()
-                    fn = lambda: api.conv_dbwd(plan, graph, xt, ev, ph, W, gt, t_gevec=rdot, ws=ws,  # noqa: E731
-                                               adj_state=adj)
-                torch.cuda.synchronize()
-                torch.cuda.reset_peak_memory_stats()
-                ms, n = time_pass(fn, torch)
-                tf = fm["passes"][pname] / (ms * 1e-3) / 1e12
-                row = dict(profile=prof, regime=kind, value=v, N=g.N, E=g.E, mean_degree=g.E / g.N, pass_=pname,
-                           ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3), tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS,
-                           peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9, workspace_gb=ws.numel() / 1e9)
+            for row in time_graph_passes(plan, W, g, passes, budget, retain):
+                row.update(profile=prof, regime=kind, value=v)
                 rows.append(row)
                 print(json.dumps({k.rstrip("_"): x for k, x in row.items()}), flush=True)
-                del ws, fn
-            del graph, xt, ev, ph, gt, state, adj, rdot
-            torch.cuda.empty_cache()
         del plan, W
     log("| profile | regime | N | E | pass | edges/s | % fp32 | peak GB |")
     log("|---|---|---:|---:|---|---:|---:|---:|")
@@ -337,6 +385,8 @@ def main():
     ap.add_argument("--regimes", default="", help="'degree', 'count' or 'all': the paper's scaling regimes on its "
                     "profiles (--profiles), one JSON line per point and pass")
     ap.add_argument("--profiles", default="128/64,128/64/64,128/64/64/64")
+    ap.add_argument("--tables", default="", help="'uvw', 'uvu' or 'all': the paper's capacity-matched grids "
+                    "(Tables 3 and 4) at its graph counts, one JSON line per profile and pass")
     ap.add_argument("--retain", action="store_true", help="regimes: keep S and Sbar across passes (default: the "
                     "paper's setting, recompute within the workspace budget)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
@@ -357,6 +407,9 @@ def main():
               "would shard); rerun with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    if args.tables:
+        tables(args.tables, args.budget, args.retain)
+        return
     if args.regimes:
         kinds = ("degree", "count") if args.regimes == "all" else tuple(args.regimes.split(","))
         regimes(kinds, args.profiles.split(","), args.budget, args.retain)

@@ -148,9 +148,44 @@ GRAPH_COUNT_GRID = (2, 3, 5, 8, 13, 23, 38, 64, 108, 181, 304, 511)
 REGIME_K = 16
 
 
+# The paper's capacity-matched grids on the fixed 128-node, degree-32 graph (Section 5.4): per profile
+# and pass the graph count B at which its comparison was run, and its own M edges/s there (RTX 5090,
+# fp32), kept only to print beside our numbers.  Table 3: fully connected uvw; Table 4: channelwise uvu.
+#   profile: (N_w, (B_fwd, B_bwd, B_dbwd), (fwd, bwd, dbwd M edges/s))
+PAPER_TABLE3_UVW = {
+    "32/16": (2304, (862, 431, 215), (661.0, 104.7, 24.3)),
+    "32/32": (4096, (487, 243, 121), (723.5, 91.9, 22.9)),
+    "32/16/16": (4608, (433, 216, 108), (188.3, 17.4, 5.3)),
+    "32/32/32": (11264, (178, 88, 44), (170.4, 11.9, 3.7)),
+    "32/16/16/16": (8192, (244, 121, 60), (85.9, 12.7, 3.3)),
+    "32/32/32/32": (23552, (85, 42, 21), (70.8, 6.9, 1.8)),
+    "64/32": (9216, (217, 108, 54), (423.9, 58.8, 14.3)),
+    "64/64": (16384, (122, 61, 30), (345.7, 43.3, 9.2)),
+    "64/32/32": (18432, (108, 54, 27), (125.7, 9.8, 3.1)),
+    "64/64/64": (45056, (44, 22, 11), (86.4, 5.5, 1.7)),
+    "64/32/32/32": (32768, (61, 30, 15), (59.7, 7.9, 2.0)),
+    "64/64/64/64": (94208, (21, 10, 5), (34.6, 3.2, 0.8)),
+    "128/64": (36864, (54, 27, 13), (197.0, 28.1, 5.4)),
+    "128/128": (65536, (30, 15, 7), (132.2, 14.0, 4.0)),
+    "128/64/64": (73728, (27, 13, 6), (66.8, 4.7, 1.4)),
+    "128/64/64/64": (131072, (15, 7, 3), (26.8, 4.0, 1.0)),
+}
+PAPER_TABLE4_UVU = {
+    "64/64/64/64": (1472, (1279, 641, 323), (108.1, 28.3, 8.6)),
+    "128/128/128": (1408, (1332, 669, 337), (390.7, 41.0, 9.9)),
+    "128/128/128/128": (2944, (647, 323, 163), (57.5, 14.7, 4.3)),
+    "256/256": (1024, (1807, 909, 460), (513.8, 52.5, 14.9)),
+    "256/256/256": (2816, (672, 336, 169), (173.4, 20.2, 5.0)),
+    "256/256/256/256": (5888, (325, 162, 81), (28.9, 6.9, 2.0)),
+    "512/512": (2048, (914, 458, 231), (262.2, 27.4, 7.8)),
+    "512/512/512": (5632, (338, 168, 85), (90.5, 10.6, 2.6)),
+    "1024/1024": (4096, (459, 229, 116), (141.1, 15.0, 4.2)),
+}
+
+
 def profile_irreps(name):
     """'128/64/64' -> ('128x0e+64x1o+64x2e', lmax 2): one irrep per l, parity (-1)^l, SH up to the same l."""
-    muls = REGIME_PROFILES[name]
+    muls = tuple(int(m) for m in name.split("/"))
     spec = "+".join(f"{m}x{l}{'e' if l % 2 == 0 else 'o'}" for l, m in enumerate(muls))
     return spec, len(muls) - 1
 
