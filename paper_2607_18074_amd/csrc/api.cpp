@@ -344,7 +344,8 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
         c.ec = ec;
         c.need = total_at(nc, ec, c.kf);
       }
-      c.score = 4 * (size_t)cdiv(N, nc) + (per_edge ? cdiv(std::max<int64_t>(1, E), c.ec) : 0);
+      const int64_t R = cdiv(N, nc), per_chunk = (std::max<int64_t>(1, E) + R - 1) / R;
+      c.score = 4 * (size_t)R + (per_edge ? (size_t)R * cdiv(per_chunk, c.ec) : 0);
       return c;
     };
     std::vector<int64_t> cands;
@@ -570,7 +571,9 @@ int run_sender_reduce(const Plan& p, const sobek_graph_s& G, int64_t ea, int64_t
 template <class F>
 int for_edge_windows(const sobek_graph_s& G, const Chunk& c, const WsPlan& w, F&& f) {
   const int32_t* rp = G.h_rowptr.data();
-  const int64_t step = std::max<int64_t>(1, w.ecap);
+  // equal windows: the fewest that respect the capacity
+  const int64_t ne = c.e1 - c.e0, cap = std::max<int64_t>(1, w.ecap);
+  const int64_t step = ne > 0 ? (ne + (ne + cap - 1) / cap - 1) / ((ne + cap - 1) / cap) : 1;
   for (int64_t ea = c.e0; ea < c.e1; ea += step) {
     const int64_t eb = std::min<int64_t>(c.e1, ea + step);
     const int ra = (int)(std::upper_bound(rp + c.r0, rp + c.r0 + c.n + 1, (int32_t)ea) - rp) - 1;
