@@ -25,6 +25,10 @@ class SobekError(RuntimeError):
     def __init__(self, code, message):
         super().__init__(f"sobek error {code} ({STATUS.get(code, '?')}): {message}")
         self.code = code
+        self.message = message
+
+    def __reduce__(self):  # picklable across the build's worker processes
+        return (SobekError, (self.code, self.message))
 
 
 class Irrep(ctypes.Structure):

@@ -498,7 +498,7 @@ int run_sbar(const Plan& p, const Chunk& c, int64_t s_ncap, const float* M, cons
     if (p.mode == SOBEK_MODE_UVU)
       LAUNCH(p.k.uvu_sbar, cdiv((int64_t)nrows * D, 256), 1, 1, s, M, nrows, D, Cg, W,
              (const int*)(p.d_ktab + g.ktab_off), Sg, dg, off, CX, r0);
-    else if (p.vec4)
+    else if (sbar_streams(p.vec4, g.C))
     {
       // spread the 64-wide column tiles over blockIdx.y until about kSaTarget blocks run,
       // keeping at least four tiles per block
@@ -658,7 +658,7 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   if ((rc = get(p.k.gemm_sbar_v, "sobek_gemm_sbar_v"))) return rc;
   if (p.vec4)
     for (auto& g : p.groups)
-      if (!p.k.gemm_sbar_c.count(g.C)) {
+      if (sbar_streams(p.vec4, g.C) && !p.k.gemm_sbar_c.count(g.C)) {
         std::string nm = "sobek_gemm_sbar_c" + std::to_string(g.C);
         hipFunction_t f = nullptr;
         if ((rc = get(f, nm.c_str()))) return rc;

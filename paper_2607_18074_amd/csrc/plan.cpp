@@ -1042,7 +1042,7 @@ std::string generate_source(const Plan& P) {
   if (P.vec4) {
     std::vector<int> cgs;
     for (auto& g : P.groups)
-      if (std::find(cgs.begin(), cgs.end(), g.C) == cgs.end()) cgs.push_back(g.C);
+      if (sbar_streams(P.vec4, g.C) && std::find(cgs.begin(), cgs.end(), g.C) == cgs.end()) cgs.push_back(g.C);
     for (int C : cgs)
       o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_gemm_sbar_c" << C
         << "(const float* M, int nrows, int D, const float* W, const int* ktab, float* Sbar, int dg, int off, int CX,"

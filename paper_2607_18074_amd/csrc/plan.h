@@ -67,6 +67,11 @@ struct AdjSlab {
   int floats = 0;
 };
 
+// The streaming adjoint-state GEMM stages the C-wide rows of 64 receivers-components in LDS
+// (about 272*C + 17k bytes), so it serves output multiplicities up to 256; wider groups use
+// the tiled sobek_gemm_sbar_64.
+inline bool sbar_streams(bool vec4, int C) { return vec4 && C <= 256; }
+
 struct Kernels {
   hipModule_t module = nullptr;
   hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, fwd_dS_r = nullptr;

@@ -17,6 +17,8 @@ SIGS = {
     "wide": ("128x0e+128x1o+128x2e+64x3o", 3, "128x0e+128x1o+128x2e+64x3o", 16),
     # odd multiplicities, a dead input irrep (0o reaches nothing) and a dead output irrep (3e)
     "odd": ("3x0e+5x1o+2x2e+1x0o", 1, "4x0e+3x1o+2x2e+1x3e", 4),
+    # an output multiplicity above 256: the adjoint-state GEMM takes the tiled kernel
+    "widec": ("320x0e+8x1o", 1, "320x0e+8x1o", 4),
     # channelwise (uvu) signatures: equal multiplicities along every path
     "uvu_small": ("16x0e+16x1o+16x2e", 2, "16x0e+16x1o+16x2e", 8),
     "uvu_l3": ("8x0e+8x1o+8x2e+8x3o", 3, "8x0e+8x1o+8x2e+8x3o", 16),

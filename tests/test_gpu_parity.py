@@ -48,6 +48,7 @@ CASES = [
     ("medium", 120, 1500, 2, 2),
     ("wide", 60, 600, 3, 1),
     ("odd", 50, 700, 4, 2),
+    ("widec", 70, 800, 5, 1),
 ]
 
 
