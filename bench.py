@@ -78,6 +78,16 @@ def flop_model(plan, N, E):
     # fwd: S, m = S A; bwd: Sbar = mbar A^T, A_bar = S^T mbar (S kept by the forward), edge adjoints;
     # dbwd (edge-vector cotangent): dS, m_dot = dS A, g_A = dS^T mbar (Sbar kept by the backward), edge terms
     passes = {"fwd": edge_fwd + gemm, "bwd": 2 * gemm + edge_adj, "dbwd": edge_fwd + 2 * gemm + edge_adj}
+    if getattr(plan, "mode", "uvw") == "uvu":
+        # channelwise: per edge and path the weight w = phi A of each channel (2K C), the CG contraction
+        # (2 nnz C) and the tied-channel product (2 C d_out); the backward adds phi_bar = A h, G = w mbar
+        # and the two transposed contractions; A_bar = S^T mbar is an elementwise reduction (2 flops per
+        # element of S).  The direct forward has no state.
+        NW = plan.n_weights
+        uf = E * (2 * K * NW + 2 * NZ + 2 * SD)
+        ua = E * (4 * K * NW + 6 * NZ + 4 * SD)
+        ug = N * 2 * K * SD
+        passes = {"fwd": uf, "bwd": ua + ug, "dbwd": uf + ua + 2 * ug}
     return dict(SD=SD, NZ=NZ, G=G, per_kernel=per_kernel, passes=passes)
 
 
@@ -219,7 +229,7 @@ def time_graph_passes(plan, W, g, passes, budget, retain):
     return out
 
 
-def tables(which, budget_gib, retain):
+def tables(which, budget_gib, retain, only=()):
     """The paper's capacity-matched grids (Section 5.4, Tables 3 and 4): every profile and pass on B copies
     of the fixed 128-node degree-32 graph, B the paper's graph count for that pass, timed with its protocol;
     the paper's own M edges/s (another GPU) printed beside ours for context."""
@@ -237,6 +247,8 @@ def tables(which, budget_gib, retain):
     rows = []
     for mode, grid in grids:
         for prof, (n_w, Bs, paper) in grid.items():
+            if only and prof not in only:
+                continue
             spec, lmax = wl.profile_irreps(prof)
             plan = api.Plan(spec, lmax, spec, wl.REGIME_K, mode=mode)
             assert plan.n_weights == n_w, (prof, plan.n_weights, n_w)
@@ -387,6 +399,7 @@ def main():
     ap.add_argument("--profiles", default="128/64,128/64/64,128/64/64/64")
     ap.add_argument("--tables", default="", help="'uvw', 'uvu' or 'all': the paper's capacity-matched grids "
                     "(Tables 3 and 4) at its graph counts, one JSON line per profile and pass")
+    ap.add_argument("--table-profiles", default="", help="tables: comma-separated subset of profiles (default all)")
     ap.add_argument("--retain", action="store_true", help="regimes: keep S and Sbar across passes (default: the "
                     "paper's setting, recompute within the workspace budget)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
@@ -408,7 +421,8 @@ def main():
         sys.exit(2)
 
     if args.tables:
-        tables(args.tables, args.budget, args.retain)
+        tables(args.tables, args.budget, args.retain,
+               tuple(p for p in args.table_profiles.split(",") if p))
         return
     if args.regimes:
         kinds = ("degree", "count") if args.regimes == "all" else tuple(args.regimes.split(","))

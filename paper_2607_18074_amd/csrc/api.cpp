@@ -498,7 +498,7 @@ int run_sbar(const Plan& p, const Chunk& c, int64_t s_ncap, const float* M, cons
     if (p.mode == SOBEK_MODE_UVU)
       LAUNCH(p.k.uvu_sbar, cdiv((int64_t)nrows * D, 256), 1, 1, s, M, nrows, D, Cg, W,
              (const int*)(p.d_ktab + g.ktab_off), Sg, dg, off, CX, r0);
-    else if (sbar_streams(p.vec4, g.C))
+    else if (sobek::sbar_streams(p.vec4, g.C))
     {
       // spread the 64-wide column tiles over blockIdx.y until about kSaTarget blocks run,
       // keeping at least four tiles per block
@@ -646,6 +646,7 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
       (rc = get(p.k.uvu_mix, "sobek_uvu_mix")) || (rc = get(p.k.uvu_sbar, "sobek_uvu_sbar")) ||
       (rc = get(p.k.uvu_ga, "sobek_uvu_ga")))
     return rc;
+  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && (rc = get(p.k.uvu_fwd, "sobek_uvu_fwd"))) return rc;
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
                 ga = std::string("sobek_gemm_ga_") + bns[b], sav = std::string("sobek_gemm_sa_v") + bns[b],
@@ -658,7 +659,7 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   if ((rc = get(p.k.gemm_sbar_v, "sobek_gemm_sbar_v"))) return rc;
   if (p.vec4)
     for (auto& g : p.groups)
-      if (sbar_streams(p.vec4, g.C) && !p.k.gemm_sbar_c.count(g.C)) {
+      if (sobek::sbar_streams(p.vec4, g.C) && !p.k.gemm_sbar_c.count(g.C)) {
         std::string nm = "sobek_gemm_sbar_c" + std::to_string(g.C);
         hipFunction_t f = nullptr;
         if ((rc = get(f, nm.c_str()))) return rc;
@@ -914,6 +915,15 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     xk = (const float*)((char*)ws + w.off_x);
     ok = (float*)((char*)ws + w.off_out);
     if ((rc = transpose(p, x, (float*)xk, G.N, true, 0, stream))) return rc;
+  }
+  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && !state) {
+    // channelwise, one multiplicity: every receiver at once, no receiver state
+    int r0 = 0, n = (int)G.N;
+    LAUNCH(p.k.uvu_fwd, cdiv(G.N, 4), cdiv(p.uvu_C, 64), 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec,
+           phi, xk, W, ok, r0, n);
+    if ((rc = zero_dead_out(p, ok, G.N, stream))) return rc;
+    if (mulir && (rc = transpose(p, ok, out, G.N, false, 1, stream))) return rc;
+    return SOBEK_OK;
   }
   float* S = state ? state : state_ptr(w, ws, p, 0);  // a retained state is one chunk of all N receivers
   for (auto& c : w.chunks) {

@@ -111,6 +111,12 @@ void build_plan(Plan& p) {
     }
   }
   p.srow = soff;
+  p.uvu_C = 0;
+  if (p.mode == 1) {
+    int C = p.paths.empty() ? 0 : p.paths[0].c_in;
+    for (auto& q : p.paths) if (q.c_in != C || q.c_out != C) C = 0;
+    p.uvu_C = C;
+  }
   for (auto& q : p.paths) {
     const std::vector<double>& Q = real_cg(q.l_in, q.l_sh, q.l_out);
     q.cg.resize(Q.size());
@@ -1025,6 +1031,79 @@ void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* ind
 
 }  // namespace
 
+// Channelwise (uvu) forward without receiver state, for plans whose paths all have
+// one multiplicity C: with channel u tied through every path (eq. uvu_connection),
+// the edge weight of (path, u) is w = sum_q phi_q A[q, path, u] and the message of
+// channel u is w times the path's CG contraction of channel u alone, so a lane owns
+// one channel of one receiver and accumulates its output components directly
+// (state-free: the receiver state would be K times larger than the output).  Blocks
+// are (4 receivers, 64-channel block); the block's A slice [path][q][channel] is
+// staged in LDS once.  C < 64 puts 64 / C edges in flight per wave (lane = edge
+// slot * C + u), combined by cross-lane adds in a fixed order.
+void emit_uvu_fwd(std::ostringstream& o, const Plan& P) {
+  const int C = P.uvu_C, UB = std::min(C, 64);
+  const int ES = (64 % UB == 0) ? 64 / UB : 1;
+  const int NPt = (int)P.paths.size();
+  const int L = P.lmax, NS = (L + 1) * (L + 1);
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_fwd(const int* __restrict__ rowptr,"
+       " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
+       " const float* __restrict__ x, const float* __restrict__ W, float* __restrict__ out, int r0, int n_recv) {\n"
+    << "  constexpr int C_ = " << C << ", UB_ = " << UB << ", ES_ = " << ES << ";\n"
+    << "  __shared__ float sA[" << NPt * P.K * UB << "];\n"
+    << "  const int cb = blockIdx.y, tid = threadIdx.x, lane = tid & 63;\n";
+  for (int t = 0; t < NPt; ++t)
+    o << "  for (int i = tid; i < K * UB_; i += 256) {\n"
+      << "    const int q = i / UB_, uc = cb * UB_ + i % UB_;\n"
+      << "    sA[" << t * P.K * UB << " + i] = uc < C_ ? W[(sb_i64)q * " << P.n_w << "LL + " << P.paths[t].w_off
+      << "LL + uc] : 0.f;\n  }\n";
+  o << "  __syncthreads();\n"
+       "  const int il = blockIdx.x * 4 + (tid >> 6);\n"
+       "  if (il >= n_recv) return;\n"
+       "  const int sub = lane / UB_, u = lane % UB_, uc = cb * UB_ + u;\n"
+       "  const bool lane_ok = sub < ES_ && uc < C_;\n";
+  for (size_t g = 0; g < P.groups.size(); ++g)
+    o << "  float acc" << g << "[" << P.groups[g].d << "];\n"
+      << "#pragma unroll\n  for (int m = 0; m < " << P.groups[g].d << "; ++m) acc" << g << "[m] = 0.f;\n";
+  o << "  const int beg = rowptr[r0 + il], end = rowptr[r0 + il + 1];\n"
+       "  for (int e = beg + sub; lane_ok && e < end; e += ES_) {\n"
+       "    const int j = sender[e];\n"
+       "    const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
+       "    const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
+       "    float Y[" << NS << "];\n    sb_sh_eval_L" << L << "(vx * rinv, vy * rinv, vz * rinv, Y);\n"
+       "    float ph[K];\n#pragma unroll\n    for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
+       "    const sb_i64 xrow = (sb_i64)j * CXI + uc;\n";
+  std::vector<bool> used(P.in.size(), false);
+  for (auto& q : P.paths) used[q.i_in] = true;
+  for (size_t a = 0; a < P.in.size(); ++a)
+    if (used[a]) {
+      const int d = 2 * P.in[a].l + 1;
+      o << "    float x" << a << "[" << d << "];\n#pragma unroll\n    for (int m = 0; m < " << d << "; ++m) x" << a
+        << "[m] = x[xrow + " << P.in[a].off << " + m * C_];\n";
+    }
+  for (int t = 0; t < NPt; ++t) {
+    const Path& q = P.paths[t];
+    const int dd = 2 * q.l_out + 1;
+    o << "    {\n      float M[P" << t << "_NP], Cc[" << dd << "];\n      sb_M" << t << "(Y + " << q.l_sh * q.l_sh
+      << ", M);\n      sb_C" << t << "(x"
+      << q.i_in << ", M, Cc);\n      float w = 0.f;\n#pragma unroll\n      for (int q = 0; q < K; ++q) w += ph[q] * sA["
+      << t * P.K * UB << " + q * UB_ + u];\n#pragma unroll\n      for (int m = 0; m < " << dd << "; ++m) acc" << q.group
+      << "[m] += w * Cc[m];\n    }\n";
+  }
+  o << "  }\n";
+  if (ES > 1) {
+    o << "#pragma unroll\n  for (int s = UB_; s < 64; s <<= 1) {\n";
+    for (size_t g = 0; g < P.groups.size(); ++g)
+      o << "#pragma unroll\n    for (int m = 0; m < " << P.groups[g].d << "; ++m) acc" << g << "[m] += __shfl_xor(acc" << g
+        << "[m], s);\n";
+    o << "  }\n";
+  }
+  o << "  if (sub == 0 && uc < C_) {\n    const sb_i64 orow = (sb_i64)(r0 + il) * CXO + uc;\n";
+  for (size_t g = 0; g < P.groups.size(); ++g)
+    o << "#pragma unroll\n    for (int m = 0; m < " << P.groups[g].d << "; ++m) out[orow + " << P.groups[g].off
+      << " + m * C_] = acc" << g << "[m];\n";
+  o << "  }\n}\n";
+}
+
 std::string generate_source(const Plan& P) {
   std::ostringstream o;
   o.precision(17);
@@ -1037,6 +1116,7 @@ std::string generate_source(const Plan& P) {
     << "\n#define EB " << P.bwd_eb << "\n#define KP " << P.adj_KP << "\n#define ADJ_W " << P.adj_waves << "\n";
   emit_sh(o, P.lmax);
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
+  if (P.mode == 1 && P.uvu_C > 0) emit_uvu_fwd(o, P);
 
   // streaming adjoint-state GEMM, one instantiation per output multiplicity
   if (P.vec4) {
