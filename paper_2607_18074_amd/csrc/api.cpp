@@ -237,6 +237,14 @@ int sa_nsplit(const sobek::Group& g, int64_t nrows, size_t kfloats, int& kper) {
   return (int)cdiv(g.D, kper);
 }
 
+// floats per edge of the state-free channelwise backward's per-block partial sums
+// (phi_bar and Y_bar of every 64-channel block), kept after the window's contributions
+int64_t uvu_edge_partials(const Plan& p, int pass) {
+  return (pass == SOBEK_PASS_BWD && p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && p.uvu_NB > 1)
+             ? (int64_t)p.uvu_NB * (p.K + p.nsh)
+             : 0;
+}
+
 // fixed part + per-receiver + per-edge bytes of a pass
 void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, int nstate, WsPlan& w, size_t& per_recv,
                 size_t& per_edge) {
@@ -257,7 +265,7 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, int nstate, WsP
   // backward needs a second one for Sbar' when dA is active
   w.nstate = nstate >= 0 ? nstate : (pass == SOBEK_PASS_DBWD ? 2 : 1);
   per_recv = (size_t)w.nstate * p.srow * 4;
-  per_edge = pass == SOBEK_PASS_FWD ? 0 : (size_t)p.dim_in * 4;
+  per_edge = pass == SOBEK_PASS_FWD ? 0 : (size_t)(p.dim_in + uvu_edge_partials(p, pass)) * 4;
 }
 
 size_t layout_total(const Plan& p, WsPlan& w, int pass) {
@@ -268,7 +276,7 @@ size_t layout_total(const Plan& p, WsPlan& w, int pass) {
   w.off_state = o;
   o = align_up(o + (size_t)w.nstate * w.ncap * p.srow * 4);
   w.off_contrib = o;
-  if (pass != SOBEK_PASS_FWD) o = align_up(o + (size_t)w.ecap * p.dim_in * 4);
+  if (pass != SOBEK_PASS_FWD) o = align_up(o + (size_t)w.ecap * (p.dim_in + uvu_edge_partials(p, pass)) * 4);
   return o;
 }
 
@@ -646,7 +654,15 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
       (rc = get(p.k.uvu_mix, "sobek_uvu_mix")) || (rc = get(p.k.uvu_sbar, "sobek_uvu_sbar")) ||
       (rc = get(p.k.uvu_ga, "sobek_uvu_ga")))
     return rc;
-  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && (rc = get(p.k.uvu_fwd, "sobek_uvu_fwd"))) return rc;
+  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0) {
+    if ((rc = get(p.k.uvu_fwd, "sobek_uvu_fwd")) || (rc = get(p.k.uvu_bwd, "sobek_uvu_bwd"))) return rc;
+    if (p.uvu_NB > 1 && (rc = get(p.k.uvu_bwd_fin, "sobek_uvu_bwd_fin"))) return rc;
+    // many paths at high order make the state-free backward spill registers to scratch,
+    // which is slower than the receiver route: take it only when it compiled without
+    int scratch = 0;
+    HIPCHK(hipFuncGetAttribute(&scratch, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd));
+    p.uvu_bwd_direct = scratch == 0;
+  }
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
                 ga = std::string("sobek_gemm_ga_") + bns[b], sav = std::string("sobek_gemm_sa_v") + bns[b],
@@ -953,7 +969,9 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   if (adj_state && !aligned16(adj_state)) return fail(SOBEK_E_ALIGN, "adj_state is not 16-byte aligned");
   WsPlan w;
   // the state slot holds S (weight gradient without a kept state) and Sbar (without a kept adjoint state)
-  const bool need_slot = (gW && !state) || (!adj_state && (gx || gevec || gphi));
+  // (the state-free channelwise edge kernel reads mbar and A directly, no Sbar)
+  const bool uvu_direct = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct;
+  const bool need_slot = (gW && !state) || (!uvu_direct && !adj_state && (gx || gevec || gphi));
   if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false, need_slot ? 1 : 0))) return rc;
   if (gW) { if ((rc = fill_zero(p, gW, (int64_t)p.K * p.n_w, stream))) return rc; }
   if (G.N == 0) return SOBEK_OK;
@@ -985,15 +1003,23 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
       if ((rc = run_ga(p, c, w, ws, S, w.ncap, gk, gW, ci == 0, ci + 1 == w.chunks.size(), stream))) return rc;
     }
     if (edge) {
-      if (!adj_state && (rc = run_sbar(p, c, w.ncap, gk, W, Sb, stream))) return rc;
+      if (!uvu_direct && !adj_state && (rc = run_sbar(p, c, w.ncap, gk, W, Sb, stream))) return rc;
       rc = for_edge_windows(G, c, w, [&](int64_t ea, int64_t eb, int ra, int nr) -> int {
         int e0 = (int)ea, e1 = (int)eb, flags = 0, sub_off = ra - c.r0;
-        long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
-        int sb_r0 = adj_state ? ra : sub_off;
-        LAUNCH_N(p.k.bwd_E, 64 * p.adj_waves, nr, adj_edge_split(p, nr, eb - ea), 1, stream, (const int*)G.rowptr,
-                 (const int*)G.sender, evec, phi, xk, (const float*)(adj_state ? adj_state : Sb), (const float*)nullptr,
-                 (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, gphi, gevec, contrib, ra, nr, ncap,
-                 e0, flags, sb_ncap, sb_r0, e0, e1, sub_off);
+        if (uvu_direct) {
+          float* part = (float*)((char*)ws + w.off_contrib) + (size_t)w.ecap * p.dim_in;
+          LAUNCH(p.k.uvu_bwd, cdiv(nr, 4), p.uvu_NB, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi,
+                 xk, W, gk, gphi, gevec, contrib, part, ra, nr, e0, e0, e1);
+          if (p.uvu_NB > 1 && (gphi || gevec))
+            LAUNCH(p.k.uvu_bwd_fin, cdiv(eb - ea, 256), 1, 1, stream, evec, (const float*)part, gphi, gevec, e0, e1);
+        } else {
+          long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
+          int sb_r0 = adj_state ? ra : sub_off;
+          LAUNCH_N(p.k.bwd_E, 64 * p.adj_waves, nr, adj_edge_split(p, nr, eb - ea), 1, stream, (const int*)G.rowptr,
+                   (const int*)G.sender, evec, phi, xk, (const float*)(adj_state ? adj_state : Sb),
+                   (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, gphi,
+                   gevec, contrib, ra, nr, ncap, e0, flags, sb_ncap, sb_r0, e0, e1, sub_off);
+        }
         const int first = first_win;
         first_win = false;
         return gx ? run_sender_reduce(p, G, ea, eb, w, ws, contrib, gxk, first, stream) : SOBEK_OK;

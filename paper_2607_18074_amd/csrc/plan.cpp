@@ -115,7 +115,10 @@ void build_plan(Plan& p) {
   if (p.mode == 1) {
     int C = p.paths.empty() ? 0 : p.paths[0].c_in;
     for (auto& q : p.paths) if (q.c_in != C || q.c_out != C) C = 0;
+    // the kernels stage A [path][q][64 channels] in LDS: keep it within 96 KB
+    if ((int64_t)p.paths.size() * p.K * std::min(C, 64) * 4 > 96 * 1024) C = 0;
     p.uvu_C = C;
+    p.uvu_NB = C > 0 ? (C + 63) / 64 : 0;
   }
   for (auto& q : p.paths) {
     const std::vector<double>& Q = real_cg(q.l_in, q.l_sh, q.l_out);
@@ -1066,6 +1069,9 @@ void emit_uvu_fwd(std::ostringstream& o, const Plan& P) {
       << "#pragma unroll\n  for (int m = 0; m < " << P.groups[g].d << "; ++m) acc" << g << "[m] = 0.f;\n";
   o << "  const int beg = rowptr[r0 + il], end = rowptr[r0 + il + 1];\n"
        "  for (int e = beg + sub; lane_ok && e < end; e += ES_) {\n"
+       // an opaque copy of the lane's channel offset keeps the A reads inside the loop
+       // (hoisted, they would hold K x paths registers per lane)
+       "    int ul = u;\n    asm volatile(\"\" : \"+v\"(ul));\n"
        "    const int j = sender[e];\n"
        "    const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
        "    const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
@@ -1085,9 +1091,10 @@ void emit_uvu_fwd(std::ostringstream& o, const Plan& P) {
     const int dd = 2 * q.l_out + 1;
     o << "    {\n      float M[P" << t << "_NP], Cc[" << dd << "];\n      sb_M" << t << "(Y + " << q.l_sh * q.l_sh
       << ", M);\n      sb_C" << t << "(x"
-      << q.i_in << ", M, Cc);\n      float w = 0.f;\n#pragma unroll\n      for (int q = 0; q < K; ++q) w += ph[q] * sA["
-      << t * P.K * UB << " + q * UB_ + u];\n#pragma unroll\n      for (int m = 0; m < " << dd << "; ++m) acc" << q.group
-      << "[m] += w * Cc[m];\n    }\n";
+      << q.i_in << ", M, Cc);\n      int ua = ul;\n      asm volatile(\"\" : \"+v\"(ua) :: \"memory\");\n"
+      << "      float w = 0.f;\n#pragma unroll\n      for (int q = 0; q < K; ++q) w += ph[q] * sA["
+      << t * P.K * UB << " + q * UB_ + ua];\n#pragma unroll\n      for (int m = 0; m < " << dd << "; ++m) acc" << q.group
+      << "[m] += w * Cc[m];\n    }\n    __builtin_amdgcn_sched_barrier(0);\n";
   }
   o << "  }\n";
   if (ES > 1) {
@@ -1104,6 +1111,139 @@ void emit_uvu_fwd(std::ostringstream& o, const Plan& P) {
   o << "  }\n}\n";
 }
 
+// Transposed couplings of one path for the channelwise backward:
+// X[m_i] += sum_{m_o} M[(m_i, m_o)] G[m_o]   (x-gradient, M = sum_y c Y_y), and
+// Yb[m_y] += sum_{(m_i, m_o)} c x[m_i] G[m_o] (SH adjoint of the path's slice).
+void emit_path_transposes(std::ostringstream& o, const Plan& P, int t) {
+  const Path& q = P.paths[t];
+  const PathTerms pt = path_terms(q);
+  o << "SB_DEV void sb_XT" << t << "(const float* M, const float* G, float* X) {\n";
+  for (size_t k = 0; k < pt.pairs.size(); ++k)
+    o << "  X[" << pt.pairs[k].first << "] += M[" << k << "]*G[" << pt.pairs[k].second << "];\n";
+  o << "}\nSB_DEV void sb_YT" << t << "(const float* x, const float* G, float* Yb) {\n";
+  for (size_t k = 0; k < pt.pairs.size(); ++k) {
+    o << "  { const float xg = x[" << pt.pairs[k].first << "]*G[" << pt.pairs[k].second << "];";
+    for (const PairTerm& tm : pt.terms[k]) o << " Yb[" << tm.my << "] += " << fl(tm.c) << "*xg;";
+    o << " }\n";
+  }
+  o << "}\n";
+}
+
+// Channelwise (uvu) backward without adjoint state, same plans as the state-free
+// forward: with G = w mbar_i (tied channel), the edge adjoints are
+//   h[path, u] = <mbar_i[u], C_path[u]>,  phi_bar[q] = sum_{path, u} A[q, path, u] h,
+//   x_bar contribution = C^T(G, Y), Y_bar = C^T(x_j, G), evec_bar = J^T Y_bar.
+// A lane owns one channel of one receiver and one edge at a time (64 / C edges in
+// flight below 64 channels); phi_bar and Y_bar are summed over the channels of a
+// lane group by cross-lane adds (fixed order).  With more than 64 channels every
+// 64-channel block writes its partial sums per edge and sobek_uvu_bwd_fin adds them
+// in block order.  Edges are those of the receiver inside [win0, win1); the
+// contribution row of edge e sits at e - e0.
+void emit_uvu_bwd(std::ostringstream& o, const Plan& P) {
+  const int C = P.uvu_C, NB = P.uvu_NB;
+  int UBP = 64;
+  if (C < 64) { UBP = 1; while (UBP < C) UBP <<= 1; }
+  const int ES = 64 / UBP;
+  const int NPt = (int)P.paths.size();
+  const int L = P.lmax, NS = (L + 1) * (L + 1), NV = P.K + NS;
+  for (int t = 0; t < NPt; ++t) emit_path_transposes(o, P, t);
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd(const int* __restrict__ rowptr,"
+       " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
+       " const float* __restrict__ x, const float* __restrict__ W, const float* __restrict__ Mb,"
+       " float* __restrict__ gphi, float* __restrict__ gevec, float* __restrict__ contrib, float* __restrict__ part,"
+       " int r0, int n_recv, int e0, int win0, int win1) {\n"
+    << "  constexpr int C_ = " << C << ", UB_ = " << UBP << ", ES_ = " << ES << ", NB_ = " << NB << ", NV_ = " << NV
+    << ";\n  __shared__ float sA[" << NPt * P.K * UBP << "];\n"
+    << "  const int cb = blockIdx.y, tid = threadIdx.x, lane = tid & 63;\n";
+  for (int t = 0; t < NPt; ++t)
+    o << "  for (int i = tid; i < K * UB_; i += 256) {\n"
+      << "    const int q = i / UB_, uc = cb * UB_ + i % UB_;\n"
+      << "    sA[" << t * P.K * UBP << " + i] = uc < C_ ? W[(sb_i64)q * " << P.n_w << "LL + " << P.paths[t].w_off
+      << "LL + uc] : 0.f;\n  }\n";
+  o << "  __syncthreads();\n"
+       "  const int il = blockIdx.x * 4 + (tid >> 6);\n"
+       "  if (il >= n_recv) return;\n"
+       "  const int sub = lane / UB_, u = lane % UB_, uc = cb * UB_ + u;\n"
+       "  const bool cv = uc < C_;\n"
+       "  const sb_i64 mrow = (sb_i64)(r0 + il) * CXO + uc;\n";
+  for (size_t g = 0; g < P.groups.size(); ++g)
+    o << "  float mb" << g << "[" << P.groups[g].d << "];\n#pragma unroll\n  for (int m = 0; m < " << P.groups[g].d
+      << "; ++m) mb" << g << "[m] = cv ? Mb[mrow + " << P.groups[g].off << " + m * C_] : 0.f;\n";
+  o << "  const int wb = max(rowptr[r0 + il], win0), we = min(rowptr[r0 + il + 1], win1);\n"
+       "  for (int e = wb + sub; e < we; e += ES_) {\n"
+       "    int ul = u;\n    asm volatile(\"\" : \"+v\"(ul));\n"
+       "    const int j = sender[e];\n"
+       "    const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
+       "    const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
+       "    const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
+       "    float Y[" << NS << "], yb[" << NS << "], pb[K];\n    sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
+       "#pragma unroll\n    for (int m = 0; m < " << NS << "; ++m) yb[m] = 0.f;\n"
+       "    float ph[K];\n#pragma unroll\n    for (int q = 0; q < K; ++q) { ph[q] = phi[(sb_i64)e * K + q]; pb[q] = 0.f; }\n"
+       "    const sb_i64 xrow = (sb_i64)j * CXI + uc;\n";
+  std::vector<bool> used(P.in.size(), false);
+  for (auto& q : P.paths) used[q.i_in] = true;
+  for (size_t a = 0; a < P.in.size(); ++a)
+    if (used[a]) {
+      const int d = 2 * P.in[a].l + 1;
+      o << "    float x" << a << "[" << d << "], xb" << a << "[" << d << "];\n#pragma unroll\n    for (int m = 0; m < " << d
+        << "; ++m) { x" << a << "[m] = cv ? x[xrow + " << P.in[a].off << " + m * C_] : 0.f; xb" << a << "[m] = 0.f; }\n";
+    }
+  for (int t = 0; t < NPt; ++t) {
+    const Path& q = P.paths[t];
+    const int dd = 2 * q.l_out + 1;
+    o << "    {\n      float M[P" << t << "_NP], Cc[" << dd << "], G[" << dd << "];\n      sb_M" << t << "(Y + "
+      << q.l_sh * q.l_sh << ", M);\n      sb_C" << t << "(x" << q.i_in << ", M, Cc);\n"
+      << "      int ua = ul;\n      asm volatile(\"\" : \"+v\"(ua) :: \"memory\");\n"
+      << "      const float* At = sA + " << t * P.K * UBP << " + ua;\n      float w = 0.f, h = 0.f;\n"
+      << "#pragma unroll\n      for (int q = 0; q < K; ++q) w += ph[q] * At[q * UB_];\n"
+      << "#pragma unroll\n      for (int m = 0; m < " << dd << "; ++m) { h += mb" << q.group << "[m] * Cc[m]; G[m] = w * mb"
+      << q.group << "[m]; }\n"
+      << "#pragma unroll\n      for (int q = 0; q < K; ++q) pb[q] += At[q * UB_] * h;\n"
+      << "      sb_XT" << t << "(M, G, xb" << q.i_in << ");\n      sb_YT" << t << "(x" << q.i_in << ", G, yb + "
+      << q.l_sh * q.l_sh << ");\n    }\n    __builtin_amdgcn_sched_barrier(0);\n";
+  }
+  // contributions (dead input irreps get zero columns)
+  o << "    if (contrib && cv) {\n      float* cr = contrib + (sb_i64)(e - e0) * CXI + uc;\n";
+  for (size_t a = 0; a < P.in.size(); ++a) {
+    const int d = 2 * P.in[a].l + 1;
+    if (used[a])
+      o << "#pragma unroll\n      for (int m = 0; m < " << d << "; ++m) cr[" << P.in[a].off << " + m * C_] = xb" << a << "[m];\n";
+    else if (P.in[a].mul == C)
+      o << "#pragma unroll\n      for (int m = 0; m < " << d << "; ++m) cr[" << P.in[a].off << " + m * C_] = 0.f;\n";
+  }
+  o << "    }\n";
+  // sums over the lane group's channels
+  o << "#pragma unroll\n    for (int s = 1; s < UB_; s <<= 1) {\n"
+       "#pragma unroll\n      for (int q = 0; q < K; ++q) pb[q] += __shfl_xor(pb[q], s);\n"
+       "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) yb[m] += __shfl_xor(yb[m], s);\n    }\n";
+  if (NB == 1)
+    o << "    if (u == 0) {\n"
+         "      if (gphi) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = pb[q];\n      }\n"
+         "      if (gevec) {\n        float gg[3];\n        sb_sh_vjp(ux, uy, uz, rinv, yb, gg);\n"
+         "        gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n"
+         "      }\n    }\n";
+  else
+    o << "    if (u == 0) {\n      float* pp = part + ((sb_i64)(e - e0) * NB_ + cb) * NV_;\n"
+         "#pragma unroll\n      for (int q = 0; q < K; ++q) pp[q] = pb[q];\n"
+         "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) pp[K + m] = yb[m];\n    }\n";
+  o << "  }\n}\n";
+  if (NB > 1) {
+    o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd_fin(const float* __restrict__ evec,"
+         " const float* __restrict__ part, float* __restrict__ gphi, float* __restrict__ gevec, int e0, int e1) {\n"
+      << "  constexpr int NB_ = " << NB << ", NV_ = " << NV << ";\n"
+      << "  const int e = e0 + blockIdx.x * 256 + threadIdx.x;\n  if (e >= e1) return;\n"
+      << "  const float* pp = part + (sb_i64)(e - e0) * NB_ * NV_;\n"
+      << "  float v[NV_];\n#pragma unroll\n  for (int k = 0; k < NV_; ++k) v[k] = pp[k];\n"
+      << "  for (int b = 1; b < NB_; ++b) {\n#pragma unroll\n    for (int k = 0; k < NV_; ++k) v[k] += pp[b * NV_ + k];\n  }\n"
+      << "  if (gphi) {\n#pragma unroll\n    for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = v[q];\n  }\n"
+      << "  if (gevec) {\n"
+      << "    const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
+      << "    const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
+      << "    float gg[3];\n    sb_sh_vjp(vx * rinv, vy * rinv, vz * rinv, rinv, v + K, gg);\n"
+      << "    gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n  }\n}\n";
+  }
+}
+
 std::string generate_source(const Plan& P) {
   std::ostringstream o;
   o.precision(17);
@@ -1116,7 +1256,10 @@ std::string generate_source(const Plan& P) {
     << "\n#define EB " << P.bwd_eb << "\n#define KP " << P.adj_KP << "\n#define ADJ_W " << P.adj_waves << "\n";
   emit_sh(o, P.lmax);
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
-  if (P.mode == 1 && P.uvu_C > 0) emit_uvu_fwd(o, P);
+  if (P.mode == 1 && P.uvu_C > 0) {
+    emit_uvu_fwd(o, P);
+    emit_uvu_bwd(o, P);
+  }
 
   // streaming adjoint-state GEMM, one instantiation per output multiplicity
   if (P.vec4) {

@@ -82,7 +82,7 @@ struct Kernels {
   hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
                 zero = nullptr, sa_reduce = nullptr;
   hipFunction_t uvu_mix = nullptr, uvu_sbar = nullptr, uvu_ga = nullptr;  // channelwise mixing
-  hipFunction_t uvu_fwd = nullptr;  // channelwise direct forward
+  hipFunction_t uvu_fwd = nullptr, uvu_bwd = nullptr, uvu_bwd_fin = nullptr;  // channelwise state-free kernels
 };
 
 struct Plan {
@@ -103,7 +103,9 @@ struct Plan {
   int bwd_eb = 64;              // edges per batch when the adjoint state needs several slabs
   int bwd_lds_max = 0;          // largest slab (floats)
   bool vec4 = false;            // every multiplicity a multiple of 4: vectorised GEMMs apply
-  int uvu_C = 0;                // uvu with one multiplicity C on every path: the direct forward applies
+  int uvu_C = 0;                // uvu with one multiplicity C on every path: the state-free kernels apply
+  int uvu_NB = 0;               // 64-channel blocks of C (the state-free backward's per-edge partial count)
+  bool uvu_bwd_direct = false;  // the state-free backward compiled without register spills (set at load)
   std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
   std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)
   std::string source;           // generated HIP source
