@@ -278,3 +278,32 @@ def test_kept_states_chunk_by_edges_only(gpu):
     ref = oc.bwd(*oracle_args(case, prob), case["gout"])
     for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
         assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
+
+
+def test_windows_split_high_degree_receivers(gpu):
+    """A budget whose edge windows are shorter than a receiver's in-degree: receivers are split across
+    windows, and inside a window their edges are spread over blockIdx.y; backward and double backward
+    still match the oracle."""
+    from paper_2607_18074_amd import _lib
+    case = make_case("small", 40, 8000, 16)        # mean in-degree 200
+    api, plan, graph, prob = setup(case)
+    g = case["graph"]
+    args = (_t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]))
+    budget = 3 << 19                                  # 1.5 MiB: windows of a few hundred edges
+    _lib.profile_reset()
+    _lib.profile_enable(True)
+    outs = api.conv_bwd(plan, graph, *args, _t(case["gout"]), budget=budget)
+    prof = _lib.profile_read()
+    _lib.profile_enable(False)
+    print("bwd_E launches", prof["sobek_bwd_E"][0], "receivers", g.N, "edges", g.E)
+    assert prof["sobek_bwd_E"][0] >= 4
+    ref = oc.bwd(*oracle_args(case, prob), case["gout"])
+    for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
+        assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
+    cot = case["cot"]
+    dref = oc.dbwd(*oracle_args(case, prob), case["gout"], t_gx=cot["x"], t_gevec=cot["evec"], t_gphi=cot["phi"],
+                   t_gW=cot["W"])
+    outs = api.conv_dbwd(plan, graph, *args, _t(case["gout"]), _t(cot["x"]), _t(cot["evec"]), _t(cot["phi"]),
+                         _t(cot["W"]), budget=budget)
+    for name, o in zip(("g_gout", "g_x", "g_evec", "g_phi", "g_W"), outs):
+        assert max_rel(_n(o), dref[name]) <= BWD_TOL, name
