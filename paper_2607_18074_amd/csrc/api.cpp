@@ -218,7 +218,7 @@ constexpr int kSaTarget = 512, kSaMaxSplit = 16;
 constexpr size_t kSaSplitCap = (size_t)4 << 20;
 
 size_t sa_split_floats(const Plan& p, int pass, int64_t ncap) {
-  if (pass == SOBEK_PASS_BWD || !p.vec4) return 0;
+  if (pass == SOBEK_PASS_BWD || !p.vec4 || p.mode == SOBEK_MODE_UVU) return 0;
   size_t m = 0;
   for (auto& g : p.groups) m = std::max(m, (size_t)g.d * g.C);
   return std::min(kSaSplitCap, (size_t)kSaMaxSplit * (size_t)std::max<int64_t>(1, ncap) * m);
@@ -264,6 +264,8 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, int nstate, WsP
   // receiver-state slots: one, reused phase by phase (S, then Sbar); the double
   // backward needs a second one for Sbar' when dA is active
   w.nstate = nstate >= 0 ? nstate : (pass == SOBEK_PASS_DBWD ? 2 : 1);
+  // the state-free channelwise forward keeps no receiver state (a kept one is the caller's)
+  if (pass == SOBEK_PASS_FWD && p.mode == SOBEK_MODE_UVU && p.uvu_C > 0) w.nstate = 0;
   per_recv = (size_t)w.nstate * p.srow * 4;
   per_edge = pass == SOBEK_PASS_FWD ? 0 : (size_t)(p.dim_in + uvu_edge_partials(p, pass)) * 4;
 }
