@@ -594,10 +594,12 @@ int for_edge_windows(const sobek_graph_s& G, const Chunk& c, const WsPlan& w, F&
 }
 
 // blockIdx.y split of the adjoint edge kernels: spread the window's receivers' edges
-// until about 512 blocks run, at least 16 edges per wave of a block
+// until about 512 blocks run, at least one 16-edge batch per block (with few receivers a
+// block's staged slabs are latency-bound, so shorter edge shares run in parallel)
 int adj_edge_split(const Plan& p, int nr, int64_t ne) {
-  const int64_t per_block = 16 * p.adj_waves;
-  const int64_t by_work = std::max<int64_t>(1, ne / std::max(1, nr) / per_block);
+  (void)p;
+  const int64_t per_block = 16;
+  const int64_t by_work = std::max<int64_t>(1, (ne / std::max(1, nr) + per_block - 1) / per_block);
   return (int)std::max<int64_t>(1, std::min<int64_t>({cdiv(512, std::max(1, nr)), by_work, 64}));
 }
 

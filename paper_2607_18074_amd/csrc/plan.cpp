@@ -1322,9 +1322,9 @@ std::string generate_source(const Plan& P) {
        "  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;\n"
        "  const int fl = FL >= 0 ? FL : flags;\n"
        // the receiver's edges inside the launch's edge window [win0, win1), split evenly over
-       // blockIdx.y in whole 16-edge batches of every wave (edge outputs need no reduction)
+       // blockIdx.y in whole 16-edge batches (edge outputs need no reduction)
        "  const int wb = max(rowptr[r0 + il], win0), we = min(rowptr[r0 + il + 1], win1);\n"
-       "  const int span = ((we - wb + (int)gridDim.y - 1) / (int)gridDim.y + 16 * ADJ_W - 1) / (16 * ADJ_W) * (16 * ADJ_W);\n"
+       "  const int span = ((we - wb + (int)gridDim.y - 1) / (int)gridDim.y + 15) / 16 * 16;\n"
        "  const int beg = wb + (int)blockIdx.y * span, end = min(we, beg + span);\n"
        "  if (beg >= end) return;\n";
   if (NSL == 1) {
