@@ -95,6 +95,9 @@ int sobek_version(void);
  *         C_out = C_in (else SOBEK_E_INVALID) and owns C_in weights,
  *         W[q][w_off + u], output channel u = input channel u.
  *   layout: SOBEK_LAYOUT_*.  dtype: SOBEK_DTYPE_F32.
+ *   (uvu plans whose paths share one multiplicity run a forward and backward
+ *   without receiver state; the environment variable SOBEK_UVU_ROUTE=receiver,
+ *   read at plan creation, keeps them on the receiver-state route instead.)
  *   path_norm: SOBEK_NORM_NONE (alpha = 1) or SOBEK_NORM_FAN_IN
  *   (alpha = 1/sqrt(fan_in), fan_in = number of terms summed into one output
  *   channel: the sum of C_in over the paths into the same output irrep for

@@ -22,6 +22,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -161,6 +162,10 @@ int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep
     return fail(SOBEK_E_UNSUPPORTED, "plan: %s", ex.what());
   }
   if (p.paths.empty()) return fail(SOBEK_E_INVALID, "no path satisfies the selection rules");
+  // SOBEK_UVU_ROUTE=receiver keeps channelwise plans on the receiver-state route (testing and
+  // comparison); the state-free kernels are then not generated
+  if (const char* r = std::getenv("SOBEK_UVU_ROUTE"))
+    if (std::strcmp(r, "receiver") == 0) { p.uvu_C = 0; p.uvu_NB = 0; }
   int64_t maxD = 0;
   for (auto& g : p.groups) maxD = std::max(maxD, g.D);
   if (p.n_w * (int64_t)K >= (1ll << 31) || maxD >= (1ll << 31))

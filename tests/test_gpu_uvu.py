@@ -122,3 +122,19 @@ def test_uvu_autograd(gpu):
     dref = oc.dbwd(*oargs(case, prob), case["gout"], t_gevec=case["cot"]["evec"])
     for name, o in zip(("g_x", "g_evec", "g_phi", "g_W"), h):
         assert max_rel(_n(o), dref[name]) <= BWD_TOL, name
+
+
+def test_uvu_receiver_route(gpu, monkeypatch):
+    """The receiver-state route of channelwise plans (taken when the state-free kernels do not apply),
+    forced with SOBEK_UVU_ROUTE=receiver: forward and backward against the oracle."""
+    monkeypatch.setenv("SOBEK_UVU_ROUTE", "receiver")
+    case = make_case("uvu_small", 120, 1500, 27, isolated=1, mode="uvu")
+    api, plan, graph, prob = setup(case)
+    g = case["graph"]
+    args = (_t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]))
+    assert max_rel(_n(api.conv_fwd(plan, graph, *args)), oc.fwd(*oargs(case, prob))) <= FWD_TOL
+    ref = oc.bwd(*oargs(case, prob), case["gout"])
+    for budget in (0, 1 << 20):
+        outs = api.conv_bwd(plan, graph, *args, _t(case["gout"]), budget=budget)
+        for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
+            assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
