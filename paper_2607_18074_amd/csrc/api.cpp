@@ -208,7 +208,10 @@ int nsplit_for(const sobek::Group& g, int64_t nrows, bool vec4) {
 
 // split partials of the weight-gradient GEMMs: one region per output group,
 // accumulated over the receiver chunks of a pass and reduced once at its end
-size_t partial_floats(const Plan& p, int64_t ncap) {
+size_t partial_floats(const Plan& p, int64_t ncap, int pass = SOBEK_PASS_BWD) {
+  // the state-free channelwise weight gradient: one partial row of K * N_w floats per wave
+  if (pass == SOBEK_PASS_BWD && p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && p.uvu_wgrad_direct)
+    return (size_t)sobek::kUvuWaves * p.K * p.n_w;
   size_t m = 0;
   for (auto& g : p.groups) m += (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C;
   return m;
@@ -277,7 +280,7 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, int nstate, WsP
 
 size_t layout_total(const Plan& p, WsPlan& w, int pass) {
   size_t o = w.fixed;
-  if (pass != SOBEK_PASS_FWD) o = align_up(o + partial_floats(p, w.ncap) * 4);
+  if (pass != SOBEK_PASS_FWD) o = align_up(o + partial_floats(p, w.ncap, pass) * 4);
   w.off_K = o;  // w.kfloats is set by the planner
   o = align_up(o + w.kfloats * 4);
   w.off_state = o;
@@ -318,7 +321,7 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
     // GEMM partials (weight-gradient splits, state-GEMM split-K) of chunks of nc receivers
     auto partial_bytes = [&](int64_t nc) -> size_t {
       nc = std::max<int64_t>(1, nc);
-      return (pass != SOBEK_PASS_FWD ? align_up(partial_floats(p, nc) * 4) + kAlign : 0) +
+      return (pass != SOBEK_PASS_FWD ? align_up(partial_floats(p, nc, pass) * 4) + kAlign : 0) +
              align_up(sa_split_floats(p, pass, nc) * 4) + kAlign;
     };
     auto total_at = [&](int64_t nc, int64_t ec, size_t kf) {
@@ -666,11 +669,14 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0) {
     if ((rc = get(p.k.uvu_fwd, "sobek_uvu_fwd")) || (rc = get(p.k.uvu_bwd, "sobek_uvu_bwd"))) return rc;
     if (p.uvu_NB > 1 && (rc = get(p.k.uvu_bwd_fin, "sobek_uvu_bwd_fin"))) return rc;
+    if ((rc = get(p.k.uvu_wgrad, "sobek_uvu_wgrad")) || (rc = get(p.k.uvu_wreduce, "sobek_uvu_wreduce"))) return rc;
     // many paths at high order make the state-free backward spill registers to scratch,
     // which is slower than the receiver route: take it only when it compiled without
-    int scratch = 0;
+    int scratch = 0, scratch_w = 0;
     HIPCHK(hipFuncGetAttribute(&scratch, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd));
+    HIPCHK(hipFuncGetAttribute(&scratch_w, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad));
     p.uvu_bwd_direct = scratch == 0;
+    p.uvu_wgrad_direct = scratch_w == 0;
   }
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
@@ -980,7 +986,9 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   // the state slot holds S (weight gradient without a kept state) and Sbar (without a kept adjoint state)
   // (the state-free channelwise edge kernel reads mbar and A directly, no Sbar)
   const bool uvu_direct = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct;
-  const bool need_slot = (gW && !state) || (!uvu_direct && !adj_state && (gx || gevec || gphi));
+  // with it, A_bar comes from the edges directly (no receiver state; a kept S is not needed)
+  const bool uvu_wg = uvu_direct && p.uvu_wgrad_direct;
+  const bool need_slot = (gW && !state && !uvu_wg) || (!uvu_direct && !adj_state && (gx || gevec || gphi));
   if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false, need_slot ? 1 : 0))) return rc;
   if (gW) { if ((rc = fill_zero(p, gW, (int64_t)p.K * p.n_w, stream))) return rc; }
   if (G.N == 0) return SOBEK_OK;
@@ -1000,14 +1008,26 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   float* contrib = gx ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = gx || gevec || gphi;
   const Chunk all{0, (int)G.N, 0, G.E};
-  if (gW && state) {
+  if (gW && state && !uvu_wg) {
     if ((rc = run_ga(p, all, w, ws, state, G.N, gk, gW, true, true, stream))) return rc;
+  }
+  if (gW && uvu_wg) {
+    int na = 0, n = (int)G.N;
+    for (size_t a = 0; a < p.in.size(); ++a)
+      for (auto& q : p.paths)
+        if (q.i_in == (int)a) { ++na; break; }
+    float* P = (float*)((char*)ws + w.off_P);
+    int rows = sobek::kUvuWaves;
+    long long nw = (long long)p.K * p.n_w;
+    LAUNCH(p.k.uvu_wgrad, sobek::kUvuWaves / 4, p.uvu_NB, na, stream, (const int*)G.rowptr, (const int*)G.sender,
+           evec, phi, xk, gk, P, n);
+    LAUNCH(p.k.uvu_wreduce, cdiv(nw, 256), 1, 1, stream, (const float*)P, rows, nw, gW);
   }
   if (adj_state && (rc = run_sbar(p, all, G.N, gk, W, adj_state, stream))) return rc;
   bool first_win = true;  // the first edge window overall initialises the sender cursors and x-gradient rows
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
-    if (gW && !state) {
+    if (gW && !state && !uvu_wg) {
       if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
       if ((rc = run_ga(p, c, w, ws, S, w.ncap, gk, gW, ci == 0, ci + 1 == w.chunks.size(), stream))) return rc;
     }

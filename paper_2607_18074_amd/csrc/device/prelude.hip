@@ -635,6 +635,24 @@ extern "C" __global__ __launch_bounds__(256) void sobek_uvu_ga(const float* __re
   *o = accumulate ? (*o + acc) : acc;
 }
 
+// gW[i] = sum over rows r < nrows of part[r][i], i < n, rows added in order
+extern "C" __global__ __launch_bounds__(256) void sobek_uvu_wreduce(const float* __restrict__ part, int nrows,
+                                                                    sb_i64 n, float* __restrict__ gW) {
+  const sb_i64 i = (sb_i64)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  int r = 0;
+  for (; r + 8 <= nrows; r += 8) {  // eight loads in flight, added in row order
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = part[(sb_i64)(r + k) * n + i];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += v[k];
+  }
+  for (; r < nrows; ++r) s += part[(sb_i64)r * n + i];
+  gW[i] = s;
+}
+
 // gW[ktab[k] + w] = (first ? 0 : gW[..]) + sum_{s < nsplit} P[s, k, w]   (fixed split order)
 extern "C" __global__ __launch_bounds__(256) void sobek_ga_reduce(const float* P, int nsplit, int D, int Cg,
                                                                   const int* ktab, float* gW, int first) {

@@ -1244,6 +1244,81 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P) {
   }
 }
 
+// Channelwise weight gradient without receiver state: A_bar[q, path, u] is the sum
+// over all edges of phi_e[q] h_e[path, u], h = <mbar_i[u], C_path[u]> (tied channel).
+// Grid (UVU_WAVES / 4, 64-channel blocks, input irreps with paths): wave w of the
+// slice (input irrep a, channel block) takes receivers w, w + UVU_WAVES, ... and
+// keeps K accumulators per path of a and channel in registers; each wave writes
+// its own partial row part[w][q * N_w + w_off + u], which sobek_uvu_wreduce adds
+// in wave order.
+void emit_uvu_wgrad(std::ostringstream& o, const Plan& P) {
+  const int C = P.uvu_C;
+  int UBP = 64;
+  if (C < 64) { UBP = 1; while (UBP < C) UBP <<= 1; }
+  const int ES = 64 / UBP;
+  const int L = P.lmax, NS = (L + 1) * (L + 1);
+  std::vector<int> ins;
+  for (size_t a = 0; a < P.in.size(); ++a)
+    for (auto& q : P.paths)
+      if (q.i_in == (int)a) { ins.push_back((int)a); break; }
+  o << "#define UVU_WAVES " << kUvuWaves << "\n"
+    << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_wgrad(const int* __restrict__ rowptr,"
+       " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
+       " const float* __restrict__ x, const float* __restrict__ Mb, float* __restrict__ part, int n_recv) {\n"
+    << "  constexpr int C_ = " << C << ", UB_ = " << UBP << ", ES_ = " << ES << ";\n"
+    << "  const int cb = blockIdx.y, lane = threadIdx.x & 63, wv = blockIdx.x * 4 + (threadIdx.x >> 6);\n"
+    << "  const int sub = lane / UB_, u = lane % UB_, uc = cb * UB_ + u;\n"
+    << "  const bool cv = uc < C_;\n"
+    << "  float* prow = part + (sb_i64)wv * " << (int64_t)P.K * P.n_w << "LL;\n"
+    << "  switch (blockIdx.z) {\n";
+  for (size_t ia = 0; ia < ins.size(); ++ia) {
+    const int a = ins[ia];
+    const int d = 2 * P.in[a].l + 1;
+    std::vector<int> ts, gs;
+    for (int t = 0; t < (int)P.paths.size(); ++t)
+      if (P.paths[t].i_in == a) {
+        ts.push_back(t);
+        if (std::find(gs.begin(), gs.end(), P.paths[t].group) == gs.end()) gs.push_back(P.paths[t].group);
+      }
+    o << "  case " << ia << ": {\n";
+    for (int t : ts) o << "    float acc" << t << "[K];\n#pragma unroll\n    for (int q = 0; q < K; ++q) acc" << t << "[q] = 0.f;\n";
+    o << "    for (int r = wv; r < n_recv; r += UVU_WAVES) {\n"
+         "      const sb_i64 mrow = (sb_i64)r * CXO + uc;\n";
+    for (int g : gs)
+      o << "      float mb" << g << "[" << P.groups[g].d << "];\n#pragma unroll\n      for (int m = 0; m < "
+        << P.groups[g].d << "; ++m) mb" << g << "[m] = cv ? Mb[mrow + " << P.groups[g].off << " + m * C_] : 0.f;\n";
+    o << "      const int beg = rowptr[r], end = rowptr[r + 1];\n"
+         "      for (int e = beg + sub; e < end; e += ES_) {\n"
+         "        const int j = sender[e];\n"
+         "        const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
+         "        const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
+         "        float Y[" << NS << "];\n        sb_sh_eval_L" << L << "(vx * rinv, vy * rinv, vz * rinv, Y);\n"
+         "        float ph[K];\n#pragma unroll\n        for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
+         "        float xa[" << d << "];\n#pragma unroll\n        for (int m = 0; m < " << d << "; ++m) xa[m] = cv ? x[(sb_i64)j * CXI + "
+      << P.in[a].off << " + m * C_ + uc] : 0.f;\n";
+    for (int t : ts) {
+      const Path& q = P.paths[t];
+      const int dd = 2 * q.l_out + 1;
+      o << "        {\n          float M[P" << t << "_NP], Cc[" << dd << "];\n          sb_M" << t << "(Y + " << q.l_sh * q.l_sh
+        << ", M);\n          sb_C" << t << "(xa, M, Cc);\n          float h = 0.f;\n#pragma unroll\n          for (int m = 0; m < "
+        << dd << "; ++m) h += mb" << q.group << "[m] * Cc[m];\n#pragma unroll\n          for (int q = 0; q < K; ++q) acc" << t
+        << "[q] += ph[q] * h;\n        }\n";
+    }
+    o << "      }\n    }\n";
+    if (ES > 1) {
+      o << "#pragma unroll\n    for (int s = UB_; s < 64; s <<= 1) {\n";
+      for (int t : ts) o << "#pragma unroll\n      for (int q = 0; q < K; ++q) acc" << t << "[q] += __shfl_xor(acc" << t << "[q], s);\n";
+      o << "    }\n";
+    }
+    o << "    if (sub == 0 && cv) {\n";
+    for (int t : ts)
+      o << "#pragma unroll\n      for (int q = 0; q < K; ++q) prow[(sb_i64)q * " << P.n_w << "LL + " << P.paths[t].w_off
+        << "LL + uc] = acc" << t << "[q];\n";
+    o << "    }\n    break;\n  }\n";
+  }
+  o << "  }\n}\n";
+}
+
 std::string generate_source(const Plan& P) {
   std::ostringstream o;
   o.precision(17);
@@ -1259,6 +1334,7 @@ std::string generate_source(const Plan& P) {
   if (P.mode == 1 && P.uvu_C > 0) {
     emit_uvu_fwd(o, P);
     emit_uvu_bwd(o, P);
+    emit_uvu_wgrad(o, P);
   }
 
   // streaming adjoint-state GEMM, one instantiation per output multiplicity

@@ -72,6 +72,9 @@ struct AdjSlab {
 // the tiled sobek_gemm_sbar_64.
 inline bool sbar_streams(bool vec4, int C) { return vec4 && C <= 256; }
 
+// waves (partial rows) per slice of the state-free channelwise weight gradient
+constexpr int kUvuWaves = 256;
+
 struct Kernels {
   hipModule_t module = nullptr;
   hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, fwd_dS_r = nullptr;
@@ -83,6 +86,7 @@ struct Kernels {
                 zero = nullptr, sa_reduce = nullptr;
   hipFunction_t uvu_mix = nullptr, uvu_sbar = nullptr, uvu_ga = nullptr;  // channelwise mixing
   hipFunction_t uvu_fwd = nullptr, uvu_bwd = nullptr, uvu_bwd_fin = nullptr;  // channelwise state-free kernels
+  hipFunction_t uvu_wgrad = nullptr, uvu_wreduce = nullptr;
 };
 
 struct Plan {
@@ -106,6 +110,7 @@ struct Plan {
   int uvu_C = 0;                // uvu with one multiplicity C on every path: the state-free kernels apply
   int uvu_NB = 0;               // 64-channel blocks of C (the state-free backward's per-edge partial count)
   bool uvu_bwd_direct = false;  // the state-free backward compiled without register spills (set at load)
+  bool uvu_wgrad_direct = false;  // likewise the state-free weight gradient
   std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
   std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)
   std::string source;           // generated HIP source
