@@ -248,8 +248,9 @@ int sa_nsplit(const sobek::Group& g, int64_t nrows, size_t kfloats, int& kper) {
 // floats per edge of the state-free channelwise backward's per-block partial sums
 // (phi_bar and Y_bar of every 64-channel block), kept after the window's contributions
 int64_t uvu_edge_partials(const Plan& p, int pass) {
-  return (pass == SOBEK_PASS_BWD && p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && p.uvu_NB > 1)
-             ? (int64_t)p.uvu_NB * (p.K + p.nsh)
+  const int64_t npart = (int64_t)p.uvu_NB * (p.uvu_sliced ? p.uvu_NA : 1);
+  return (pass == SOBEK_PASS_BWD && p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && npart > 1)
+             ? npart * (p.K + p.nsh)
              : 0;
 }
 
@@ -667,16 +668,28 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
       (rc = get(p.k.uvu_ga, "sobek_uvu_ga")))
     return rc;
   if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0) {
-    if ((rc = get(p.k.uvu_fwd, "sobek_uvu_fwd")) || (rc = get(p.k.uvu_bwd, "sobek_uvu_bwd"))) return rc;
-    if (p.uvu_NB > 1 && (rc = get(p.k.uvu_bwd_fin, "sobek_uvu_bwd_fin"))) return rc;
+    hipFunction_t bu = nullptr, bs = nullptr;
+    if ((rc = get(p.k.uvu_fwd, "sobek_uvu_fwd")) || (rc = get(bu, "sobek_uvu_bwd_u")) ||
+        (rc = get(bs, "sobek_uvu_bwd_s")))
+      return rc;
     if ((rc = get(p.k.uvu_wgrad, "sobek_uvu_wgrad")) || (rc = get(p.k.uvu_wreduce, "sobek_uvu_wreduce"))) return rc;
     // many paths at high order make the state-free backward spill registers to scratch,
-    // which is slower than the receiver route: take it only when it compiled without
-    int scratch = 0, scratch_w = 0;
-    HIPCHK(hipFuncGetAttribute(&scratch, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd));
-    HIPCHK(hipFuncGetAttribute(&scratch_w, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad));
-    p.uvu_bwd_direct = scratch == 0;
-    p.uvu_wgrad_direct = scratch_w == 0;
+    // which is slower than the receiver route: take the all-irrep form when it compiled
+    // without spills and below the 256-register cap (two waves per SIMD), else the
+    // per-input-irrep form, else the receiver route
+    int su = 0, ss = 0, sw = 0, ru = 0;
+    HIPCHK(hipFuncGetAttribute(&su, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, bu));
+    HIPCHK(hipFuncGetAttribute(&ss, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, bs));
+    HIPCHK(hipFuncGetAttribute(&sw, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad));
+    HIPCHK(hipFuncGetAttribute(&ru, HIP_FUNC_ATTRIBUTE_NUM_REGS, bu));
+    p.uvu_bwd_direct = su == 0 || ss == 0;
+    p.uvu_sliced = su != 0 || (ru >= 256 && ss == 0);
+    p.k.uvu_bwd = p.uvu_sliced ? bs : bu;
+    const int npart = p.uvu_NB * (p.uvu_sliced ? p.uvu_NA : 1);
+    if (p.uvu_bwd_direct && npart > 1 &&
+        (rc = get(p.k.uvu_bwd_fin, p.uvu_sliced ? "sobek_uvu_bwd_fin_s" : "sobek_uvu_bwd_fin_u")))
+      return rc;
+    p.uvu_wgrad_direct = sw == 0;
   }
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
@@ -1037,9 +1050,10 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
         int e0 = (int)ea, e1 = (int)eb, flags = 0, sub_off = ra - c.r0;
         if (uvu_direct) {
           float* part = (float*)((char*)ws + w.off_contrib) + (size_t)w.ecap * p.dim_in;
-          LAUNCH(p.k.uvu_bwd, cdiv(nr, 4), p.uvu_NB, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi,
-                 xk, W, gk, gphi, gevec, contrib, part, ra, nr, e0, e0, e1);
-          if (p.uvu_NB > 1 && (gphi || gevec))
+          const int ns = p.uvu_sliced ? p.uvu_NA : 1;
+          LAUNCH(p.k.uvu_bwd, cdiv(nr, 4), p.uvu_NB, ns, stream, (const int*)G.rowptr, (const int*)G.sender, evec,
+                 phi, xk, W, gk, gphi, gevec, contrib, part, ra, nr, e0, e0, e1);
+          if (p.uvu_NB * ns > 1 && (gphi || gevec))
             LAUNCH(p.k.uvu_bwd_fin, cdiv(eb - ea, 256), 1, 1, stream, evec, (const float*)part, gphi, gevec, e0, e1);
         } else {
           long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;

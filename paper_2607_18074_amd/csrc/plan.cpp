@@ -119,6 +119,10 @@ void build_plan(Plan& p) {
     if ((int64_t)p.paths.size() * p.K * std::min(C, 64) * 4 > 96 * 1024) C = 0;
     p.uvu_C = C;
     p.uvu_NB = C > 0 ? (C + 63) / 64 : 0;
+    p.uvu_NA = 0;
+    for (size_t a = 0; a < p.in.size(); ++a)
+      for (auto& q : p.paths)
+        if (q.i_in == (int)a) { ++p.uvu_NA; break; }
   }
   for (auto& q : p.paths) {
     const std::vector<double>& Q = real_cg(q.l_in, q.l_sh, q.l_out);
@@ -1134,107 +1138,138 @@ void emit_path_transposes(std::ostringstream& o, const Plan& P, int t) {
 //   h[path, u] = <mbar_i[u], C_path[u]>,  phi_bar[q] = sum_{path, u} A[q, path, u] h,
 //   x_bar contribution = C^T(G, Y), Y_bar = C^T(x_j, G), evec_bar = J^T Y_bar.
 // A lane owns one channel of one receiver and one edge at a time (64 / C edges in
-// flight below 64 channels); phi_bar and Y_bar are summed over the channels of a
-// lane group by cross-lane adds (fixed order).  With more than 64 channels every
-// 64-channel block writes its partial sums per edge and sobek_uvu_bwd_fin adds them
-// in block order.  Edges are those of the receiver inside [win0, win1); the
+// flight below 64 channels).  Slices (blockIdx.z, blockIdx.y = 64-channel block) hold
+// all input irreps (suffix _u) or one input irrep each (suffix _s, fewer registers for
+// plans with many paths, at one more pass over the edges per irrep): each slice
+// writes its own columns of the x-gradient contribution rows, and its phi_bar and
+// Y_bar summed over the lane group's channels (fixed order); with one slice they are
+// final, else each slice writes per-edge partials that sobek_uvu_bwd_fin adds in
+// slice order.  Edges are those of the receiver inside [win0, win1); the
 // contribution row of edge e sits at e - e0.
-void emit_uvu_bwd(std::ostringstream& o, const Plan& P) {
+void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
   const int C = P.uvu_C, NB = P.uvu_NB;
+  const char* sfx = sliced ? "_s" : "_u";
   int UBP = 64;
   if (C < 64) { UBP = 1; while (UBP < C) UBP <<= 1; }
   const int ES = 64 / UBP;
   const int NPt = (int)P.paths.size();
   const int L = P.lmax, NS = (L + 1) * (L + 1), NV = P.K + NS;
-  for (int t = 0; t < NPt; ++t) emit_path_transposes(o, P, t);
-  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd(const int* __restrict__ rowptr,"
+  std::vector<int> ins;
+  std::vector<bool> used(P.in.size(), false);
+  for (auto& q : P.paths) used[q.i_in] = true;
+  for (size_t a = 0; a < P.in.size(); ++a)
+    if (used[a]) ins.push_back((int)a);
+  // slices: one input irrep each (sliced), or all of them in one (unsliced)
+  std::vector<std::vector<int>> slices;
+  if (sliced) for (int a : ins) slices.push_back({a});
+  else slices.push_back(ins);
+  const int NA = (int)slices.size(), NPART = NA * NB;
+  int maxp = 1;
+  for (auto& sl : slices) {
+    int n = 0;
+    for (auto& q : P.paths) n += std::find(sl.begin(), sl.end(), q.i_in) != sl.end();
+    maxp = std::max(maxp, n);
+  }
+  if (!sliced)
+    for (int t = 0; t < NPt; ++t) emit_path_transposes(o, P, t);
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd" << sfx << "(const int* __restrict__ rowptr,"
        " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
        " const float* __restrict__ x, const float* __restrict__ W, const float* __restrict__ Mb,"
        " float* __restrict__ gphi, float* __restrict__ gevec, float* __restrict__ contrib, float* __restrict__ part,"
        " int r0, int n_recv, int e0, int win0, int win1) {\n"
     << "  constexpr int C_ = " << C << ", UB_ = " << UBP << ", ES_ = " << ES << ", NB_ = " << NB << ", NV_ = " << NV
-    << ";\n  __shared__ float sA[" << NPt * P.K * UBP << "];\n"
-    << "  const int cb = blockIdx.y, tid = threadIdx.x, lane = tid & 63;\n";
-  for (int t = 0; t < NPt; ++t)
-    o << "  for (int i = tid; i < K * UB_; i += 256) {\n"
-      << "    const int q = i / UB_, uc = cb * UB_ + i % UB_;\n"
-      << "    sA[" << t * P.K * UBP << " + i] = uc < C_ ? W[(sb_i64)q * " << P.n_w << "LL + " << P.paths[t].w_off
-      << "LL + uc] : 0.f;\n  }\n";
-  o << "  __syncthreads();\n"
-       "  const int il = blockIdx.x * 4 + (tid >> 6);\n"
-       "  if (il >= n_recv) return;\n"
-       "  const int sub = lane / UB_, u = lane % UB_, uc = cb * UB_ + u;\n"
-       "  const bool cv = uc < C_;\n"
-       "  const sb_i64 mrow = (sb_i64)(r0 + il) * CXO + uc;\n";
-  for (size_t g = 0; g < P.groups.size(); ++g)
-    o << "  float mb" << g << "[" << P.groups[g].d << "];\n#pragma unroll\n  for (int m = 0; m < " << P.groups[g].d
-      << "; ++m) mb" << g << "[m] = cv ? Mb[mrow + " << P.groups[g].off << " + m * C_] : 0.f;\n";
-  o << "  const int wb = max(rowptr[r0 + il], win0), we = min(rowptr[r0 + il + 1], win1);\n"
-       "  for (int e = wb + sub; e < we; e += ES_) {\n"
-       "    int ul = u;\n    asm volatile(\"\" : \"+v\"(ul));\n"
-       "    const int j = sender[e];\n"
-       "    const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
-       "    const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
-       "    const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
-       "    float Y[" << NS << "], yb[" << NS << "], pb[K];\n    sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
-       "#pragma unroll\n    for (int m = 0; m < " << NS << "; ++m) yb[m] = 0.f;\n"
-       "    float ph[K];\n#pragma unroll\n    for (int q = 0; q < K; ++q) { ph[q] = phi[(sb_i64)e * K + q]; pb[q] = 0.f; }\n"
-       "    const sb_i64 xrow = (sb_i64)j * CXI + uc;\n";
-  std::vector<bool> used(P.in.size(), false);
-  for (auto& q : P.paths) used[q.i_in] = true;
-  for (size_t a = 0; a < P.in.size(); ++a)
-    if (used[a]) {
+    << ", NPART_ = " << NPART << ";\n  __shared__ float sA[" << maxp * P.K * UBP << "];\n"
+    << "  const int cb = blockIdx.y, tid = threadIdx.x, lane = tid & 63;\n"
+    << "  const int il = blockIdx.x * 4 + (tid >> 6);\n"
+    << "  const int sub = lane / UB_, u = lane % UB_, uc = cb * UB_ + u;\n"
+    << "  const bool cv = uc < C_;\n"
+    << "  const sb_i64 mrow = (sb_i64)(r0 + il) * CXO + uc;\n"
+    << "  switch (blockIdx.z) {\n";
+  for (int ia = 0; ia < NA; ++ia) {
+    const std::vector<int>& sl = slices[ia];
+    std::vector<int> ts, gs;
+    for (int t = 0; t < NPt; ++t)
+      if (std::find(sl.begin(), sl.end(), P.paths[t].i_in) != sl.end()) {
+        ts.push_back(t);
+        if (std::find(gs.begin(), gs.end(), P.paths[t].group) == gs.end()) gs.push_back(P.paths[t].group);
+      }
+    o << "  case " << ia << ": {\n";
+    for (size_t k = 0; k < ts.size(); ++k)
+      o << "    for (int i = tid; i < K * UB_; i += 256) {\n"
+        << "      const int q = i / UB_, uc2 = cb * UB_ + i % UB_;\n"
+        << "      sA[" << k * P.K * UBP << " + i] = uc2 < C_ ? W[(sb_i64)q * " << P.n_w << "LL + " << P.paths[ts[k]].w_off
+        << "LL + uc2] : 0.f;\n    }\n";
+    o << "    __syncthreads();\n    if (il >= n_recv) return;\n";
+    for (int g : gs)
+      o << "    float mb" << g << "[" << P.groups[g].d << "];\n#pragma unroll\n    for (int m = 0; m < " << P.groups[g].d
+        << "; ++m) mb" << g << "[m] = cv ? Mb[mrow + " << P.groups[g].off << " + m * C_] : 0.f;\n";
+    o << "    const int wb = max(rowptr[r0 + il], win0), we = min(rowptr[r0 + il + 1], win1);\n"
+         "    for (int e = wb + sub; e < we; e += ES_) {\n"
+         "      int ul = u;\n      asm volatile(\"\" : \"+v\"(ul));\n"
+         "      const int j = sender[e];\n"
+         "      const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
+         "      const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
+         "      const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
+         "      float Y[" << NS << "], yb[" << NS << "], pb[K];\n      sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
+         "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) yb[m] = 0.f;\n"
+         "      float ph[K];\n#pragma unroll\n      for (int q = 0; q < K; ++q) { ph[q] = phi[(sb_i64)e * K + q]; pb[q] = 0.f; }\n"
+         "      const sb_i64 xrow = (sb_i64)j * CXI + uc;\n";
+    for (int a : sl) {
       const int d = 2 * P.in[a].l + 1;
-      o << "    float x" << a << "[" << d << "], xb" << a << "[" << d << "];\n#pragma unroll\n    for (int m = 0; m < " << d
+      o << "      float x" << a << "[" << d << "], xb" << a << "[" << d << "];\n#pragma unroll\n      for (int m = 0; m < " << d
         << "; ++m) { x" << a << "[m] = cv ? x[xrow + " << P.in[a].off << " + m * C_] : 0.f; xb" << a << "[m] = 0.f; }\n";
     }
-  for (int t = 0; t < NPt; ++t) {
-    const Path& q = P.paths[t];
-    const int dd = 2 * q.l_out + 1;
-    o << "    {\n      float M[P" << t << "_NP], Cc[" << dd << "], G[" << dd << "];\n      sb_M" << t << "(Y + "
-      << q.l_sh * q.l_sh << ", M);\n      sb_C" << t << "(x" << q.i_in << ", M, Cc);\n"
-      << "      int ua = ul;\n      asm volatile(\"\" : \"+v\"(ua) :: \"memory\");\n"
-      << "      const float* At = sA + " << t * P.K * UBP << " + ua;\n      float w = 0.f, h = 0.f;\n"
-      << "#pragma unroll\n      for (int q = 0; q < K; ++q) w += ph[q] * At[q * UB_];\n"
-      << "#pragma unroll\n      for (int m = 0; m < " << dd << "; ++m) { h += mb" << q.group << "[m] * Cc[m]; G[m] = w * mb"
-      << q.group << "[m]; }\n"
-      << "#pragma unroll\n      for (int q = 0; q < K; ++q) pb[q] += At[q * UB_] * h;\n"
-      << "      sb_XT" << t << "(M, G, xb" << q.i_in << ");\n      sb_YT" << t << "(x" << q.i_in << ", G, yb + "
-      << q.l_sh * q.l_sh << ");\n    }\n    __builtin_amdgcn_sched_barrier(0);\n";
+    for (size_t k = 0; k < ts.size(); ++k) {
+      const int t = ts[k];
+      const Path& q = P.paths[t];
+      const int dd = 2 * q.l_out + 1;
+      o << "      {\n        float M[P" << t << "_NP], Cc[" << dd << "], G[" << dd << "];\n        sb_M" << t << "(Y + "
+        << q.l_sh * q.l_sh << ", M);\n        sb_C" << t << "(x" << q.i_in << ", M, Cc);\n"
+        << "        int ua = ul;\n        asm volatile(\"\" : \"+v\"(ua) :: \"memory\");\n"
+        << "        const float* At = sA + " << k * P.K * UBP << " + ua;\n        float w = 0.f, h = 0.f;\n"
+        << "#pragma unroll\n        for (int q = 0; q < K; ++q) w += ph[q] * At[q * UB_];\n"
+        << "#pragma unroll\n        for (int m = 0; m < " << dd << "; ++m) { h += mb" << q.group << "[m] * Cc[m]; G[m] = w * mb"
+        << q.group << "[m]; }\n"
+        << "#pragma unroll\n        for (int q = 0; q < K; ++q) pb[q] += At[q * UB_] * h;\n"
+        << "        sb_XT" << t << "(M, G, xb" << q.i_in << ");\n        sb_YT" << t << "(x" << q.i_in << ", G, yb + "
+        << q.l_sh * q.l_sh << ");\n      }\n"
+        << "      __builtin_amdgcn_sched_barrier(0);\n";
+    }
+    o << "      if (contrib) {\n        float* cr = contrib + (sb_i64)(e - e0) * CXI;\n        if (cv) {\n";
+    for (int a : sl)
+      o << "#pragma unroll\n          for (int m = 0; m < " << 2 * P.in[a].l + 1 << "; ++m) cr[" << P.in[a].off
+        << " + m * C_ + uc] = xb" << a << "[m];\n";
+    o << "        }\n";
+    if (ia == 0)  // dead input irreps: zero columns, written by the first slice's first channel block
+      for (size_t a2 = 0; a2 < P.in.size(); ++a2)
+        if (!used[a2])
+          o << "        if (cb == 0)\n          for (int c = u; c < " << P.in[a2].dim() << "; c += UB_) cr[" << P.in[a2].off
+            << " + c] = 0.f;\n";
+    o << "      }\n"
+         "#pragma unroll\n      for (int s = 1; s < UB_; s <<= 1) {\n"
+         "#pragma unroll\n        for (int q = 0; q < K; ++q) pb[q] += __shfl_xor(pb[q], s);\n"
+         "#pragma unroll\n        for (int m = 0; m < " << NS << "; ++m) yb[m] += __shfl_xor(yb[m], s);\n      }\n";
+    if (NPART == 1)
+      o << "      if (u == 0) {\n"
+           "        if (gphi) {\n#pragma unroll\n          for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = pb[q];\n        }\n"
+           "        if (gevec) {\n          float gg[3];\n          sb_sh_vjp(ux, uy, uz, rinv, yb, gg);\n"
+           "          gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n"
+           "        }\n      }\n";
+    else
+      o << "      if (u == 0) {\n        float* pp = part + ((sb_i64)(e - e0) * NPART_ + " << ia << " * NB_ + cb) * NV_;\n"
+           "#pragma unroll\n        for (int q = 0; q < K; ++q) pp[q] = pb[q];\n"
+           "#pragma unroll\n        for (int m = 0; m < " << NS << "; ++m) pp[K + m] = yb[m];\n      }\n";
+    o << "    }\n    break;\n  }\n";
   }
-  // contributions (dead input irreps get zero columns)
-  o << "    if (contrib && cv) {\n      float* cr = contrib + (sb_i64)(e - e0) * CXI + uc;\n";
-  for (size_t a = 0; a < P.in.size(); ++a) {
-    const int d = 2 * P.in[a].l + 1;
-    if (used[a])
-      o << "#pragma unroll\n      for (int m = 0; m < " << d << "; ++m) cr[" << P.in[a].off << " + m * C_] = xb" << a << "[m];\n";
-    else if (P.in[a].mul == C)
-      o << "#pragma unroll\n      for (int m = 0; m < " << d << "; ++m) cr[" << P.in[a].off << " + m * C_] = 0.f;\n";
-  }
-  o << "    }\n";
-  // sums over the lane group's channels
-  o << "#pragma unroll\n    for (int s = 1; s < UB_; s <<= 1) {\n"
-       "#pragma unroll\n      for (int q = 0; q < K; ++q) pb[q] += __shfl_xor(pb[q], s);\n"
-       "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) yb[m] += __shfl_xor(yb[m], s);\n    }\n";
-  if (NB == 1)
-    o << "    if (u == 0) {\n"
-         "      if (gphi) {\n#pragma unroll\n        for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = pb[q];\n      }\n"
-         "      if (gevec) {\n        float gg[3];\n        sb_sh_vjp(ux, uy, uz, rinv, yb, gg);\n"
-         "        gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n"
-         "      }\n    }\n";
-  else
-    o << "    if (u == 0) {\n      float* pp = part + ((sb_i64)(e - e0) * NB_ + cb) * NV_;\n"
-         "#pragma unroll\n      for (int q = 0; q < K; ++q) pp[q] = pb[q];\n"
-         "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) pp[K + m] = yb[m];\n    }\n";
   o << "  }\n}\n";
-  if (NB > 1) {
-    o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd_fin(const float* __restrict__ evec,"
+  if (NPART > 1) {
+    o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd_fin" << sfx << "(const float* __restrict__ evec,"
          " const float* __restrict__ part, float* __restrict__ gphi, float* __restrict__ gevec, int e0, int e1) {\n"
-      << "  constexpr int NB_ = " << NB << ", NV_ = " << NV << ";\n"
+      << "  constexpr int NPART_ = " << NPART << ", NV_ = " << NV << ";\n"
       << "  const int e = e0 + blockIdx.x * 256 + threadIdx.x;\n  if (e >= e1) return;\n"
-      << "  const float* pp = part + (sb_i64)(e - e0) * NB_ * NV_;\n"
+      << "  const float* pp = part + (sb_i64)(e - e0) * NPART_ * NV_;\n"
       << "  float v[NV_];\n#pragma unroll\n  for (int k = 0; k < NV_; ++k) v[k] = pp[k];\n"
-      << "  for (int b = 1; b < NB_; ++b) {\n#pragma unroll\n    for (int k = 0; k < NV_; ++k) v[k] += pp[b * NV_ + k];\n  }\n"
+      << "  for (int b = 1; b < NPART_; ++b) {\n#pragma unroll\n    for (int k = 0; k < NV_; ++k) v[k] += pp[b * NV_ + k];\n  }\n"
       << "  if (gphi) {\n#pragma unroll\n    for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = v[q];\n  }\n"
       << "  if (gevec) {\n"
       << "    const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
@@ -1333,7 +1368,8 @@ std::string generate_source(const Plan& P) {
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
   if (P.mode == 1 && P.uvu_C > 0) {
     emit_uvu_fwd(o, P);
-    emit_uvu_bwd(o, P);
+    emit_uvu_bwd(o, P, false);
+    emit_uvu_bwd(o, P, true);
     emit_uvu_wgrad(o, P);
   }
 

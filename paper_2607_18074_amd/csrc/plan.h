@@ -108,8 +108,10 @@ struct Plan {
   int bwd_lds_max = 0;          // largest slab (floats)
   bool vec4 = false;            // every multiplicity a multiple of 4: vectorised GEMMs apply
   int uvu_C = 0;                // uvu with one multiplicity C on every path: the state-free kernels apply
-  int uvu_NB = 0;               // 64-channel blocks of C (the state-free backward's per-edge partial count)
+  int uvu_NB = 0;               // 64-channel blocks of C
+  int uvu_NA = 0;               // input irreps with paths (slices of the state-free backward)
   bool uvu_bwd_direct = false;  // the state-free backward compiled without register spills (set at load)
+  bool uvu_sliced = false;      // ... in its per-input-irrep form (the all-irrep form spilled)
   bool uvu_wgrad_direct = false;  // likewise the state-free weight gradient
   std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
   std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)

@@ -24,6 +24,7 @@ SIGS = {
     "uvu_l3": ("8x0e+8x1o+8x2e+8x3o", 3, "8x0e+8x1o+8x2e+8x3o", 16),
     "uvu_odd": ("3x0e+3x1o+3x1e+3x2e", 1, "3x0e+3x1o+3x1e+3x2e+1x3e", 4),   # 3e: dead output
     "uvu_wide": ("96x0e+96x1o", 1, "96x0e+96x1o", 4),   # two 64-channel blocks, the second half full
+    "uvu_dead": ("4x0e+4x1o+2x0o", 1, "4x0e+4x1o", 4),   # 2x0o reaches no output: zero x-gradient
 }
 
 

@@ -11,7 +11,7 @@ from tests.cases import BWD_TOL, FWD_TOL, make_case, max_rel
 pytestmark = pytest.mark.gpu
 
 CASES = [("uvu_small", 200, 3000, 21, 2), ("uvu_l3", 60, 700, 22, 1), ("uvu_odd", 50, 600, 23, 1),
-         ("uvu_wide", 80, 1000, 26, 1)]
+         ("uvu_wide", 80, 1000, 26, 1), ("uvu_dead", 60, 700, 28, 1)]
 
 
 def _t(a):
