@@ -210,10 +210,12 @@ int nsplit_for(const sobek::Group& g, int64_t nrows, bool vec4) {
 // accumulated over the receiver chunks of a pass and reduced once at its end
 size_t partial_floats(const Plan& p, int64_t ncap, int pass = SOBEK_PASS_BWD) {
   // the state-free channelwise weight gradient: one partial row of K * N_w floats per wave
-  if (pass == SOBEK_PASS_BWD && p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && p.uvu_wgrad_direct)
-    return (size_t)sobek::kUvuWaves * p.K * p.n_w;
+  // (the double backward may also take the receiver route: room for both)
+  const bool free = p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && p.uvu_wgrad_direct;
+  if (pass == SOBEK_PASS_BWD && free) return (size_t)sobek::kUvuWaves * p.K * p.n_w;
   size_t m = 0;
   for (auto& g : p.groups) m += (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C;
+  if (pass == SOBEK_PASS_DBWD && free) m = std::max(m, (size_t)sobek::kUvuWaves * p.K * p.n_w);
   return m;
 }
 
@@ -249,7 +251,7 @@ int sa_nsplit(const sobek::Group& g, int64_t nrows, size_t kfloats, int& kper) {
 // (phi_bar and Y_bar of every 64-channel block), kept after the window's contributions
 int64_t uvu_edge_partials(const Plan& p, int pass) {
   const int64_t npart = (int64_t)p.uvu_NB * (p.uvu_sliced ? p.uvu_NA : 1);
-  return (pass == SOBEK_PASS_BWD && p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && npart > 1)
+  return (pass != SOBEK_PASS_FWD && p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && npart > 1)
              ? npart * (p.K + p.nsh)
              : 0;
 }
@@ -690,6 +692,17 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
         (rc = get(p.k.uvu_bwd_fin, p.uvu_sliced ? "sobek_uvu_bwd_fin_s" : "sobek_uvu_bwd_fin_u")))
       return rc;
     p.uvu_wgrad_direct = sw == 0;
+    // the edge-vector-tangent variants (double backward), same slicing
+    if ((rc = get(p.k.uvu_fwd_t, "sobek_uvu_fwd_t")) || (rc = get(p.k.uvu_wgrad_t, "sobek_uvu_wgrad_t")) ||
+        (rc = get(p.k.uvu_bwd_t, p.uvu_sliced ? "sobek_uvu_bwd_st" : "sobek_uvu_bwd_ut")))
+      return rc;
+    if (p.uvu_bwd_direct && npart > 1 &&
+        (rc = get(p.k.uvu_bwd_fin_t, p.uvu_sliced ? "sobek_uvu_bwd_fin_st" : "sobek_uvu_bwd_fin_ut")))
+      return rc;
+    int st = 0, swt = 0;
+    HIPCHK(hipFuncGetAttribute(&st, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd_t));
+    HIPCHK(hipFuncGetAttribute(&swt, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad_t));
+    p.uvu_tan_direct = st == 0 && swt == 0;
   }
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
@@ -964,7 +977,7 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     // channelwise, one multiplicity: every receiver at once, no receiver state
     int r0 = 0, n = (int)G.N;
     LAUNCH(p.k.uvu_fwd, cdiv(G.N, 4), cdiv(p.uvu_C, 64), 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec,
-           phi, xk, W, ok, r0, n);
+           phi, xk, W, ok, r0, n, (const float*)nullptr);
     if ((rc = zero_dead_out(p, ok, G.N, stream))) return rc;
     if (mulir && (rc = transpose(p, ok, out, G.N, false, 1, stream))) return rc;
     return SOBEK_OK;
@@ -1033,7 +1046,7 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     int rows = sobek::kUvuWaves;
     long long nw = (long long)p.K * p.n_w;
     LAUNCH(p.k.uvu_wgrad, sobek::kUvuWaves / 4, p.uvu_NB, na, stream, (const int*)G.rowptr, (const int*)G.sender,
-           evec, phi, xk, gk, P, n);
+           evec, phi, xk, gk, P, n, (const float*)nullptr);
     LAUNCH(p.k.uvu_wreduce, cdiv(nw, 256), 1, 1, stream, (const float*)P, rows, nw, gW);
   }
   if (adj_state && (rc = run_sbar(p, all, G.N, gk, W, adj_state, stream))) return rc;
@@ -1052,9 +1065,10 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
           float* part = (float*)((char*)ws + w.off_contrib) + (size_t)w.ecap * p.dim_in;
           const int ns = p.uvu_sliced ? p.uvu_NA : 1;
           LAUNCH(p.k.uvu_bwd, cdiv(nr, 4), p.uvu_NB, ns, stream, (const int*)G.rowptr, (const int*)G.sender, evec,
-                 phi, xk, W, gk, gphi, gevec, contrib, part, ra, nr, e0, e0, e1);
+                 phi, xk, W, gk, gphi, gevec, contrib, part, ra, nr, e0, e0, e1, (const float*)nullptr);
           if (p.uvu_NB * ns > 1 && (gphi || gevec))
-            LAUNCH(p.k.uvu_bwd_fin, cdiv(eb - ea, 256), 1, 1, stream, evec, (const float*)part, gphi, gevec, e0, e1);
+            LAUNCH(p.k.uvu_bwd_fin, cdiv(eb - ea, 256), 1, 1, stream, evec, (const float*)part, gphi, gevec, e0, e1,
+                   (const float*)nullptr);
         } else {
           long long ncap = w.ncap, sb_ncap = adj_state ? G.N : w.ncap;
           int sb_r0 = adj_state ? ra : sub_off;
@@ -1133,9 +1147,13 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
   const Plan& p = plan->p;
   const sobek_graph_s& G = *graph;
   WsPlan w;
-  // the second state slot (Sbar') is needed only with a dA cotangent
-  if ((rc = plan_workspace(p, G, SOBEK_PASS_DBWD, ws_bytes, w, false, t_gW ? 2 : 1))) return rc;
   const int flags = (t_gphi ? 1 : 0) | (t_gx ? 2 : 0) | (t_gevec ? 4 : 0) | (t_gW ? 8 : 0);
+  // channelwise plans with the state-free kernels take the double backward of an edge-vector
+  // cotangent alone without receiver state: m_dot, g_W and the edge terms along Ydot = J evd
+  const bool uvu_free = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct && p.uvu_wgrad_direct &&
+                        p.uvu_tan_direct && flags == 4;
+  // the second state slot (Sbar') is needed only with a dA cotangent
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_DBWD, ws_bytes, w, false, uvu_free ? 0 : (t_gW ? 2 : 1)))) return rc;
   const bool tan = flags & 7;
   if (g_W) { if ((rc = fill_zero(p, g_W, (int64_t)p.K * p.n_w, stream))) return rc; }
   if (G.N == 0) return SOBEK_OK;
@@ -1155,6 +1173,47 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
     if (g_x) gxk = (float*)((char*)ws + w.off_gx);
   }
   if (g_gout && !tan && !t_gW) { if ((rc = fill_zero(p, ggk, G.N * p.dim_out, stream))) return rc; }
+  if (uvu_free) {
+    int n = (int)G.N, r0 = 0;
+    if (g_gout) {
+      LAUNCH(p.k.uvu_fwd_t, cdiv(G.N, 4), p.uvu_NB, 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec, phi,
+             xk, W, ggk, r0, n, t_gevec);
+      if ((rc = zero_dead_out(p, ggk, G.N, stream))) return rc;
+    }
+    if (g_W) {
+      float* P = (float*)((char*)ws + w.off_P);
+      int rows = sobek::kUvuWaves;
+      long long nw = (long long)p.K * p.n_w;
+      LAUNCH(p.k.uvu_wgrad_t, sobek::kUvuWaves / 4, p.uvu_NB, p.uvu_NA, stream, (const int*)G.rowptr,
+             (const int*)G.sender, evec, phi, xk, gk, P, n, t_gevec);
+      LAUNCH(p.k.uvu_wreduce, cdiv(nw, 256), 1, 1, stream, (const float*)P, rows, nw, g_W);
+    }
+    float* contrib = g_x ? (float*)((char*)ws + w.off_contrib) : nullptr;
+    float* part = (float*)((char*)ws + w.off_contrib) + (size_t)w.ecap * p.dim_in;
+    const int ns = p.uvu_sliced ? p.uvu_NA : 1;
+    bool first_win = true;
+    if (g_x || g_evec || g_phi)
+      for (const Chunk& c : w.chunks) {
+        rc = for_edge_windows(G, c, w, [&](int64_t ea, int64_t eb, int ra, int nr) -> int {
+          int e0 = (int)ea, e1 = (int)eb;
+          LAUNCH(p.k.uvu_bwd_t, cdiv(nr, 4), p.uvu_NB, ns, stream, (const int*)G.rowptr, (const int*)G.sender, evec,
+                 phi, xk, W, gk, g_phi, g_evec, contrib, part, ra, nr, e0, e0, e1, t_gevec);
+          if (p.uvu_NB * ns > 1 && (g_phi || g_evec))
+            LAUNCH(p.k.uvu_bwd_fin_t, cdiv(eb - ea, 256), 1, 1, stream, evec, (const float*)part, g_phi, g_evec, e0,
+                   e1, t_gevec);
+          const int first = first_win;
+          first_win = false;
+          return g_x ? run_sender_reduce(p, G, ea, eb, w, ws, contrib, gxk, first, stream) : SOBEK_OK;
+        });
+        if (rc) return rc;
+      }
+    if (g_x && first_win && (rc = fill_zero(p, gxk, G.N * p.dim_in, stream))) return rc;
+    if (mulir) {
+      if (g_gout && (rc = transpose(p, ggk, g_gout, G.N, false, 1, stream))) return rc;
+      if (g_x && (rc = transpose(p, gxk, g_x, G.N, true, 1, stream))) return rc;
+    }
+    return SOBEK_OK;
+  }
   // one slot reused in stream order: dS (for m_dot and g_W), then S (for m_dot += S dA),
   // then Sbar; the second slot holds Sbar' when dA is active
   float* dS = state_ptr(w, ws, p, 0);

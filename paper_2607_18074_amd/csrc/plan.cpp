@@ -1047,14 +1047,15 @@ void emit_adj_stage(std::ostringstream& o, const Plan& P, int s, const char* ind
 // are (4 receivers, 64-channel block); the block's A slice [path][q][channel] is
 // staged in LDS once.  C < 64 puts 64 / C edges in flight per wave (lane = edge
 // slot * C + u), combined by cross-lane adds in a fixed order.
-void emit_uvu_fwd(std::ostringstream& o, const Plan& P) {
+void emit_uvu_fwd(std::ostringstream& o, const Plan& P, bool tan) {
   const int C = P.uvu_C, UB = std::min(C, 64);
   const int ES = (64 % UB == 0) ? 64 / UB : 1;
   const int NPt = (int)P.paths.size();
   const int L = P.lmax, NS = (L + 1) * (L + 1);
-  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_fwd(const int* __restrict__ rowptr,"
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_fwd" << (tan ? "_t" : "") << "(const int* __restrict__ rowptr,"
        " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
-       " const float* __restrict__ x, const float* __restrict__ W, float* __restrict__ out, int r0, int n_recv) {\n"
+       " const float* __restrict__ x, const float* __restrict__ W, float* __restrict__ out, int r0, int n_recv,"
+       " const float* __restrict__ evd) {\n"
     << "  constexpr int C_ = " << C << ", UB_ = " << UB << ", ES_ = " << ES << ";\n"
     << "  __shared__ float sA[" << NPt * P.K * UB << "];\n"
     << "  const int cb = blockIdx.y, tid = threadIdx.x, lane = tid & 63;\n";
@@ -1082,6 +1083,10 @@ void emit_uvu_fwd(std::ostringstream& o, const Plan& P) {
        "    float Y[" << NS << "];\n    sb_sh_eval_L" << L << "(vx * rinv, vy * rinv, vz * rinv, Y);\n"
        "    float ph[K];\n#pragma unroll\n    for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
        "    const sb_i64 xrow = (sb_i64)j * CXI + uc;\n";
+  if (tan)  // the tangent variant takes the message along Ydot = J evd (the tangent output)
+    o << "    {\n      float Yd[" << NS << "];\n      sb_sh_jvp_L" << L << "(vx * rinv, vy * rinv, vz * rinv, rinv,"
+         " evd[3 * (sb_i64)e], evd[3 * (sb_i64)e + 1], evd[3 * (sb_i64)e + 2], Y, Yd);\n"
+         "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) Y[m] = Yd[m];\n    }\n";
   std::vector<bool> used(P.in.size(), false);
   for (auto& q : P.paths) used[q.i_in] = true;
   for (size_t a = 0; a < P.in.size(); ++a)
@@ -1146,9 +1151,9 @@ void emit_path_transposes(std::ostringstream& o, const Plan& P, int t) {
 // final, else each slice writes per-edge partials that sobek_uvu_bwd_fin adds in
 // slice order.  Edges are those of the receiver inside [win0, win1); the
 // contribution row of edge e sits at e - e0.
-void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
+void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced, bool tan) {
   const int C = P.uvu_C, NB = P.uvu_NB;
-  const char* sfx = sliced ? "_s" : "_u";
+  const std::string sfx = std::string(sliced ? "_s" : "_u") + (tan ? "t" : "");
   int UBP = 64;
   if (C < 64) { UBP = 1; while (UBP < C) UBP <<= 1; }
   const int ES = 64 / UBP;
@@ -1170,13 +1175,13 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
     for (auto& q : P.paths) n += std::find(sl.begin(), sl.end(), q.i_in) != sl.end();
     maxp = std::max(maxp, n);
   }
-  if (!sliced)
+  if (!sliced && !tan)
     for (int t = 0; t < NPt; ++t) emit_path_transposes(o, P, t);
   o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd" << sfx << "(const int* __restrict__ rowptr,"
        " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
        " const float* __restrict__ x, const float* __restrict__ W, const float* __restrict__ Mb,"
        " float* __restrict__ gphi, float* __restrict__ gevec, float* __restrict__ contrib, float* __restrict__ part,"
-       " int r0, int n_recv, int e0, int win0, int win1) {\n"
+       " int r0, int n_recv, int e0, int win0, int win1, const float* __restrict__ evd) {\n"
     << "  constexpr int C_ = " << C << ", UB_ = " << UBP << ", ES_ = " << ES << ", NB_ = " << NB << ", NV_ = " << NV
     << ", NPART_ = " << NPART << ";\n  __shared__ float sA[" << maxp * P.K * UBP << "];\n"
     << "  const int cb = blockIdx.y, tid = threadIdx.x, lane = tid & 63;\n"
@@ -1211,7 +1216,15 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
          "      const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
          "      const float ux = vx * rinv, uy = vy * rinv, uz = vz * rinv;\n"
          "      float Y[" << NS << "], yb[" << NS << "], pb[K];\n      sb_sh_eval_L" << L << "(ux, uy, uz, Y);\n"
-         "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) yb[m] = 0.f;\n"
+         // double backward along an edge-vector tangent (no other cotangent): h and the
+         // x-gradient contribution are taken along Ydot = J evd, Y_bar stays the backward's
+         // and the edge-vector output is its Hessian term sum_m Y_bar_m Hess(Y_m) evd
+         << (tan ? std::string("      const float tx = evd[3 * (sb_i64)e], ty = evd[3 * (sb_i64)e + 1], tz = evd[3 * (sb_i64)e + 2];\n"
+                               "      {\n        float Yd[") + std::to_string(NS) + "];\n        sb_sh_jvp_L" + std::to_string(L) +
+                       "(ux, uy, uz, rinv, tx, ty, tz, Y, Yd);\n#pragma unroll\n        for (int m = 0; m < " +
+                       std::to_string(NS) + "; ++m) Y[m] = Yd[m];\n      }\n"
+                 : std::string())
+      << "#pragma unroll\n      for (int m = 0; m < " << NS << "; ++m) yb[m] = 0.f;\n"
          "      float ph[K];\n#pragma unroll\n      for (int q = 0; q < K; ++q) { ph[q] = phi[(sb_i64)e * K + q]; pb[q] = 0.f; }\n"
          "      const sb_i64 xrow = (sb_i64)j * CXI + uc;\n";
     for (int a : sl) {
@@ -1252,8 +1265,9 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
     if (NPART == 1)
       o << "      if (u == 0) {\n"
            "        if (gphi) {\n#pragma unroll\n          for (int q = 0; q < K; ++q) gphi[(sb_i64)e * K + q] = pb[q];\n        }\n"
-           "        if (gevec) {\n          float gg[3];\n          sb_sh_vjp(ux, uy, uz, rinv, yb, gg);\n"
-           "          gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n"
+           "        if (gevec) {\n          float gg[3];\n"
+        << (tan ? "          sb_sh_hvp(ux, uy, uz, rinv, yb, tx, ty, tz, gg);\n" : "          sb_sh_vjp(ux, uy, uz, rinv, yb, gg);\n")
+        << "          gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n"
            "        }\n      }\n";
     else
       o << "      if (u == 0) {\n        float* pp = part + ((sb_i64)(e - e0) * NPART_ + " << ia << " * NB_ + cb) * NV_;\n"
@@ -1264,7 +1278,8 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
   o << "  }\n}\n";
   if (NPART > 1) {
     o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_bwd_fin" << sfx << "(const float* __restrict__ evec,"
-         " const float* __restrict__ part, float* __restrict__ gphi, float* __restrict__ gevec, int e0, int e1) {\n"
+         " const float* __restrict__ part, float* __restrict__ gphi, float* __restrict__ gevec, int e0, int e1,"
+         " const float* __restrict__ evd) {\n"
       << "  constexpr int NPART_ = " << NPART << ", NV_ = " << NV << ";\n"
       << "  const int e = e0 + blockIdx.x * 256 + threadIdx.x;\n  if (e >= e1) return;\n"
       << "  const float* pp = part + (sb_i64)(e - e0) * NPART_ * NV_;\n"
@@ -1274,7 +1289,10 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
       << "  if (gevec) {\n"
       << "    const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
       << "    const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
-      << "    float gg[3];\n    sb_sh_vjp(vx * rinv, vy * rinv, vz * rinv, rinv, v + K, gg);\n"
+      << "    float gg[3];\n"
+      << (tan ? "    sb_sh_hvp(vx * rinv, vy * rinv, vz * rinv, rinv, v + K, evd[3 * (sb_i64)e], evd[3 * (sb_i64)e + 1],"
+                " evd[3 * (sb_i64)e + 2], gg);\n"
+              : "    sb_sh_vjp(vx * rinv, vy * rinv, vz * rinv, rinv, v + K, gg);\n")
       << "    gevec[3 * (sb_i64)e] = gg[0]; gevec[3 * (sb_i64)e + 1] = gg[1]; gevec[3 * (sb_i64)e + 2] = gg[2];\n  }\n}\n";
   }
 }
@@ -1286,7 +1304,7 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced) {
 // keeps K accumulators per path of a and channel in registers; each wave writes
 // its own partial row part[w][q * N_w + w_off + u], which sobek_uvu_wreduce adds
 // in wave order.
-void emit_uvu_wgrad(std::ostringstream& o, const Plan& P) {
+void emit_uvu_wgrad(std::ostringstream& o, const Plan& P, bool tan) {
   const int C = P.uvu_C;
   int UBP = 64;
   if (C < 64) { UBP = 1; while (UBP < C) UBP <<= 1; }
@@ -1296,10 +1314,11 @@ void emit_uvu_wgrad(std::ostringstream& o, const Plan& P) {
   for (size_t a = 0; a < P.in.size(); ++a)
     for (auto& q : P.paths)
       if (q.i_in == (int)a) { ins.push_back((int)a); break; }
-  o << "#define UVU_WAVES " << kUvuWaves << "\n"
-    << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_wgrad(const int* __restrict__ rowptr,"
+  if (!tan) o << "#define UVU_WAVES " << kUvuWaves << "\n";
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_wgrad" << (tan ? "_t" : "") << "(const int* __restrict__ rowptr,"
        " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
-       " const float* __restrict__ x, const float* __restrict__ Mb, float* __restrict__ part, int n_recv) {\n"
+       " const float* __restrict__ x, const float* __restrict__ Mb, float* __restrict__ part, int n_recv,"
+       " const float* __restrict__ evd) {\n"
     << "  constexpr int C_ = " << C << ", UB_ = " << UBP << ", ES_ = " << ES << ";\n"
     << "  const int cb = blockIdx.y, lane = threadIdx.x & 63, wv = blockIdx.x * 4 + (threadIdx.x >> 6);\n"
     << "  const int sub = lane / UB_, u = lane % UB_, uc = cb * UB_ + u;\n"
@@ -1328,7 +1347,12 @@ void emit_uvu_wgrad(std::ostringstream& o, const Plan& P) {
          "        const float vx = evec[3 * (sb_i64)e], vy = evec[3 * (sb_i64)e + 1], vz = evec[3 * (sb_i64)e + 2];\n"
          "        const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
          "        float Y[" << NS << "];\n        sb_sh_eval_L" << L << "(vx * rinv, vy * rinv, vz * rinv, Y);\n"
-         "        float ph[K];\n#pragma unroll\n        for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
+         << (tan ? std::string("        {\n          float Yd[") + std::to_string(NS) + "];\n          sb_sh_jvp_L" +
+                       std::to_string(L) + "(vx * rinv, vy * rinv, vz * rinv, rinv, evd[3 * (sb_i64)e], evd[3 * (sb_i64)e + 1],"
+                       " evd[3 * (sb_i64)e + 2], Y, Yd);\n#pragma unroll\n          for (int m = 0; m < " + std::to_string(NS) +
+                       "; ++m) Y[m] = Yd[m];\n        }\n"
+                     : std::string())
+      << "        float ph[K];\n#pragma unroll\n        for (int q = 0; q < K; ++q) ph[q] = phi[(sb_i64)e * K + q];\n"
          "        float xa[" << d << "];\n#pragma unroll\n        for (int m = 0; m < " << d << "; ++m) xa[m] = cv ? x[(sb_i64)j * CXI + "
       << P.in[a].off << " + m * C_ + uc] : 0.f;\n";
     for (int t : ts) {
@@ -1367,10 +1391,12 @@ std::string generate_source(const Plan& P) {
   emit_sh(o, P.lmax);
   for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
   if (P.mode == 1 && P.uvu_C > 0) {
-    emit_uvu_fwd(o, P);
-    emit_uvu_bwd(o, P, false);
-    emit_uvu_bwd(o, P, true);
-    emit_uvu_wgrad(o, P);
+    for (int tan = 0; tan < 2; ++tan) {  // plain and edge-vector-tangent (double backward) variants
+      emit_uvu_fwd(o, P, tan);
+      emit_uvu_bwd(o, P, false, tan);
+      emit_uvu_bwd(o, P, true, tan);
+      emit_uvu_wgrad(o, P, tan);
+    }
   }
 
   // streaming adjoint-state GEMM, one instantiation per output multiplicity

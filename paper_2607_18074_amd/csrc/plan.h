@@ -87,6 +87,7 @@ struct Kernels {
   hipFunction_t uvu_mix = nullptr, uvu_sbar = nullptr, uvu_ga = nullptr;  // channelwise mixing
   hipFunction_t uvu_fwd = nullptr, uvu_bwd = nullptr, uvu_bwd_fin = nullptr;  // channelwise state-free kernels
   hipFunction_t uvu_wgrad = nullptr, uvu_wreduce = nullptr;
+  hipFunction_t uvu_fwd_t = nullptr, uvu_bwd_t = nullptr, uvu_bwd_fin_t = nullptr, uvu_wgrad_t = nullptr;  // tangent
 };
 
 struct Plan {
@@ -113,6 +114,7 @@ struct Plan {
   bool uvu_bwd_direct = false;  // the state-free backward compiled without register spills (set at load)
   bool uvu_sliced = false;      // ... in its per-input-irrep form (the all-irrep form spilled)
   bool uvu_wgrad_direct = false;  // likewise the state-free weight gradient
+  bool uvu_tan_direct = false;    // and their edge-vector-tangent variants (double backward)
   std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
   std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)
   std::string source;           // generated HIP source
