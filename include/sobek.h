@@ -112,7 +112,11 @@ int sobek_plan_create(const sobek_irrep *in, int n_in, int lmax, const sobek_irr
 int sobek_plan_destroy(sobek_plan plan);
 /* Generate and compile (hipRTC, gfx950) the kernels of a signature into the
  * on-disk code-object cache without touching a GPU; arguments as in
- * sobek_plan_create.  Lets a build step prepare kernels ahead of a GPU run. */
+ * sobek_plan_create.  Lets a build step prepare kernels ahead of a GPU run.
+ * Channelwise plans with the state-free kernels load those at creation and the
+ * receiver-route kernels on first use (a double backward with cotangents other
+ * than the edge vectors', a forward that keeps its state); both are compiled
+ * here, or only the first with SOBEK_JIT_STATE_FREE_ONLY=1 in the environment. */
 int sobek_jit_compile(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out, int K,
                       int mode, int layout, int dtype, int path_norm);
 /* Full HIP source generated for a signature (prelude + plan code), NUL-terminated

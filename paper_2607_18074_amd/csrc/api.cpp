@@ -171,6 +171,7 @@ int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep
   if (p.n_w * (int64_t)K >= (1ll << 31) || maxD >= (1ll << 31))
     return fail(SOBEK_E_UNSUPPORTED, "weight tensor too large for 32-bit indexing");
   p.source = sobek::generate_source(p);
+  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0) p.source_u = sobek::generate_source(p, false);
   return SOBEK_OK;
 }
 
@@ -637,39 +638,74 @@ extern "C" {
 const char* sobek_last_error(void) { return g_err.c_str(); }
 int sobek_version(void) { return 1; }
 
-int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int mode,
-                      int layout, int dtype, int path_norm, sobek_plan* plan) {
-  if (!plan) return fail(SOBEK_E_INVALID, "plan output pointer is NULL");
-  *plan = nullptr;
-  std::unique_ptr<sobek_plan_s> h(new sobek_plan_s());
-  Plan& p = h->p;
-  int rc = build_signature(in, n_in, lmax, out, n_out, K, mode, layout, dtype, path_norm, p);
-  if (rc != SOBEK_OK) return rc;
+}  // extern "C"
+
+namespace {
+
+int load_module(const std::string& src, hipModule_t& m) {
   std::vector<char> code;
   try {
-    code = sobek::jit_compile(p.source);
+    code = sobek::jit_compile(src);
   } catch (const std::exception& ex) {
     return fail(SOBEK_E_COMPILE, "%s", ex.what());
   }
-  HIPCHK(hipModuleLoadData(&p.k.module, code.data()));
-  auto get = [&](hipFunction_t& f, const char* name) -> int {
-    hipError_t e = hipModuleGetFunction(&f, p.k.module, name);
-    if (e != hipSuccess) return fail(SOBEK_E_INTERNAL, "kernel %s missing: %s", name, hipGetErrorString(e));
-    std::lock_guard<std::mutex> lk(g_prof_mu);
-    g_names[f] = name;
-    return SOBEK_OK;
-  };
-  const char* bns[3] = {"16", "32", "64"};
-  if ((rc = get(p.k.fwd_S, "sobek_fwd_S")) || (rc = get(p.k.fwd_dS, "sobek_fwd_dS")) ||
-      (rc = get(p.k.fwd_dS_r, "sobek_fwd_dS_r")) || (rc = get(p.k.bwd_E, "sobek_bwd_E")) ||
-      (rc = get(p.k.dbwd_E, "sobek_dbwd_E")) || (rc = get(p.k.dbwd_E_r, "sobek_dbwd_E_r")) ||
-      (rc = get(p.k.ga_reduce, "sobek_ga_reduce")) || (rc = get(p.k.sender_reduce, "sobek_sender_reduce")) ||
-      (rc = get(p.k.transpose, "sobek_transpose")) || (rc = get(p.k.fill_cols, "sobek_fill_cols")) ||
-      (rc = get(p.k.zero, "sobek_zero")) || (rc = get(p.k.sa_reduce, "sobek_sa_reduce")) ||
-      (rc = get(p.k.uvu_mix, "sobek_uvu_mix")) || (rc = get(p.k.uvu_sbar, "sobek_uvu_sbar")) ||
-      (rc = get(p.k.uvu_ga, "sobek_uvu_ga")))
+  HIPCHK(hipModuleLoadData(&m, code.data()));
+  return SOBEK_OK;
+}
+
+int get_fn(hipModule_t m, hipFunction_t& f, const char* name) {
+  hipError_t e = hipModuleGetFunction(&f, m, name);
+  if (e != hipSuccess) return fail(SOBEK_E_INTERNAL, "kernel %s missing: %s", name, hipGetErrorString(e));
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_names[f] = name;
+  return SOBEK_OK;
+}
+
+// kernels every route uses (prelude and the sender gather)
+int load_common(Plan& p, hipModule_t m) {
+  int rc;
+  if ((rc = get_fn(m, p.k.ga_reduce, "sobek_ga_reduce")) || (rc = get_fn(m, p.k.sender_reduce, "sobek_sender_reduce")) ||
+      (rc = get_fn(m, p.k.transpose, "sobek_transpose")) || (rc = get_fn(m, p.k.fill_cols, "sobek_fill_cols")) ||
+      (rc = get_fn(m, p.k.zero, "sobek_zero")) || (rc = get_fn(m, p.k.sa_reduce, "sobek_sa_reduce")) ||
+      (rc = get_fn(m, p.k.uvu_mix, "sobek_uvu_mix")) || (rc = get_fn(m, p.k.uvu_sbar, "sobek_uvu_sbar")) ||
+      (rc = get_fn(m, p.k.uvu_ga, "sobek_uvu_ga")))
     return rc;
-  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0) {
+  return SOBEK_OK;
+}
+
+// the receiver-state route: state and adjoint edge kernels, channel GEMMs
+int load_receiver_route(Plan& p, hipModule_t m) {
+  int rc;
+  if ((rc = get_fn(m, p.k.fwd_S, "sobek_fwd_S")) || (rc = get_fn(m, p.k.fwd_dS, "sobek_fwd_dS")) ||
+      (rc = get_fn(m, p.k.fwd_dS_r, "sobek_fwd_dS_r")) || (rc = get_fn(m, p.k.bwd_E, "sobek_bwd_E")) ||
+      (rc = get_fn(m, p.k.dbwd_E, "sobek_dbwd_E")) || (rc = get_fn(m, p.k.dbwd_E_r, "sobek_dbwd_E_r")))
+    return rc;
+  const char* bns[3] = {"16", "32", "64"};
+  for (int b = 0; b < 3; ++b) {
+    std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
+                ga = std::string("sobek_gemm_ga_") + bns[b], sav = std::string("sobek_gemm_sa_v") + bns[b],
+                gav = std::string("sobek_gemm_ga_v") + bns[b];
+    if ((rc = get_fn(m, p.k.gemm_sa[b], sa.c_str())) || (rc = get_fn(m, p.k.gemm_sbar[b], sb.c_str())) ||
+        (rc = get_fn(m, p.k.gemm_ga[b], ga.c_str())) || (rc = get_fn(m, p.k.gemm_sa_v[b], sav.c_str())) ||
+        (rc = get_fn(m, p.k.gemm_ga_v[b], gav.c_str())))
+      return rc;
+  }
+  if ((rc = get_fn(m, p.k.gemm_sbar_v, "sobek_gemm_sbar_v"))) return rc;
+  if (p.vec4)
+    for (auto& g : p.groups)
+      if (sobek::sbar_streams(p.vec4, g.C) && !p.k.gemm_sbar_c.count(g.C)) {
+        std::string nm = "sobek_gemm_sbar_c" + std::to_string(g.C);
+        hipFunction_t f = nullptr;
+        if ((rc = get_fn(m, f, nm.c_str()))) return rc;
+        p.k.gemm_sbar_c[g.C] = f;
+      }
+  return SOBEK_OK;
+}
+
+// channelwise state-free kernels, with the route choice from their scratch and register use
+int load_uvu(Plan& p, hipModule_t m) {
+  int rc;
+  auto get = [&](hipFunction_t& f, const char* name) { return get_fn(m, f, name); };
     hipFunction_t bu = nullptr, bs = nullptr;
     if ((rc = get(p.k.uvu_fwd, "sobek_uvu_fwd")) || (rc = get(bu, "sobek_uvu_bwd_u")) ||
         (rc = get(bs, "sobek_uvu_bwd_s")))
@@ -703,25 +739,46 @@ int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
     HIPCHK(hipFuncGetAttribute(&st, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd_t));
     HIPCHK(hipFuncGetAttribute(&swt, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad_t));
     p.uvu_tan_direct = st == 0 && swt == 0;
+    return SOBEK_OK;
+}
+
+std::mutex g_rr_mu;
+
+// the receiver-route kernels of a channelwise plan, compiled and loaded on first use
+int ensure_receiver_route(sobek_plan plan) {
+  Plan& p = plan->p;
+  std::lock_guard<std::mutex> lk(g_rr_mu);
+  if (p.rr_loaded) return SOBEK_OK;
+  int rc;
+  if ((rc = load_module(p.source, p.k.module))) return rc;
+  if ((rc = load_receiver_route(p, p.k.module))) return rc;
+  p.rr_loaded = true;
+  return SOBEK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sobek_plan_create(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep* out, int n_out, int K, int mode,
+                      int layout, int dtype, int path_norm, sobek_plan* plan) {
+  if (!plan) return fail(SOBEK_E_INVALID, "plan output pointer is NULL");
+  *plan = nullptr;
+  std::unique_ptr<sobek_plan_s> h(new sobek_plan_s());
+  Plan& p = h->p;
+  int rc = build_signature(in, n_in, lmax, out, n_out, K, mode, layout, dtype, path_norm, p);
+  if (rc != SOBEK_OK) return rc;
+  // channelwise plans with the state-free kernels compile that part first; the
+  // receiver-route kernels follow on first use (ensure_receiver_route)
+  const bool split = !p.source_u.empty();
+  if ((rc = load_module(split ? p.source_u : p.source, split ? p.k.module_u : p.k.module))) return rc;
+  hipModule_t m0 = split ? p.k.module_u : p.k.module;
+  if ((rc = load_common(p, m0))) return rc;
+  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && (rc = load_uvu(p, m0))) return rc;
+  if (!split) {
+    if ((rc = load_receiver_route(p, p.k.module))) return rc;
+    p.rr_loaded = true;
   }
-  for (int b = 0; b < 3; ++b) {
-    std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
-                ga = std::string("sobek_gemm_ga_") + bns[b], sav = std::string("sobek_gemm_sa_v") + bns[b],
-                gav = std::string("sobek_gemm_ga_v") + bns[b];
-    if ((rc = get(p.k.gemm_sa[b], sa.c_str())) || (rc = get(p.k.gemm_sbar[b], sb.c_str())) ||
-        (rc = get(p.k.gemm_ga[b], ga.c_str())) || (rc = get(p.k.gemm_sa_v[b], sav.c_str())) ||
-        (rc = get(p.k.gemm_ga_v[b], gav.c_str())))
-      return rc;
-  }
-  if ((rc = get(p.k.gemm_sbar_v, "sobek_gemm_sbar_v"))) return rc;
-  if (p.vec4)
-    for (auto& g : p.groups)
-      if (sobek::sbar_streams(p.vec4, g.C) && !p.k.gemm_sbar_c.count(g.C)) {
-        std::string nm = "sobek_gemm_sbar_c" + std::to_string(g.C);
-        hipFunction_t f = nullptr;
-        if ((rc = get(f, nm.c_str()))) return rc;
-        p.k.gemm_sbar_c[g.C] = f;
-      }
   HIPCHK(hipMalloc(&p.d_ktab, std::max<size_t>(4, p.ktab.size() * 4)));
   HIPCHK(hipMemcpy(p.d_ktab, p.ktab.data(), p.ktab.size() * 4, hipMemcpyHostToDevice));
   auto blocks = [](const std::vector<sobek::Irrep>& v) {
@@ -748,7 +805,10 @@ int sobek_jit_compile(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
   int rc = build_signature(in, n_in, lmax, out, n_out, K, mode, layout, dtype, path_norm, p);
   if (rc != SOBEK_OK) return rc;
   try {
-    sobek::jit_compile(p.source);
+    if (!p.source_u.empty()) sobek::jit_compile(p.source_u);
+    // SOBEK_JIT_STATE_FREE_ONLY=1: channelwise plans compile only the part a plan loads at creation
+    const char* sf = std::getenv("SOBEK_JIT_STATE_FREE_ONLY");
+    if (p.source_u.empty() || !sf || std::strcmp(sf, "1") != 0) sobek::jit_compile(p.source);
   } catch (const std::exception& ex) {
     return fail(SOBEK_E_COMPILE, "%s", ex.what());
   }
@@ -816,6 +876,7 @@ int sobek_plan_destroy(sobek_plan plan) {
   if (p.d_in_blocks) (void)hipFree(p.d_in_blocks);
   if (p.d_out_blocks) (void)hipFree(p.d_out_blocks);
   if (p.k.module) (void)hipModuleUnload(p.k.module);
+  if (p.k.module_u) (void)hipModuleUnload(p.k.module_u);
   delete plan;
   return SOBEK_OK;
 }
@@ -973,6 +1034,7 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     ok = (float*)((char*)ws + w.off_out);
     if ((rc = transpose(p, x, (float*)xk, G.N, true, 0, stream))) return rc;
   }
+  if (!(p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && !state) && (rc = ensure_receiver_route(plan))) return rc;
   if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && !state) {
     // channelwise, one multiplicity: every receiver at once, no receiver state
     int r0 = 0, n = (int)G.N;
@@ -1015,6 +1077,7 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   // with it, A_bar comes from the edges directly (no receiver state; a kept S is not needed)
   const bool uvu_wg = uvu_direct && p.uvu_wgrad_direct;
   const bool need_slot = (gW && !state && !uvu_wg) || (!uvu_direct && !adj_state && (gx || gevec || gphi));
+  if ((!uvu_direct || (gW && !uvu_wg)) && (rc = ensure_receiver_route(plan))) return rc;
   if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false, need_slot ? 1 : 0))) return rc;
   if (gW) { if ((rc = fill_zero(p, gW, (int64_t)p.K * p.n_w, stream))) return rc; }
   if (G.N == 0) return SOBEK_OK;
@@ -1152,6 +1215,7 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
   // cotangent alone without receiver state: m_dot, g_W and the edge terms along Ydot = J evd
   const bool uvu_free = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct && p.uvu_wgrad_direct &&
                         p.uvu_tan_direct && flags == 4;
+  if (!uvu_free && (rc = ensure_receiver_route(plan))) return rc;
   // the second state slot (Sbar') is needed only with a dA cotangent
   if ((rc = plan_workspace(p, G, SOBEK_PASS_DBWD, ws_bytes, w, false, uvu_free ? 0 : (t_gW ? 2 : 1)))) return rc;
   const bool tan = flags & 7;

@@ -1378,7 +1378,7 @@ void emit_uvu_wgrad(std::ostringstream& o, const Plan& P, bool tan) {
   o << "  }\n}\n";
 }
 
-std::string generate_source(const Plan& P) {
+std::string generate_source(const Plan& P, bool receiver_route) {
   std::ostringstream o;
   o.precision(17);
   o << "\n// ---- generated for: K=" << P.K << " lmax=" << P.lmax << " in=";
@@ -1417,6 +1417,7 @@ std::string generate_source(const Plan& P) {
        "  (void)CX;\n"
        "  sb_sender_reduce<CXI>(send_rowptr, send_perm, contrib, gx, cursor, N, e0, e1, first);\n"
        "}\n";
+  if (!receiver_route) return o.str();
 
   // forward S / dS kernels: one wave per (receiver, unit)
   for (int t = 0; t < (int)P.fwd_units.size(); ++t) emit_fwd_unit(o, P, P.fwd_units[t], t);

@@ -76,7 +76,9 @@ inline bool sbar_streams(bool vec4, int C) { return vec4 && C <= 256; }
 constexpr int kUvuWaves = 256;
 
 struct Kernels {
-  hipModule_t module = nullptr;
+  hipModule_t module = nullptr;    // every kernel of the plan (for channelwise plans with the
+                                   // state-free kernels: the receiver-route kernels, loaded on first use)
+  hipModule_t module_u = nullptr;  // channelwise plans: the state-free kernels and the common ones
   hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, fwd_dS_r = nullptr;
   hipFunction_t bwd_E = nullptr, dbwd_E = nullptr, dbwd_E_r = nullptr;
   hipFunction_t gemm_sa[3] = {}, gemm_sbar[3] = {}, gemm_ga[3] = {};  // BN = 16, 32, 64
@@ -118,6 +120,8 @@ struct Plan {
   std::vector<int> dead_in;     // input irreps no path reads (their gradients are zero)
   std::vector<int> dead_out;    // output irreps no path writes (their outputs are zero)
   std::string source;           // generated HIP source
+  std::string source_u;         // channelwise plans with the state-free kernels: that part alone
+  bool rr_loaded = false;       // the receiver-route kernels are loaded
   std::string cache_key;
   Kernels k;
   // device tables
@@ -129,6 +133,6 @@ struct Plan {
 // Builds paths, groups, units and slabs for a validated signature.
 void build_plan(Plan& p);
 // Generates the plan-specific HIP source (prepended by the shared prelude at compile time).
-std::string generate_source(const Plan& p);
+std::string generate_source(const Plan& p, bool receiver_route = true);
 
 }  // namespace sobek
