@@ -209,11 +209,13 @@ int nsplit_for(const sobek::Group& g, int64_t nrows, bool vec4) {
 
 // split partials of the weight-gradient GEMMs: one region per output group,
 // accumulated over the receiver chunks of a pass and reduced once at its end
-size_t partial_floats(const Plan& p, int64_t ncap, int pass = SOBEK_PASS_BWD) {
+size_t partial_floats(const Plan& p, int64_t ncap, int pass = SOBEK_PASS_BWD, int nstate = -1) {
   // the state-free channelwise weight gradient: one partial row of K * N_w floats per wave
-  // (the double backward may also take the receiver route: room for both)
+  // (a double backward planned with receiver state may take either route: room for both;
+  // one planned without takes the state-free route)
   const bool free = p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && p.uvu_wgrad_direct;
-  if (pass == SOBEK_PASS_BWD && free) return (size_t)sobek::kUvuWaves * p.K * p.n_w;
+  if ((pass == SOBEK_PASS_BWD || (pass == SOBEK_PASS_DBWD && nstate == 0)) && free)
+    return (size_t)sobek::kUvuWaves * p.K * p.n_w;
   size_t m = 0;
   for (auto& g : p.groups) m += (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C;
   if (pass == SOBEK_PASS_DBWD && free) m = std::max(m, (size_t)sobek::kUvuWaves * p.K * p.n_w);
@@ -282,16 +284,28 @@ void pass_costs(const Plan& p, const sobek_graph_s& G, int pass, int nstate, WsP
   per_edge = pass == SOBEK_PASS_FWD ? 0 : (size_t)(p.dim_in + uvu_edge_partials(p, pass)) * 4;
 }
 
+// The state-free channelwise weight gradient (backward, and the double backward planned
+// without receiver state) writes and reduces its partial rows before the first edge window:
+// they share the region of the per-edge contributions.
+bool partials_share_contrib(const Plan& p, const WsPlan& w, int pass) {
+  const bool free = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct && p.uvu_wgrad_direct;
+  return free && (pass == SOBEK_PASS_BWD || (pass == SOBEK_PASS_DBWD && w.nstate == 0));
+}
+
 size_t layout_total(const Plan& p, WsPlan& w, int pass) {
   size_t o = w.fixed;
-  if (pass != SOBEK_PASS_FWD) o = align_up(o + partial_floats(p, w.ncap, pass) * 4);
+  const bool share = partials_share_contrib(p, w, pass);
+  const size_t pbytes = pass != SOBEK_PASS_FWD ? partial_floats(p, w.ncap, pass, w.nstate) * 4 : 0;
+  if (!share) o = align_up(o + pbytes);
   w.off_K = o;  // w.kfloats is set by the planner
   o = align_up(o + w.kfloats * 4);
   w.off_state = o;
   o = align_up(o + (size_t)w.nstate * w.ncap * p.srow * 4);
   w.off_contrib = o;
-  if (pass != SOBEK_PASS_FWD) o = align_up(o + (size_t)w.ecap * (p.dim_in + uvu_edge_partials(p, pass)) * 4);
-  return o;
+  w.off_P = share ? o : w.fixed;
+  size_t cbytes = pass != SOBEK_PASS_FWD ? (size_t)w.ecap * (p.dim_in + uvu_edge_partials(p, pass)) * 4 : 0;
+  if (share) cbytes = std::max(cbytes, pbytes);
+  return align_up(o + cbytes);
 }
 
 // nstate: receiver-state slots per receiver (-1: the pass's general need; the
@@ -325,7 +339,7 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
     // GEMM partials (weight-gradient splits, state-GEMM split-K) of chunks of nc receivers
     auto partial_bytes = [&](int64_t nc) -> size_t {
       nc = std::max<int64_t>(1, nc);
-      return (pass != SOBEK_PASS_FWD ? align_up(partial_floats(p, nc, pass) * 4) + kAlign : 0) +
+      return (pass != SOBEK_PASS_FWD ? align_up(partial_floats(p, nc, pass, w.nstate) * 4) + kAlign : 0) +
              align_up(sa_split_floats(p, pass, nc) * 4) + kAlign;
     };
     auto total_at = [&](int64_t nc, int64_t ec, size_t kf) {
@@ -360,7 +374,17 @@ int plan_workspace(const Plan& p, const sobek_graph_s& G, int pass, size_t ws_by
         c.kf = w.kfloats;
       }
       c.ec = ec0;
-      if (per_edge) {
+      if (per_edge && partials_share_contrib(p, w, pass)) {
+        // the largest window that fits (the shared region is not additive in ec)
+        int64_t lo = ec0, hi = eall;
+        if (total_at(nc, hi, c.kf) <= ws_bytes) lo = hi;
+        while (hi - lo > 1) {
+          const int64_t mid = lo + (hi - lo) / 2;
+          (total_at(nc, mid, c.kf) <= ws_bytes ? lo : hi) = mid;
+        }
+        c.ec = lo;
+        c.need = total_at(nc, lo, c.kf);
+      } else if (per_edge) {
         int64_t ec = std::min<int64_t>(eall, ec0 + (int64_t)((ws_bytes - c.need) / per_edge));
         while (ec > ec0 && total_at(nc, ec, c.kf) > ws_bytes) ec = std::max<int64_t>(ec0, ec - 64);
         c.ec = ec;
