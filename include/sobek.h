@@ -69,7 +69,7 @@ typedef enum sobek_status {
 } sobek_status;
 
 enum { SOBEK_LAYOUT_IR_MUL = 0, SOBEK_LAYOUT_MUL_IR = 1 };
-enum { SOBEK_DTYPE_F32 = 0 };
+enum { SOBEK_DTYPE_F32 = 0, SOBEK_DTYPE_BF16_GEMM = 1 };
 enum { SOBEK_NORM_NONE = 0, SOBEK_NORM_FAN_IN = 1 };
 enum { SOBEK_MODE_UVW = 0, SOBEK_MODE_UVU = 1 };
 enum { SOBEK_PASS_FWD = 0, SOBEK_PASS_BWD = 1, SOBEK_PASS_DBWD = 2 };
@@ -94,7 +94,15 @@ int sobek_version(void);
  *         SOBEK_MODE_UVU, channelwise (eq. uvu_connection): every path needs
  *         C_out = C_in (else SOBEK_E_INVALID) and owns C_in weights,
  *         W[q][w_off + u], output channel u = input channel u.
- *   layout: SOBEK_LAYOUT_*.  dtype: SOBEK_DTYPE_F32.
+ *   layout: SOBEK_LAYOUT_*.
+ *   dtype: SOBEK_DTYPE_F32, fp32 throughout (the paper's precision, Section 5.1);
+ *          SOBEK_DTYPE_BF16_GEMM, a reduced-precision option for uvw plans whose
+ *          multiplicities are all multiples of 4 (else SOBEK_E_UNSUPPORTED): the
+ *          channel GEMM m = S A (Section 4.2 eq. receiver_matrix_product; the
+ *          forward, and the double backward's products with S and dS) rounds S
+ *          and A to bf16 (nearest even) and accumulates in fp32 on bf16 MFMA.
+ *          Every tensor at this boundary stays fp32; the edge stage, the
+ *          backward's GEMMs and every reduction stay fp32.
  *   (uvu plans whose paths share one multiplicity run a forward and backward
  *   without receiver state; the environment variable SOBEK_UVU_ROUTE=receiver,
  *   read at plan creation, keeps them on the receiver-state route instead.)

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libsobek_hip.so")
 LAYOUTS = {"ir_mul": 0, "mul_ir": 1}
 NORMS = {"none": 0, "fan_in": 1}
 MODES = {"uvw": 0, "uvu": 1}
+DTYPES = {"f32": 0, "bf16_gemm": 1}
 PASSES = {"fwd": 0, "bwd": 1, "dbwd": 2}
 STATUS = {0: "OK", -1: "INVALID", -2: "UNSUPPORTED", -3: "SHAPE", -4: "ALIGN", -5: "WORKSPACE",
           -6: "HIP", -7: "INTERNAL", -8: "COMPILE"}
@@ -124,20 +125,20 @@ def irrep_array(spec):
     return arr, len(v)
 
 
-def _sig_args(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
+def _sig_args(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw", dtype="f32"):
     a, na = irrep_array(irreps_in)
     b, nb = irrep_array(irreps_out)
-    return (a, na, int(lmax), b, nb, int(K), MODES[mode], LAYOUTS[layout], 0, NORMS[normalization])
+    return (a, na, int(lmax), b, nb, int(K), MODES[mode], LAYOUTS[layout], DTYPES[dtype], NORMS[normalization])
 
 
-def jit_compile(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
+def jit_compile(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw", dtype="f32"):
     """Generate and compile the kernels of a signature into the code-object cache (no GPU needed)."""
-    check(lib().sobek_jit_compile(*_sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode)))
+    check(lib().sobek_jit_compile(*_sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode, dtype)))
 
 
-def plan_source(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
+def plan_source(irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw", dtype="f32"):
     """The full HIP source compiled for a signature."""
-    args = _sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode)
+    args = _sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode, dtype)
     need = _SZ(0)
     check(lib().sobek_plan_source(*args, None, 0, ctypes.byref(need)))
     buf = ctypes.create_string_buffer(need.value)

@@ -41,14 +41,16 @@ def _check_tensor(t, name, shape, dtype=torch.float32):
 
 class Plan:
     """Operator signature: irreps, spherical-harmonic order, radial width, channel mode ("uvw" fully
-    connected, "uvu" channelwise)."""
+    connected, "uvu" channelwise), dtype ("f32", or "bf16_gemm": the channel GEMM m = S A on bf16
+    MFMA with fp32 accumulation; tensors stay fp32)."""
 
-    def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw"):
+    def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw",
+                 dtype="f32"):
         self.irreps_in = _lib.parse_irreps(irreps_in)
         self.irreps_out = _lib.parse_irreps(irreps_out)
         self.lmax, self.K, self.layout, self.normalization = int(lmax), int(K), layout, normalization
-        self.mode = mode
-        args = _lib._sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode)
+        self.mode, self.dtype = mode, dtype
+        args = _lib._sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode, dtype)
         h = _P()
         check(lib().sobek_plan_create(*args, ctypes.byref(h)))
         self._h = h

@@ -2,7 +2,8 @@
 
 1. Embed csrc/device/prelude.hip (hand-written device code) into the library as
    a string; the library prepends it to every generated plan and compiles the
-   result with hipRTC for gfx950.
+   result with hipRTC for gfx950.  csrc/device/gemm_bf16.hip is embedded the same
+   way and appended to the plans built with the bf16 GEMM option.
 2. Compile the host runtime (C ABI, plan builder, kernel generator, hipRTC
    driver) into paper_2607_18074_amd/libsobek_hip.so.
 3. Optionally pre-compile the kernels of the given operator signatures into the
@@ -24,17 +25,21 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 SOURCES = ["api.cpp", "plan.cpp", "tables.cpp", "jit.cpp"]
 
 
-def embed_prelude():
-    src = os.path.join(CSRC, "device", "prelude.hip")
+def _embed(name, delim):
+    src = os.path.join(CSRC, "device", name + ".hip")
     with open(src) as f:
         text = f.read()
-    delim = "SOBEKPRELUDE"
     assert f"){delim}\"" not in text
-    out = os.path.join(CSRC, "prelude_embed.inc")
+    out = os.path.join(CSRC, name + "_embed.inc")
     content = f'R"{delim}(\n{text}\n){delim}"\n'
     if not os.path.exists(out) or open(out).read() != content:
         with open(out, "w") as f:
             f.write(content)
+
+
+def embed_prelude():
+    _embed("prelude", "SOBEKPRELUDE")
+    _embed("gemm_bf16", "SOBEKBF16")
 
 
 def build_library(verbose=False):

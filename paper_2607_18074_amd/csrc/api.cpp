@@ -150,7 +150,9 @@ int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep
   if (lmax > 3) return fail(SOBEK_E_UNSUPPORTED, "lmax %d > 3 not supported", lmax);
   if (K < 1 || K > 64) return fail(SOBEK_E_INVALID, "K = %d outside [1, 64]", K);
   if (layout != SOBEK_LAYOUT_IR_MUL && layout != SOBEK_LAYOUT_MUL_IR) return fail(SOBEK_E_INVALID, "bad layout");
-  if (dtype != SOBEK_DTYPE_F32) return fail(SOBEK_E_UNSUPPORTED, "only SOBEK_DTYPE_F32 is implemented");
+  if (dtype != SOBEK_DTYPE_F32 && dtype != SOBEK_DTYPE_BF16_GEMM) return fail(SOBEK_E_INVALID, "bad dtype");
+  if (dtype == SOBEK_DTYPE_BF16_GEMM && mode != SOBEK_MODE_UVW)
+    return fail(SOBEK_E_UNSUPPORTED, "SOBEK_DTYPE_BF16_GEMM is implemented for uvw plans only");
   if (norm != SOBEK_NORM_NONE && norm != SOBEK_NORM_FAN_IN) return fail(SOBEK_E_INVALID, "bad path normalisation");
   if (mode != SOBEK_MODE_UVW && mode != SOBEK_MODE_UVU) return fail(SOBEK_E_INVALID, "bad mode");
   p.lmax = lmax; p.K = K; p.layout = layout; p.dtype = dtype; p.norm = norm; p.mode = mode;
@@ -162,6 +164,8 @@ int build_signature(const sobek_irrep* in, int n_in, int lmax, const sobek_irrep
     return fail(SOBEK_E_UNSUPPORTED, "plan: %s", ex.what());
   }
   if (p.paths.empty()) return fail(SOBEK_E_INVALID, "no path satisfies the selection rules");
+  if (dtype == SOBEK_DTYPE_BF16_GEMM && !p.vec4)
+    return fail(SOBEK_E_UNSUPPORTED, "SOBEK_DTYPE_BF16_GEMM needs every multiplicity a multiple of 4");
   // SOBEK_UVU_ROUTE=receiver keeps channelwise plans on the receiver-state route (testing and
   // comparison); the state-free kernels are then not generated
   if (const char* r = std::getenv("SOBEK_UVU_ROUTE"))
@@ -707,7 +711,8 @@ int load_receiver_route(Plan& p, hipModule_t m) {
   const char* bns[3] = {"16", "32", "64"};
   for (int b = 0; b < 3; ++b) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
-                ga = std::string("sobek_gemm_ga_") + bns[b], sav = std::string("sobek_gemm_sa_v") + bns[b],
+                ga = std::string("sobek_gemm_ga_") + bns[b],
+                sav = std::string(p.dtype == SOBEK_DTYPE_BF16_GEMM ? "sobek_gemm_sa_vb" : "sobek_gemm_sa_v") + bns[b],
                 gav = std::string("sobek_gemm_ga_v") + bns[b];
     if ((rc = get_fn(m, p.k.gemm_sa[b], sa.c_str())) || (rc = get_fn(m, p.k.gemm_sbar[b], sb.c_str())) ||
         (rc = get_fn(m, p.k.gemm_ga[b], ga.c_str())) || (rc = get_fn(m, p.k.gemm_sa_v[b], sav.c_str())) ||

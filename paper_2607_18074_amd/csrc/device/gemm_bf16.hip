@@ -1,0 +1,123 @@
+// Channel GEMM m_g = S_g A_g on bf16 MFMA, for plans built with the dtype
+// SOBEK_DTYPE_BF16_GEMM (Section 4.2 eq. receiver_matrix_product, the product
+// the paper runs as an fp32 GEMM).  The generator appends this file to the
+// plan's source only for such plans; it relies on the fp32 device code that
+// precedes every plan (sb_gemm_sa_v's tiling constants, loads and row mapping).
+//
+// Same blocking and staging as sb_gemm_sa_v: a 128-row x BN-column block, four
+// waves of 32 rows, 32-deep k slabs of S and A staged in LDS as fp32 and the
+// next slab prefetched into registers.  Each 16x16 tile then takes one
+// v_mfma_f32_16x16x32_bf16 per slab instead of eight v_mfma_f32_16x16x4_f32:
+// the lane's eight k values of S and of A are rounded to bf16 (round to nearest
+// even, v_cvt_pk_bf16_f32) as they leave LDS, and products accumulate in fp32.
+//
+// Operand layout of v_mfma_f32_16x16x32_bf16 (lane l of the wave): A row
+// (l & 15) and B column (l & 15) supply the eight k values of slot group
+// l >> 4; both operands use the same slot for the same k, so the tile sums
+// S[i][k] A[k][j] over the 32 k of the slab.  D[4g + r][j] sits in accumulator
+// register r of lane j + 16g, as for the fp32 instruction.
+
+typedef __bf16 sb_b8 __attribute__((ext_vector_type(8)));
+
+template <int BN>
+SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const float* __restrict__ W,
+                          const int* __restrict__ ktab, float* __restrict__ out, int dg, int Cg, int off, int CX,
+                          int r0, int accumulate, float* __restrict__ P, int kper) {
+  __shared__ float sA[SB_VK][SB_VM + 4];
+  __shared__ float sB[SB_VK][BN + 4];
+  static_assert(SB_VK == 32, "one 32-deep bf16 MFMA per slab");
+  constexpr int NB = (SB_VK * BN / 4 + 255) / 256;  // float4 loads of B per thread
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int rb = blockIdx.x * SB_VM, cb = blockIdx.y * BN;
+  const int kbeg = blockIdx.z * kper, kend = min(D, kbeg + kper);
+  const int kg = 8 * (lane >> 4), li = lane & 15;
+  sb_f4 acc[2][BN / 16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t) acc[i][t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  sb_v4 ra[4], rbv[NB];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (tid >> 3) + 32 * i, k = k0 + 4 * (tid & 7);
+      const int gr = rb + row;
+      ra[i] = (gr < nrows && k < kend) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      const int kk = idx / (BN / 4), c = 4 * (idx % (BN / 4));
+      const int gk = k0 + kk;
+      rbv[i] = (idx < SB_VK * BN / 4 && gk < kend && cb + c < Cg) ? sb_ld4(W + (sb_i64)ktab[gk] + cb + c)
+                                                                : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (tid >> 3) + 32 * i, kq = 4 * (tid & 7);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) sA[kq + c][row] = ra[i][c];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < SB_VK * BN / 4) *(sb_v4*)&sB[idx / (BN / 4)][4 * (idx % (BN / 4))] = rbv[i];
+    }
+  };
+  load(kbeg);
+  store();
+  __syncthreads();
+  for (int k0 = kbeg; k0 < kend; k0 += SB_VK) {
+    const bool more = k0 + SB_VK < kend;
+    if (more) load(k0 + SB_VK);
+    sb_b8 a0, a1;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      a0[j] = (__bf16)sA[kg + j][32 * wave + li];
+      a1[j] = (__bf16)sA[kg + j][32 * wave + 16 + li];
+    }
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t) {
+      sb_b8 b;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) b[j] = (__bf16)sB[kg + j][16 * t + li];
+      acc[0][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b, acc[0][t], 0, 0, 0);
+      acc[1][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b, acc[1][t], 0, 0, 0);
+    }
+    __syncthreads();
+    if (more) {
+      store();
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb + 32 * wave + 16 * i + 4 * (lane >> 4) + r;
+        const int col = cb + 16 * t + li;
+        if (row < nrows && col < Cg) {
+          if (gridDim.z > 1) {  // partial of this split: P[z][row][col], summed by sobek_sa_reduce
+            P[((sb_i64)blockIdx.z * nrows + row) * Cg + col] = acc[i][t][r];
+          } else {
+            float* o = out + sb_row_addr(row, dg, Cg, off, CX, r0) + col;
+            *o = accumulate ? (*o + acc[i][t][r]) : acc[i][t][r];
+          }
+        }
+      }
+}
+
+#define SB_GEMM_VB_ENTRY(BN)                                                                         \
+  extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sa_vb##BN(                           \
+      const float* S, int nrows, int D, const float* W, const int* ktab, float* out, int dg,       \
+      int Cg, int off, int CX, int r0, int accumulate, float* P, int kper) {                       \
+    sb_gemm_sa_vb<BN>(S, nrows, D, W, ktab, out, dg, Cg, off, CX, r0, accumulate, P, kper);        \
+  }
+
+SB_GEMM_VB_ENTRY(16)
+SB_GEMM_VB_ENTRY(32)
+SB_GEMM_VB_ENTRY(64)

@@ -17,6 +17,11 @@
 namespace sobek {
 
 namespace {
+// device/gemm_bf16.hip, embedded by the build
+const char* kGemmBf16 =
+#include "gemm_bf16_embed.inc"
+    ;
+
 constexpr int kAccMax = 128;        // forward accumulators per lane per wave unit
 constexpr int kFetchRing = 2;       // forward edge-data register sets in flight
 constexpr int kSlabFloats = 10240;  // backward LDS budget for one slab of adjoint state (40 KiB)
@@ -1418,6 +1423,8 @@ std::string generate_source(const Plan& P, bool receiver_route) {
        "  sb_sender_reduce<CXI>(send_rowptr, send_perm, contrib, gx, cursor, N, e0, e1, first);\n"
        "}\n";
   if (!receiver_route) return o.str();
+  // reduced-precision plans: the bf16 variant of the vec4 channel GEMM
+  if (P.dtype == 1) o << kGemmBf16;
 
   // forward S / dS kernels: one wave per (receiver, unit)
   for (int t = 0; t < (int)P.fwd_units.size(); ++t) emit_fwd_unit(o, P, P.fwd_units[t], t);
