@@ -119,8 +119,9 @@ def time_pass(fn, torch):
     return float(np.median(samples)), len(samples)
 
 
-def sweep(budget_gib, names):
-    """Every workload and pass of the benchmark configurations: one JSON line each, then a table."""
+def sweep(budget_gib, names, dtype="f32"):
+    """Every workload and pass of the benchmark configurations: one JSON line each, then a table.
+    dtype "bf16_gemm" runs the plans' channel GEMM m = S A on bf16 MFMA (tensors stay fp32)."""
     import torch
 
     from paper_2607_18074_amd import api
@@ -131,7 +132,7 @@ def sweep(budget_gib, names):
     for name in names:
         cfg = wl.CONFIGS[name]
         g = wl.config_graph(name)
-        plan = api.Plan(cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"])
+        plan = api.Plan(cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"], dtype=dtype)
         T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
         graph = api.Graph(T(g.rowptr), T(g.sender))
         xt = T(wl.node_features(g.N, plan.dim_in, cfg["index"]))
@@ -170,7 +171,8 @@ def sweep(budget_gib, names):
             ms, n = time_pass(fns[pname], torch)
             tf = fm["passes"][pname] / (ms * 1e-3) / 1e12
             gbs = bm[pname] / (ms * 1e-3) / 1e9
-            row = dict(workload=name, pass_=pname, N=g.N, E=g.E, ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3),
+            row = dict(workload=name if dtype == "f32" else f"{name} ({dtype})", dtype=dtype, pass_=pname,
+                       N=g.N, E=g.E, ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3),
                        tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS, alg_gbs=gbs, frac_hbm=gbs / PEAK_HBM_GBS,
                        peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9,
                        workspace_gb=ws[pname].numel() / 1e9,
@@ -394,6 +396,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", default="", help="comma-separated workloads (or 'all'): time every pass of each "
                     "with the paper's protocol instead of the step benchmark, one JSON line per pass")
+    ap.add_argument("--dtype", default="f32", choices=["f32", "bf16_gemm"],
+                    help="sweep: plan dtype (bf16_gemm: the channel GEMM m = S A on bf16 MFMA)")
     ap.add_argument("--regimes", default="", help="'degree', 'count' or 'all': the paper's scaling regimes on its "
                     "profiles (--profiles), one JSON line per point and pass")
     ap.add_argument("--profiles", default="128/64,128/64/64,128/64/64/64")
@@ -430,7 +434,7 @@ def main():
         return
     if args.sweep:
         names = ["tiny", "small", "medium", "wide", "stress"] if args.sweep == "all" else args.sweep.split(",")
-        sweep(args.budget, names)
+        sweep(args.budget, names, args.dtype)
         return
 
     import torch
