@@ -100,3 +100,44 @@ def test_bf16_double_backward(gpu, sig, N, E, seed, iso):
         print(f"bf16 dbwd {sig} {name}: {err:.2e}")
         # g_gout is built from m = S A products; the rest from the fp32 adjoint kernels
         assert err <= (BF16_TOL if name == "g_gout" else BWD_TOL), name
+
+
+@pytest.mark.timeout(600)
+def test_bf16_full_size_wide(gpu):
+    """The Wide workload at full size (50,000 nodes, 2.0M edges) in the benchmark's launch
+    configuration (8 GiB workspace, several receiver chunks): forward m and the double backward's
+    g_gout at sampled receivers against the oracle on their in-edges."""
+    import torch
+    from paper_2607_18074_amd import api
+    from paper_2607_18074_amd import workloads as wl
+    from tests.cases import edge_subgraph, in_edges, std_for
+
+    cfg = wl.CONFIGS["wide"]
+    sig = (cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"])
+    g = wl.config_graph("wide")
+    std = std_for(cfg["irreps_in"], cfg["irreps_out"], cfg["lmax"], cfg["K"])
+    prob = oc.Problem(*sig)
+    x = wl.node_features(g.N, prob.dim_in, cfg["index"])
+    W = wl.weights(cfg["K"], std, cfg["index"])
+    gout = wl.out_cotangent(g.N, prob.dim_out, cfg["index"])
+    rdot = wl.cotangents(g.N, g.E, cfg["K"], prob.dim_in, len(std), cfg["index"], which=("evec",))["evec"]
+    R = np.sort(np.random.default_rng(2000 + cfg["index"]).choice(g.N, size=8, replace=False))
+    print(f"wide bf16: N={g.N} E={g.E}, receivers {R.tolist()}", flush=True)
+
+    plan = api.Plan(*sig, dtype="bf16_gemm")
+    graph = api.Graph(_t(g.rowptr), _t(g.sender))
+    args = (_t(x), _t(g.evec), _t(g.phi), _t(W))
+    m = _n(api.conv_fwd(plan, graph, *args, budget=8 << 30))
+    gg = _n(api.conv_dbwd(plan, graph, *args, _t(gout), t_gevec=_t(rdot), budget=8 << 30,
+                          need=(True, False, False, False, False))[0])
+    del args, graph
+    torch.cuda.empty_cache()
+
+    A = in_edges(g, R)
+    rp, snd, ev, ph, rec = edge_subgraph(g, A)
+    oa = (prob, x, ev, ph, W, rp, snd)
+    for name, got, ref in (("fwd m", m[rec], oc.fwd(*oa)),
+                           ("dbwd g_gout", gg[rec], oc.dbwd(*oa, gout[rec], t_gevec=rdot[A])["g_gout"])):
+        err = max_rel(got, ref)
+        print(f"  {name}: max rel err {err:.2e}", flush=True)
+        assert err <= BF16_TOL, name
