@@ -215,14 +215,12 @@ int nsplit_for(const sobek::Group& g, int64_t nrows, bool vec4) {
 // accumulated over the receiver chunks of a pass and reduced once at its end
 size_t partial_floats(const Plan& p, int64_t ncap, int pass = SOBEK_PASS_BWD, int nstate = -1) {
   // the state-free channelwise weight gradient: one partial row of K * N_w floats per wave
-  // (a double backward planned with receiver state may take either route: room for both;
-  // one planned without takes the state-free route)
+  // (the backward, and a double backward planned without receiver state, take that route)
   const bool free = p.mode == SOBEK_MODE_UVU && p.uvu_bwd_direct && p.uvu_wgrad_direct;
   if ((pass == SOBEK_PASS_BWD || (pass == SOBEK_PASS_DBWD && nstate == 0)) && free)
-    return (size_t)sobek::kUvuWaves * p.K * p.n_w;
+    return (size_t)sobek::uvu_wgrad_waves(p.K, p.n_w) * p.K * p.n_w;
   size_t m = 0;
   for (auto& g : p.groups) m += (size_t)nsplit_for(g, ncap * g.d, p.vec4) * g.D * g.C;
-  if (pass == SOBEK_PASS_DBWD && free) m = std::max(m, (size_t)sobek::kUvuWaves * p.K * p.n_w);
   return m;
 }
 
@@ -1032,8 +1030,18 @@ int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t bu
   if (!plan || !graph || !bytes) return fail(SOBEK_E_INVALID, "NULL argument");
   if (pass < SOBEK_PASS_FWD || pass > SOBEK_PASS_DBWD) return fail(SOBEK_E_INVALID, "bad pass");
   WsPlan w;
-  plan_workspace(plan->p, *graph, pass, budget ? budget : default_budget(), w, true);
+  const size_t b = budget ? budget : default_budget();
+  plan_workspace(plan->p, *graph, pass, b, w, true);
   *bytes = w.total;
+  // a channelwise double backward may take the state-free route (edge-vector cotangent
+  // alone): room for its layout too
+  const Plan& p = plan->p;
+  if (pass == SOBEK_PASS_DBWD && p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct &&
+      p.uvu_wgrad_direct) {
+    WsPlan w0;
+    plan_workspace(p, *graph, pass, b, w0, true, 0);
+    *bytes = std::max(*bytes, w0.total);
+  }
   return SOBEK_OK;
 }
 
@@ -1135,10 +1143,10 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
       for (auto& q : p.paths)
         if (q.i_in == (int)a) { ++na; break; }
     float* P = (float*)((char*)ws + w.off_P);
-    int rows = sobek::kUvuWaves;
+    int rows = sobek::uvu_wgrad_waves(p.K, p.n_w);
     long long nw = (long long)p.K * p.n_w;
-    LAUNCH(p.k.uvu_wgrad, sobek::kUvuWaves / 4, p.uvu_NB, na, stream, (const int*)G.rowptr, (const int*)G.sender,
-           evec, phi, xk, gk, P, n, (const float*)nullptr);
+    LAUNCH(p.k.uvu_wgrad, rows / 4, p.uvu_NB, na, stream, (const int*)G.rowptr, (const int*)G.sender,
+           evec, phi, xk, gk, P, n, (const float*)nullptr, rows);
     LAUNCH(p.k.uvu_wreduce, cdiv(nw, 256), 1, 1, stream, (const float*)P, rows, nw, gW);
   }
   if (adj_state && (rc = run_sbar(p, all, G.N, gk, W, adj_state, stream))) return rc;
@@ -1275,10 +1283,10 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
     }
     if (g_W) {
       float* P = (float*)((char*)ws + w.off_P);
-      int rows = sobek::kUvuWaves;
+      int rows = sobek::uvu_wgrad_waves(p.K, p.n_w);
       long long nw = (long long)p.K * p.n_w;
-      LAUNCH(p.k.uvu_wgrad_t, sobek::kUvuWaves / 4, p.uvu_NB, p.uvu_NA, stream, (const int*)G.rowptr,
-             (const int*)G.sender, evec, phi, xk, gk, P, n, t_gevec);
+      LAUNCH(p.k.uvu_wgrad_t, rows / 4, p.uvu_NB, p.uvu_NA, stream, (const int*)G.rowptr,
+             (const int*)G.sender, evec, phi, xk, gk, P, n, t_gevec, rows);
       LAUNCH(p.k.uvu_wreduce, cdiv(nw, 256), 1, 1, stream, (const float*)P, rows, nw, g_W);
     }
     float* contrib = g_x ? (float*)((char*)ws + w.off_contrib) : nullptr;

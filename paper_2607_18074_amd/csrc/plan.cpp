@@ -1304,8 +1304,8 @@ void emit_uvu_bwd(std::ostringstream& o, const Plan& P, bool sliced, bool tan) {
 
 // Channelwise weight gradient without receiver state: A_bar[q, path, u] is the sum
 // over all edges of phi_e[q] h_e[path, u], h = <mbar_i[u], C_path[u]> (tied channel).
-// Grid (UVU_WAVES / 4, 64-channel blocks, input irreps with paths): wave w of the
-// slice (input irrep a, channel block) takes receivers w, w + UVU_WAVES, ... and
+// Grid (nwv / 4, 64-channel blocks, input irreps with paths): wave w of the
+// slice (input irrep a, channel block) takes receivers w, w + nwv, ... and
 // keeps K accumulators per path of a and channel in registers; each wave writes
 // its own partial row part[w][q * N_w + w_off + u], which sobek_uvu_wreduce adds
 // in wave order.
@@ -1319,11 +1319,10 @@ void emit_uvu_wgrad(std::ostringstream& o, const Plan& P, bool tan) {
   for (size_t a = 0; a < P.in.size(); ++a)
     for (auto& q : P.paths)
       if (q.i_in == (int)a) { ins.push_back((int)a); break; }
-  if (!tan) o << "#define UVU_WAVES " << kUvuWaves << "\n";
   o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_uvu_wgrad" << (tan ? "_t" : "") << "(const int* __restrict__ rowptr,"
        " const int* __restrict__ sender, const float* __restrict__ evec, const float* __restrict__ phi,"
        " const float* __restrict__ x, const float* __restrict__ Mb, float* __restrict__ part, int n_recv,"
-       " const float* __restrict__ evd) {\n"
+       " const float* __restrict__ evd, int nwv) {\n"
     << "  constexpr int C_ = " << C << ", UB_ = " << UBP << ", ES_ = " << ES << ";\n"
     << "  const int cb = blockIdx.y, lane = threadIdx.x & 63, wv = blockIdx.x * 4 + (threadIdx.x >> 6);\n"
     << "  const int sub = lane / UB_, u = lane % UB_, uc = cb * UB_ + u;\n"
@@ -1341,7 +1340,7 @@ void emit_uvu_wgrad(std::ostringstream& o, const Plan& P, bool tan) {
       }
     o << "  case " << ia << ": {\n";
     for (int t : ts) o << "    float acc" << t << "[K];\n#pragma unroll\n    for (int q = 0; q < K; ++q) acc" << t << "[q] = 0.f;\n";
-    o << "    for (int r = wv; r < n_recv; r += UVU_WAVES) {\n"
+    o << "    for (int r = wv; r < n_recv; r += nwv) {\n"
          "      const sb_i64 mrow = (sb_i64)r * CXO + uc;\n";
     for (int g : gs)
       o << "      float mb" << g << "[" << P.groups[g].d << "];\n#pragma unroll\n      for (int m = 0; m < "

@@ -72,8 +72,14 @@ struct AdjSlab {
 // the tiled sobek_gemm_sbar_64.
 inline bool sbar_streams(bool vec4, int C) { return vec4 && C <= 256; }
 
-// waves (partial rows) per slice of the state-free channelwise weight gradient
-constexpr int kUvuWaves = 256;
+// waves per slice of the state-free channelwise weight gradient, each writing one partial
+// row of K * N_w floats: up to 1024 for occupancy, halved while the rows exceed 96 MiB (they
+// share the per-edge contribution region of the workspace)
+inline int uvu_wgrad_waves(int K, int64_t n_w) {
+  int w = 1024;
+  while (w > 64 && (int64_t)w * K * n_w * 4 > ((int64_t)96 << 20)) w >>= 1;
+  return w;
+}
 
 struct Kernels {
   hipModule_t module = nullptr;    // every kernel of the plan (for channelwise plans with the
