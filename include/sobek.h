@@ -164,9 +164,13 @@ int sobek_graph_info(sobek_graph graph, int64_t *N, int64_t *E);
 /* Workspace for one pass: the bytes of a single chunk over every receiver when
  * that fits in `budget` (budget 0 = the default of 1 GiB), else `budget` itself
  * (or the minimum for chunks of one receiver, if larger), so that a call given
- * exactly the reported bytes chunks as finely as the budget requires and no finer.  The bytes never scale with E * n_weights or E * dim_out: receiver
+ * exactly the reported bytes chunks as finely as the budget requires and no
+ * finer.  The bytes never scale with E * n_weights or E * dim_out: receiver
  * state is bounded by the chunk size, per-edge x-gradient contributions by the
- * chunk's edges.  conv_* derive their chunking from ws_bytes. */
+ * chunk's edges.  conv_* derive their chunking from ws_bytes.  For the double
+ * backward of a channelwise plan with the state-free kernels the figure covers
+ * both routes a call may take (receiver state for general cotangents, none for
+ * an edge-vector cotangent alone). */
 int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t budget, size_t *bytes);
 
 /* Forward (Section 4.2): out[N][dim_out] = conv(x, evec, phi, W). */
