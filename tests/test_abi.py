@@ -112,3 +112,37 @@ def test_jit_compiles_for_gfx950():
     _lib.jit_compile("8x0e+8x1o", 1, "8x0e+8x1o", 8)
     _lib.jit_compile("8x0e+8x1o", 1, "8x0e+8x1o", 8, "ir_mul", "fan_in", "uvu")
     _lib.jit_compile("3x0e+5x1o+2x2e+1x0o", 1, "4x0e+3x1o+2x2e+1x3e", 4, "mul_ir", "fan_in")
+
+
+def test_bf16_gemm_option():
+    sig = ("32x0e+32x1o+32x2e", 2, "32x0e+32x1o+32x2e", 8)
+    s32 = _lib.plan_source(*sig)
+    sbf = _lib.plan_source(*sig, "ir_mul", "none", "uvw", "bf16_gemm")
+    # the bf16 GEMM text is added to bf16 plans only: removing it gives the fp32 source exactly
+    here = os.path.dirname(os.path.abspath(__file__))
+    with open(os.path.join(here, "..", "paper_2607_18074_amd", "csrc", "device", "gemm_bf16.hip")) as f:
+        block = "\n" + f.read() + "\n"
+    assert "__builtin_amdgcn_mfma_f32_16x16x32_bf16" in sbf and "SB_GEMM_VB_ENTRY(64)" in sbf
+    assert "bf16" not in s32
+    assert sbf.count(block) == 1 and sbf.replace(block, "") == s32
+    # reduced precision is implemented for uvw plans whose multiplicities are multiples of 4
+    for args in (("8x0e+8x1o", 1, "8x0e+8x1o", 4, "ir_mul", "none", "uvu", "bf16_gemm"),
+                 ("6x0e+4x1o", 1, "6x0e+4x1o", 4, "ir_mul", "none", "uvw", "bf16_gemm")):
+        with pytest.raises(_lib.SobekError) as e:
+            _lib.plan_source(*args)
+        assert e.value.code == -2
+    with pytest.raises(KeyError):
+        _lib.plan_source(*sig, "ir_mul", "none", "uvw", "f16")
+
+
+def test_channelwise_state_free_source_is_separate():
+    # a channelwise plan with the state-free kernels compiles them at creation and the
+    # receiver-route kernels on first use; building only the first needs no GPU either
+    os.environ["SOBEK_JIT_STATE_FREE_ONLY"] = "1"
+    try:
+        _lib.jit_compile("8x0e+8x1o", 1, "8x0e+8x1o", 4, "ir_mul", "none", "uvu")
+    finally:
+        del os.environ["SOBEK_JIT_STATE_FREE_ONLY"]
+    src = _lib.plan_source("8x0e+8x1o", 1, "8x0e+8x1o", 4, "ir_mul", "none", "uvu")
+    for kname in ("sobek_uvu_fwd", "sobek_uvu_wgrad", "sobek_fwd_S", "sobek_dbwd_E_r"):
+        assert kname in src
