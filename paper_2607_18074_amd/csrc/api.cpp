@@ -733,39 +733,39 @@ int load_receiver_route(Plan& p, hipModule_t m) {
 int load_uvu(Plan& p, hipModule_t m) {
   int rc;
   auto get = [&](hipFunction_t& f, const char* name) { return get_fn(m, f, name); };
-    hipFunction_t bu = nullptr, bs = nullptr;
-    if ((rc = get(p.k.uvu_fwd, "sobek_uvu_fwd")) || (rc = get(bu, "sobek_uvu_bwd_u")) ||
-        (rc = get(bs, "sobek_uvu_bwd_s")))
-      return rc;
-    if ((rc = get(p.k.uvu_wgrad, "sobek_uvu_wgrad")) || (rc = get(p.k.uvu_wreduce, "sobek_uvu_wreduce"))) return rc;
-    // many paths at high order make the state-free backward spill registers to scratch,
-    // which is slower than the receiver route: take the all-irrep form when it compiled
-    // without spills and below the 256-register cap (two waves per SIMD), else the
-    // per-input-irrep form, else the receiver route
-    int su = 0, ss = 0, sw = 0, ru = 0;
-    HIPCHK(hipFuncGetAttribute(&su, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, bu));
-    HIPCHK(hipFuncGetAttribute(&ss, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, bs));
-    HIPCHK(hipFuncGetAttribute(&sw, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad));
-    HIPCHK(hipFuncGetAttribute(&ru, HIP_FUNC_ATTRIBUTE_NUM_REGS, bu));
-    p.uvu_bwd_direct = su == 0 || ss == 0;
-    p.uvu_sliced = su != 0 || (ru >= 256 && ss == 0);
-    p.k.uvu_bwd = p.uvu_sliced ? bs : bu;
-    const int npart = p.uvu_NB * (p.uvu_sliced ? p.uvu_NA : 1);
-    if (p.uvu_bwd_direct && npart > 1 &&
-        (rc = get(p.k.uvu_bwd_fin, p.uvu_sliced ? "sobek_uvu_bwd_fin_s" : "sobek_uvu_bwd_fin_u")))
-      return rc;
-    p.uvu_wgrad_direct = sw == 0;
-    // the edge-vector-tangent variants (double backward), same slicing
-    if ((rc = get(p.k.uvu_fwd_t, "sobek_uvu_fwd_t")) || (rc = get(p.k.uvu_wgrad_t, "sobek_uvu_wgrad_t")) ||
-        (rc = get(p.k.uvu_bwd_t, p.uvu_sliced ? "sobek_uvu_bwd_st" : "sobek_uvu_bwd_ut")))
-      return rc;
-    if (p.uvu_bwd_direct && npart > 1 &&
-        (rc = get(p.k.uvu_bwd_fin_t, p.uvu_sliced ? "sobek_uvu_bwd_fin_st" : "sobek_uvu_bwd_fin_ut")))
-      return rc;
-    int st = 0, swt = 0;
-    HIPCHK(hipFuncGetAttribute(&st, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd_t));
-    HIPCHK(hipFuncGetAttribute(&swt, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad_t));
-    p.uvu_tan_direct = st == 0 && swt == 0;
+  hipFunction_t bu = nullptr, bs = nullptr;
+  if ((rc = get(p.k.uvu_fwd, "sobek_uvu_fwd")) || (rc = get(bu, "sobek_uvu_bwd_u")) ||
+      (rc = get(bs, "sobek_uvu_bwd_s")))
+    return rc;
+  if ((rc = get(p.k.uvu_wgrad, "sobek_uvu_wgrad")) || (rc = get(p.k.uvu_wreduce, "sobek_uvu_wreduce"))) return rc;
+  // many paths at high order make the state-free backward spill registers to scratch,
+  // which is slower than the receiver route: take the all-irrep form when it compiled
+  // without spills and below the 256-register cap (two waves per SIMD), else the
+  // per-input-irrep form, else the receiver route
+  int su = 0, ss = 0, sw = 0, ru = 0;
+  HIPCHK(hipFuncGetAttribute(&su, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, bu));
+  HIPCHK(hipFuncGetAttribute(&ss, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, bs));
+  HIPCHK(hipFuncGetAttribute(&sw, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad));
+  HIPCHK(hipFuncGetAttribute(&ru, HIP_FUNC_ATTRIBUTE_NUM_REGS, bu));
+  p.uvu_bwd_direct = su == 0 || ss == 0;
+  p.uvu_sliced = su != 0 || (ru >= 256 && ss == 0);
+  p.k.uvu_bwd = p.uvu_sliced ? bs : bu;
+  const int npart = p.uvu_NB * (p.uvu_sliced ? p.uvu_NA : 1);
+  if (p.uvu_bwd_direct && npart > 1 &&
+      (rc = get(p.k.uvu_bwd_fin, p.uvu_sliced ? "sobek_uvu_bwd_fin_s" : "sobek_uvu_bwd_fin_u")))
+    return rc;
+  p.uvu_wgrad_direct = sw == 0;
+  // the edge-vector-tangent variants (double backward), same slicing
+  if ((rc = get(p.k.uvu_fwd_t, "sobek_uvu_fwd_t")) || (rc = get(p.k.uvu_wgrad_t, "sobek_uvu_wgrad_t")) ||
+      (rc = get(p.k.uvu_bwd_t, p.uvu_sliced ? "sobek_uvu_bwd_st" : "sobek_uvu_bwd_ut")))
+    return rc;
+  if (p.uvu_bwd_direct && npart > 1 &&
+      (rc = get(p.k.uvu_bwd_fin_t, p.uvu_sliced ? "sobek_uvu_bwd_fin_st" : "sobek_uvu_bwd_fin_ut")))
+    return rc;
+  int st = 0, swt = 0;
+  HIPCHK(hipFuncGetAttribute(&st, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd_t));
+  HIPCHK(hipFuncGetAttribute(&swt, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad_t));
+  p.uvu_tan_direct = st == 0 && swt == 0;
     return SOBEK_OK;
 }
 
