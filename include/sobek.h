@@ -98,11 +98,13 @@ int sobek_version(void);
  *   dtype: SOBEK_DTYPE_F32, fp32 throughout (the paper's precision, Section 5.1);
  *          SOBEK_DTYPE_BF16_GEMM, a reduced-precision option for uvw plans whose
  *          multiplicities are all multiples of 4 (else SOBEK_E_UNSUPPORTED): the
- *          channel GEMM m = S A (Section 4.2 eq. receiver_matrix_product; the
- *          forward, and the double backward's products with S and dS) rounds S
- *          and A to bf16 (nearest even) and accumulates in fp32 on bf16 MFMA.
- *          Every tensor at this boundary stays fp32; the edge stage, the
- *          backward's GEMMs and every reduction stay fp32.
+ *          channel GEMMs with the receiver state, m = S A (Section 4.2 eq.
+ *          receiver_matrix_product; the forward, and the double backward's
+ *          products with S and dS) and A_bar = S^T mbar (Section 4.3 eq.
+ *          receiver_adjoint; the weight gradients), round both operands to bf16
+ *          (nearest even) and accumulate in fp32 on bf16 MFMA.  Every tensor at
+ *          this boundary stays fp32; the edge stage, Sbar = mbar A^T and every
+ *          reduction stay fp32.
  *   (uvu plans whose paths share one multiplicity run a forward and backward
  *   without receiver state; the environment variable SOBEK_UVU_ROUTE=receiver,
  *   read at plan creation, keeps them on the receiver-state route instead.)

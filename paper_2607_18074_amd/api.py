@@ -41,8 +41,8 @@ def _check_tensor(t, name, shape, dtype=torch.float32):
 
 class Plan:
     """Operator signature: irreps, spherical-harmonic order, radial width, channel mode ("uvw" fully
-    connected, "uvu" channelwise), dtype ("f32", or "bf16_gemm": the channel GEMM m = S A on bf16
-    MFMA with fp32 accumulation; tensors stay fp32)."""
+    connected, "uvu" channelwise), dtype ("f32", or "bf16_gemm": the channel GEMMs with the receiver
+    state, m = S A and A_bar = S^T mbar, on bf16 MFMA with fp32 accumulation; tensors stay fp32)."""
 
     def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw",
                  dtype="f32"):

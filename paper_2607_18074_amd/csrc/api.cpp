@@ -711,7 +711,7 @@ int load_receiver_route(Plan& p, hipModule_t m) {
     std::string sa = std::string("sobek_gemm_sa_") + bns[b], sb = std::string("sobek_gemm_sbar_") + bns[b],
                 ga = std::string("sobek_gemm_ga_") + bns[b],
                 sav = std::string(p.dtype == SOBEK_DTYPE_BF16_GEMM ? "sobek_gemm_sa_vb" : "sobek_gemm_sa_v") + bns[b],
-                gav = std::string("sobek_gemm_ga_v") + bns[b];
+                gav = std::string(p.dtype == SOBEK_DTYPE_BF16_GEMM ? "sobek_gemm_ga_vb" : "sobek_gemm_ga_v") + bns[b];
     if ((rc = get_fn(m, p.k.gemm_sa[b], sa.c_str())) || (rc = get_fn(m, p.k.gemm_sbar[b], sb.c_str())) ||
         (rc = get_fn(m, p.k.gemm_ga[b], ga.c_str())) || (rc = get_fn(m, p.k.gemm_sa_v[b], sav.c_str())) ||
         (rc = get_fn(m, p.k.gemm_ga_v[b], gav.c_str())))

@@ -1,6 +1,7 @@
-// Channel GEMM m_g = S_g A_g on bf16 MFMA, for plans built with the dtype
-// SOBEK_DTYPE_BF16_GEMM (Section 4.2 eq. receiver_matrix_product, the product
-// the paper runs as an fp32 GEMM).  The generator appends this file to the
+// The channel GEMMs with the receiver state S on bf16 MFMA, for plans built with
+// the dtype SOBEK_DTYPE_BF16_GEMM: m_g = S_g A_g (Section 4.2 eq.
+// receiver_matrix_product) and the weight gradient A_bar = S^T mbar (Section 4.3
+// eq. receiver_adjoint), which the paper runs as fp32 GEMMs.  The generator appends this file to the
 // plan's source only for such plans; it relies on the fp32 device code that
 // precedes every plan (sb_gemm_sa_v's tiling constants, loads and row mapping).
 //
@@ -19,6 +20,28 @@
 
 typedef __bf16 sb_b8 __attribute__((ext_vector_type(8)));
 
+// acc += the 32-deep slab product of sA[kk][32 * wave + 0..31] and sB[kk][0..BN-1]
+// (kk = 0..31, the reduction index), rounded to bf16 as it leaves LDS
+template <int BN>
+SB_DEV void sb_slab_bf16(const float (*sA)[SB_VM + 4], const float (*sB)[BN + 4], int wave, int lane,
+                         sb_f4 (&acc)[2][BN / 16]) {
+  const int kg = 8 * (lane >> 4), li = lane & 15;
+  sb_b8 a0, a1;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    a0[j] = (__bf16)sA[kg + j][32 * wave + li];
+    a1[j] = (__bf16)sA[kg + j][32 * wave + 16 + li];
+  }
+#pragma unroll
+  for (int t = 0; t < BN / 16; ++t) {
+    sb_b8 b;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b[j] = (__bf16)sB[kg + j][16 * t + li];
+    acc[0][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b, acc[0][t], 0, 0, 0);
+    acc[1][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b, acc[1][t], 0, 0, 0);
+  }
+}
+
 template <int BN>
 SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const float* __restrict__ W,
                           const int* __restrict__ ktab, float* __restrict__ out, int dg, int Cg, int off, int CX,
@@ -30,7 +53,7 @@ SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const f
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int rb = blockIdx.x * SB_VM, cb = blockIdx.y * BN;
   const int kbeg = blockIdx.z * kper, kend = min(D, kbeg + kper);
-  const int kg = 8 * (lane >> 4), li = lane & 15;
+  const int li = lane & 15;
   sb_f4 acc[2][BN / 16];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -72,20 +95,7 @@ SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const f
   for (int k0 = kbeg; k0 < kend; k0 += SB_VK) {
     const bool more = k0 + SB_VK < kend;
     if (more) load(k0 + SB_VK);
-    sb_b8 a0, a1;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      a0[j] = (__bf16)sA[kg + j][32 * wave + li];
-      a1[j] = (__bf16)sA[kg + j][32 * wave + 16 + li];
-    }
-#pragma unroll
-    for (int t = 0; t < BN / 16; ++t) {
-      sb_b8 b;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) b[j] = (__bf16)sB[kg + j][16 * t + li];
-      acc[0][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b, acc[0][t], 0, 0, 0);
-      acc[1][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b, acc[1][t], 0, 0, 0);
-    }
+    sb_slab_bf16<BN>(sA, sB, wave, lane, acc);
     __syncthreads();
     if (more) {
       store();
@@ -111,11 +121,95 @@ SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const f
       }
 }
 
+// Weight-gradient partials P[split][k][w] (+)= sum over the split's rows r of S[r][k] mbar(r, w)
+// (Section 4.3 eq. receiver_adjoint, A_bar = S^T mbar): the blocking of sb_gemm_ga_v (a 128-k x
+// BN-w block walking 32-row slabs of its split), with the slab product on bf16 MFMA.
+template <int BN>
+SB_DEV void sb_gemm_ga_vb(const float* __restrict__ S, int nrows, int D, const float* __restrict__ M,
+                          float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split,
+                          int accumulate) {
+  __shared__ float sA[SB_VK][SB_VM + 4];
+  __shared__ float sB[SB_VK][BN + 4];
+  constexpr int NB = (SB_VK * BN / 4 + 255) / 256;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int kb = blockIdx.x * SB_VM, cb = blockIdx.y * BN, split = blockIdx.z;
+  const int rbeg = split * rows_per_split;
+  const int rend = min(nrows, rbeg + rows_per_split);
+  sb_f4 acc[2][BN / 16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t) acc[i][t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+  sb_v4 ra[4], rbv[NB];
+  auto load = [&](int rr0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = (tid >> 5) + 8 * i, k = kb + 4 * (tid & 31);
+      const int gr = rr0 + rr;
+      ra[i] = (gr < rend && k < D) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      const int rr = idx / (BN / 4), c = 4 * (idx % (BN / 4));
+      const int gr = rr0 + rr;
+      rbv[i] = (idx < SB_VK * BN / 4 && gr < rend && cb + c < Cg)
+                   ? sb_ld4(M + sb_row_addr(gr, dg, Cg, off, CX, r0) + cb + c)
+                   : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = (tid >> 5) + 8 * i;
+      *(sb_v4*)&sA[rr][4 * (tid & 31)] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < SB_VK * BN / 4) *(sb_v4*)&sB[idx / (BN / 4)][4 * (idx % (BN / 4))] = rbv[i];
+    }
+  };
+  if (rbeg < rend) {
+    load(rbeg);
+    store();
+  }
+  __syncthreads();
+  for (int rr0 = rbeg; rr0 < rend; rr0 += SB_VK) {
+    const bool more = rr0 + SB_VK < rend;
+    if (more) load(rr0 + SB_VK);
+    sb_slab_bf16<BN>(sA, sB, wave, lane, acc);
+    __syncthreads();
+    if (more) {
+      store();
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < BN / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int k = kb + 32 * wave + 16 * i + 4 * (lane >> 4) + r;
+        const int col = cb + 16 * t + (lane & 15);
+        if (k < D && col < Cg) {
+          float* o = P + ((sb_i64)split * D + k) * Cg + col;
+          *o = accumulate ? (*o + acc[i][t][r]) : acc[i][t][r];
+        }
+      }
+}
+
 #define SB_GEMM_VB_ENTRY(BN)                                                                         \
   extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sa_vb##BN(                           \
       const float* S, int nrows, int D, const float* W, const int* ktab, float* out, int dg,       \
       int Cg, int off, int CX, int r0, int accumulate, float* P, int kper) {                       \
     sb_gemm_sa_vb<BN>(S, nrows, D, W, ktab, out, dg, Cg, off, CX, r0, accumulate, P, kper);        \
+  }                                                                                                \
+  extern "C" __global__ __launch_bounds__(256) void sobek_gemm_ga_vb##BN(                           \
+      const float* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \
+      int r0, int rows_per_split, int accumulate) {                                                \
+    sb_gemm_ga_vb<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split, accumulate);         \
   }
 
 SB_GEMM_VB_ENTRY(16)

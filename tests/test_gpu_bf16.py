@@ -1,17 +1,20 @@
 """GPU parity of the reduced-precision channel GEMM (plan dtype "bf16_gemm").
 
-Such a plan rounds S and A to bf16 inside the GEMM m = S A (Section 4.2 eq.
-receiver_matrix_product) and accumulates in fp32; every tensor at the
+Such a plan rounds both operands to bf16 inside the GEMMs with the receiver
+state, m = S A (Section 4.2 eq. receiver_matrix_product) and A_bar = S^T mbar
+(Section 4.3 eq. receiver_adjoint), and accumulates in fp32; every tensor at the
 boundary and every other stage stays fp32.  Checked through the C ABI against
 the float64 oracle on fp32 inputs:
 
-* forward and the double backward's output cotangent (both take m = S A) within
-  the reduced-precision bound 1e-2 (max-norm relative): bf16 keeps 8 mantissa
-  bits, so each rounded operand is off by at most 2^-9 relative, and the
-  accumulated sum stays well inside 1e-2 of the largest output;
+* the outputs those GEMMs produce (forward m, the weight gradients, the double
+  backward's g_gout) within the reduced-precision bound 1e-2 (max-norm
+  relative): bf16 keeps 8 mantissa bits, so each rounded operand is off by at
+  most 2^-9 relative, and the accumulated sum stays well inside 1e-2 of the
+  largest output;
 * the forward really took the bf16 kernel: it differs from the fp32 plan's
   forward by more than fp32 rounding could explain;
-* the backward, which has no m = S A product, keeps the fp32 tolerance.
+* every other output (x_bar, phi_bar, evec_bar and their double-backward
+  counterparts, built from the fp32 adjoint state) keeps the fp32 tolerance.
 """
 
 import numpy as np
@@ -72,7 +75,7 @@ def test_bf16_forward(gpu, sig, N, E, seed, iso, budget):
 
 
 @pytest.mark.parametrize("sig,N,E,seed,iso", CASES[1:3])
-def test_bf16_backward_stays_fp32(gpu, sig, N, E, seed, iso):
+def test_bf16_backward(gpu, sig, N, E, seed, iso):
     case = make_case(sig, N, E, seed, isolated=iso)
     api, plan, graph, prob = _setup(case, "bf16_gemm")
     g = case["graph"]
@@ -81,7 +84,7 @@ def test_bf16_backward_stays_fp32(gpu, sig, N, E, seed, iso):
     for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
         err = max_rel(_n(o), ref[name])
         print(f"bf16-plan bwd {sig} {name}: {err:.2e}")
-        assert err <= BWD_TOL, name
+        assert err <= (BF16_TOL if name == "gW" else BWD_TOL), name
 
 
 @pytest.mark.parametrize("sig,N,E,seed,iso", CASES[1:3])
@@ -98,8 +101,8 @@ def test_bf16_double_backward(gpu, sig, N, E, seed, iso):
     for name, o in zip(names, outs):
         err = max_rel(_n(o), ref[name])
         print(f"bf16 dbwd {sig} {name}: {err:.2e}")
-        # g_gout is built from m = S A products; the rest from the fp32 adjoint kernels
-        assert err <= (BF16_TOL if name == "g_gout" else BWD_TOL), name
+        # g_gout and g_W come from the bf16 GEMMs; the rest from the fp32 adjoint kernels
+        assert err <= (BF16_TOL if name in ("g_gout", "g_W") else BWD_TOL), name
 
 
 @pytest.mark.timeout(600)
