@@ -109,7 +109,9 @@ def test_bf16_double_backward(gpu, sig, N, E, seed, iso):
 def test_bf16_full_size_wide(gpu):
     """The Wide workload at full size (50,000 nodes, 2.0M edges) in the benchmark's launch
     configuration (8 GiB workspace, several receiver chunks): forward m and the double backward's
-    g_gout at sampled receivers against the oracle on their in-edges."""
+    g_gout at sampled receivers against the oracle on their in-edges, and the weight gradient A_bar
+    of a backward whose m_bar is zero outside the sampled receivers (A_bar is linear in m_bar, so
+    the oracle on those receivers' in-edges gives all of it)."""
     import torch
     from paper_2607_18074_amd import api
     from paper_2607_18074_amd import workloads as wl
@@ -133,6 +135,9 @@ def test_bf16_full_size_wide(gpu):
     m = _n(api.conv_fwd(plan, graph, *args, budget=8 << 30))
     gg = _n(api.conv_dbwd(plan, graph, *args, _t(gout), t_gevec=_t(rdot), budget=8 << 30,
                           need=(True, False, False, False, False))[0])
+    gout_m = np.zeros_like(gout)
+    gout_m[R] = gout[R]
+    gW = _n(api.conv_bwd(plan, graph, *args, _t(gout_m), need=(False, False, False, True), budget=8 << 30)[3])
     del args, graph
     torch.cuda.empty_cache()
 
@@ -140,7 +145,8 @@ def test_bf16_full_size_wide(gpu):
     rp, snd, ev, ph, rec = edge_subgraph(g, A)
     oa = (prob, x, ev, ph, W, rp, snd)
     for name, got, ref in (("fwd m", m[rec], oc.fwd(*oa)),
-                           ("dbwd g_gout", gg[rec], oc.dbwd(*oa, gout[rec], t_gevec=rdot[A])["g_gout"])):
+                           ("dbwd g_gout", gg[rec], oc.dbwd(*oa, gout[rec], t_gevec=rdot[A])["g_gout"]),
+                           ("bwd A_bar (restricted m_bar)", gW, oc.bwd(*oa, gout[rec])["gW"])):
         err = max_rel(got, ref)
         print(f"  {name}: max rel err {err:.2e}", flush=True)
         assert err <= BF16_TOL, name
