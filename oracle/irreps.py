@@ -137,10 +137,3 @@ def blocks_to_flat(blocks, irreps, layout="ir_mul"):
             raise ValueError(layout)
     return np.concatenate(parts, axis=-1)
 
-
-def fan_in_per_output(paths, n_out):
-    """fan_in_g = sum of C_in over the paths that reach output irrep g."""
-    f = [0] * n_out
-    for p in paths:
-        f[p["i_out"]] += p["c_in"]
-    return f
