@@ -107,7 +107,11 @@ int sobek_version(void);
  *          reduction stay fp32.
  *   (uvu plans whose paths share one multiplicity run a forward and backward
  *   without receiver state; the environment variable SOBEK_UVU_ROUTE=receiver,
- *   read at plan creation, keeps them on the receiver-state route instead.)
+ *   read at plan creation, keeps them on the receiver-state route instead.
+ *   Their backward edge kernel has two forms, all input irreps per lane or one
+ *   input irrep per slice, chosen at plan creation from the compiled kernels'
+ *   register and scratch use; SOBEK_UVU_FORM=u or SOBEK_UVU_FORM=s, read at
+ *   plan creation, forces the first or the second, for testing.)
  *   path_norm: SOBEK_NORM_NONE (alpha = 1) or SOBEK_NORM_FAN_IN
  *   (alpha = 1/sqrt(fan_in), fan_in = number of terms summed into one output
  *   channel: the sum of C_in over the paths into the same output irrep for

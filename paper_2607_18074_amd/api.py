@@ -121,13 +121,19 @@ class Graph:
     def handle(self):
         return self._h
 
+    def workspace_bytes(self, plan, pass_, budget=0):
+        """sobek_workspace_size of a pass ("fwd", "bwd", "dbwd") at `budget` bytes (0 = the default; 1 gives
+        the minimum, chunks of one receiver)."""
+        nb = ctypes.c_size_t()
+        check(lib().sobek_workspace_size(plan.handle, self._h, _lib.PASSES[pass_], budget, ctypes.byref(nb)))
+        return int(nb.value)
+
     def workspace(self, plan, pass_, budget=0):
         """Cached workspace tensor for (plan, pass, budget)."""
         key = (id(plan), pass_, budget)
         if key not in self._ws:
-            nb = ctypes.c_size_t()
-            check(lib().sobek_workspace_size(plan.handle, self._h, _lib.PASSES[pass_], budget, ctypes.byref(nb)))
-            self._ws[key] = torch.empty(max(int(nb.value), 256), dtype=torch.uint8, device=self.rowptr.device)
+            nb = self.workspace_bytes(plan, pass_, budget)
+            self._ws[key] = torch.empty(max(nb, 256), dtype=torch.uint8, device=self.rowptr.device)
         return self._ws[key]
 
     def __del__(self):

@@ -749,6 +749,14 @@ int load_uvu(Plan& p, hipModule_t m) {
   HIPCHK(hipFuncGetAttribute(&ru, HIP_FUNC_ATTRIBUTE_NUM_REGS, bu));
   p.uvu_bwd_direct = su == 0 || ss == 0;
   p.uvu_sliced = su != 0 || (ru >= 256 && ss == 0);
+  // SOBEK_UVU_FORM=u|s forces one form (testing: both forms run on any signature; a form that
+  // spills is slower, not wrong)
+  const char* form = std::getenv("SOBEK_UVU_FORM");
+  const bool forced = form && (std::strcmp(form, "u") == 0 || std::strcmp(form, "s") == 0);
+  if (forced) {
+    p.uvu_bwd_direct = true;
+    p.uvu_sliced = form[0] == 's';
+  }
   p.k.uvu_bwd = p.uvu_sliced ? bs : bu;
   const int npart = p.uvu_NB * (p.uvu_sliced ? p.uvu_NA : 1);
   if (p.uvu_bwd_direct && npart > 1 &&
@@ -765,8 +773,8 @@ int load_uvu(Plan& p, hipModule_t m) {
   int st = 0, swt = 0;
   HIPCHK(hipFuncGetAttribute(&st, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_bwd_t));
   HIPCHK(hipFuncGetAttribute(&swt, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, p.k.uvu_wgrad_t));
-  p.uvu_tan_direct = st == 0 && swt == 0;
-    return SOBEK_OK;
+  p.uvu_tan_direct = (st == 0 || forced) && swt == 0;
+  return SOBEK_OK;
 }
 
 std::mutex g_rr_mu;
