@@ -85,6 +85,13 @@ def test_bf16_backward(gpu, sig, N, E, seed, iso):
         err = max_rel(_n(o), ref[name])
         print(f"bf16-plan bwd {sig} {name}: {err:.2e}")
         assert err <= (BF16_TOL if name == "gW" else BWD_TOL), name
+    # the weight gradient came from the bf16 kernel: the fp32 plan's differs by more than rounding
+    _, plan32, graph32, _ = _setup(case, "f32")
+    gW32 = api.conv_bwd(plan32, graph32, _t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]), _t(case["gout"]),
+                        need=(False, False, False, True))[3]
+    gap = max_rel(_n(outs[3]), _n(gW32))
+    print(f"bf16-plan bwd {sig} gW vs fp32 plan: {gap:.2e}")
+    assert gap > 1e-5
 
 
 @pytest.mark.parametrize("sig,N,E,seed,iso", CASES[1:3])

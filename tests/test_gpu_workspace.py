@@ -1,0 +1,78 @@
+"""The workspace is bounded by nodes, not edges (the purpose of the edge-scaling stress workload; the
+paper's schedule keeps receiver state and chunk buffers within a fixed scratch budget, Section 4.2 and
+its Appendix on the scratch budget).
+
+Two graphs with the same node count and six times as many edges in the second: at a budget below what
+one chunk over every receiver would need, sobek_workspace_size reports the same bytes for both graphs and
+every pass, and so does the minimum workspace (chunks of one receiver, windows of one edge).  The backward
+and double backward on the larger graph then run in exactly that workspace (many receiver chunks and
+edge windows) and match the oracle.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import conv as oc
+from paper_2607_18074_amd import workloads as wl
+from tests.cases import BWD_TOL, FWD_TOL, SIGS, max_rel, std_for
+
+pytestmark = pytest.mark.gpu
+
+
+def _t(a):
+    import torch
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _n(t):
+    return None if t is None else t.detach().cpu().numpy()
+
+
+def test_workspace_independent_of_edge_count(gpu):
+    import torch
+    from paper_2607_18074_amd import _lib, api
+    irr_in, lmax, irr_out, K = SIGS["small"]
+    plan = api.Plan(irr_in, lmax, irr_out, K)
+    N = 300
+    small_g = wl.random_graph(N, 2000, 51, K=K)
+    big_g = wl.random_graph(N, 12000, 52, K=K)
+    graphs = [api.Graph(_t(g.rowptr), _t(g.sender)) for g in (small_g, big_g)]
+    budget = 4 << 20   # one chunk needs N * state + E * dim_in floats: 10.8 MB of state alone
+    for p in ("fwd", "bwd", "dbwd"):
+        sizes = [gr.workspace_bytes(plan, p, budget) for gr in graphs]
+        mins = [gr.workspace_bytes(plan, p, 1) for gr in graphs]
+        print(f"{p}: workspace at 4 MiB {sizes}, minimum {mins}")
+        assert sizes[0] == sizes[1], p
+        assert mins[0] == mins[1], p
+        assert sizes[1] <= budget
+
+    g = big_g
+    graph = graphs[1]
+    prob = oc.Problem(irr_in, lmax, irr_out, K)
+    std = std_for(irr_in, irr_out, lmax, K)
+    x = wl.node_features(N, prob.dim_in, 53)
+    W = wl.weights(K, std, 53)
+    gout = wl.out_cotangent(N, prob.dim_out, 53)
+    tev = wl.cotangents(N, g.E, K, prob.dim_in, len(std), 53, which=("evec",))["evec"]
+    args = (_t(x), _t(g.evec), _t(g.phi), _t(W))
+    oa = (prob, x, g.evec, g.phi, W, g.rowptr, g.sender)
+    ws = {p: torch.empty(graph.workspace_bytes(plan, p, budget), dtype=torch.uint8, device="cuda")
+          for p in ("fwd", "bwd", "dbwd")}
+    _lib.profile_reset()
+    _lib.profile_enable(True)
+    try:
+        m = api.conv_fwd(plan, graph, *args, ws=ws["fwd"])
+        outs = api.conv_bwd(plan, graph, *args, _t(gout), ws=ws["bwd"])
+        douts = api.conv_dbwd(plan, graph, *args, _t(gout), t_gevec=_t(tev), ws=ws["dbwd"])
+        prof = _lib.profile_read()
+    finally:
+        _lib.profile_enable(False)
+    print("launches:", {k: v[0] for k, v in prof.items()})
+    assert prof["sobek_fwd_S"][0] >= 3 and prof["sobek_bwd_E"][0] >= 3 and prof["sobek_dbwd_E_r"][0] >= 3
+    assert max_rel(_n(m), oc.fwd(*oa)) <= FWD_TOL
+    ref = oc.bwd(*oa, gout)
+    for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
+        assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
+    dref = oc.dbwd(*oa, gout, t_gevec=tev)
+    for name, o in zip(("g_gout", "g_x", "g_evec", "g_phi", "g_W"), douts):
+        assert max_rel(_n(o), dref[name]) <= BWD_TOL, name
