@@ -21,14 +21,22 @@ measured with HIP events recorded on its launch stream inside the timed region.
 cpu_baseline: the float64 oracle, timed on this host on a bounded receiver
 sample of the same workload, scaled to edges/s.
 
-Per-kernel algorithmic FLOP model (per edge E, per receiver N; SD = sum_pi
-C_in d_out, NZ = sum_pi C_in nnz_pi, G = sum_pi C_in d_out C_out):
-  fwd_S / fwd_dS (r-only tangent)  E (2 K SD + 2 NZ)
-  gemm_sa, gemm_sbar, gemm_ga      N 2 K G each
+Algorithmic FLOP model (per edge E, per receiver N; SD = sum_pi C_in d_out,
+NZ = sum_pi C_in nnz_pi, G = sum_pi C_in d_out C_out), per pass:
+  fwd   E (2 K SD + 2 NZ) + N 2 K G
+  bwd   E (4 K SD + 6 NZ) + N 4 K G
+  dbwd  E (6 K SD + 6 NZ) + N 6 K G   (edge-vector cotangent alone)
+and per kernel:
+  fwd_S, fwd_dS (r-only tangent)   E (2 K SD + 2 NZ)
+  gemm_sa, gemm_sbar, gemm_ga      N 2 K G per launch set (one per group)
   bwd_E                            E (4 K SD + 6 NZ)
-  dbwd_E (r-only tangent)          E (4 K SD + 6 NZ)
-With the state kept by the forward, every launch of a kernel in a step is
-algorithmic work (the backward recomputes nothing).
+  dbwd_E (r-only tangent)          E (4 K SD + 4 NZ): the double backward's
+                                   E (6 K SD + 6 NZ) less the directional state
+                                   that fwd_dS computes
+The double backward reads the adjoint state the backward kept, so its share
+N 2 K G of Sbar = gout A^T runs once per step, in the backward; the pass model
+still counts it, as the paper's pass does.  With the states kept, no kernel
+launch in a step is recomputation.
 
 paper_context quotes the paper's own figures with their hardware (an NVIDIA
 RTX 5090, fp32, against OpenEquivariance on other workloads): context, not a
@@ -69,15 +77,16 @@ def flop_model(plan, N, E):
         NZ += cin * nnz
         G += cin * (2 * lo + 1) * (1 if getattr(plan, "mode", "uvw") == "uvu" else cout)  # uvu: elementwise
     edge_fwd = E * (2 * K * SD + 2 * NZ)
-    edge_adj = E * (4 * K * SD + 6 * NZ)
+    edge_bwd = E * (4 * K * SD + 6 * NZ)
+    edge_dbwd = E * (4 * K * SD + 4 * NZ)
     gemm = N * 2 * K * G
     per_kernel = {
-        "fwd_S": edge_fwd, "fwd_dS": edge_fwd, "bwd_E": edge_adj, "dbwd_E": edge_adj,
+        "fwd_S": edge_fwd, "fwd_dS": edge_fwd, "bwd_E": edge_bwd, "dbwd_E": edge_dbwd,
         "gemm_sa": gemm, "gemm_sbar": gemm, "gemm_ga": gemm,
     }
-    # fwd: S, m = S A; bwd: Sbar = mbar A^T, A_bar = S^T mbar (S kept by the forward), edge adjoints;
-    # dbwd (edge-vector cotangent): dS, m_dot = dS A, g_A = dS^T mbar (Sbar kept by the backward), edge terms
-    passes = {"fwd": edge_fwd + gemm, "bwd": 2 * gemm + edge_adj, "dbwd": edge_fwd + 2 * gemm + edge_adj}
+    # fwd: S, m = S A; bwd: Sbar = mbar A^T, A_bar = S^T mbar, edge adjoints; dbwd (edge-vector
+    # cotangent): dS, m_dot = dS A, g_A = dS^T mbar, Sbar = mbar A^T, edge terms
+    passes = {"fwd": edge_fwd + gemm, "bwd": edge_bwd + 2 * gemm, "dbwd": edge_fwd + edge_dbwd + 3 * gemm}
     if getattr(plan, "mode", "uvw") == "uvu":
         # channelwise: per edge and path the weight w = phi A of each channel (2K C), the CG contraction
         # (2 nnz C) and the tied-channel product (2 C d_out); the backward adds phi_bar = A h, G = w mbar
@@ -119,7 +128,7 @@ def time_pass(fn, torch):
     return float(np.median(samples)), len(samples)
 
 
-def sweep(budget_gib, names, dtype="f32"):
+def sweep(budget_gib, names, dtype="f32", retain=True):
     """Every workload and pass of the benchmark configurations: one JSON line each, then a table.
     dtype "bf16_gemm" runs the plans' channel GEMM m = S A on bf16 MFMA (tensors stay fp32)."""
     import torch
@@ -140,8 +149,8 @@ def sweep(budget_gib, names, dtype="f32"):
         gt = T(wl.out_cotangent(g.N, plan.dim_out, cfg["index"]))
         ev, ph = T(g.evec), T(g.phi)
         ws = {}   # one pass's workspace at a time, so each pass's peak counts only what it needs
-        state = api.new_state(plan, graph) if "bwd" in cfg["passes"] else None
-        adj = api.new_state(plan, graph) if "dbwd" in cfg["passes"] else None
+        state = api.new_state(plan, graph) if ("bwd" in cfg["passes"] and retain) else None
+        adj = api.new_state(plan, graph) if ("dbwd" in cfg["passes"] and retain) else None
         out = torch.empty(g.N, plan.dim_out, device="cuda")
         fm, bm = flop_model(plan, g.N, g.E), byte_model(plan, g.N, g.E)
         fns = {"fwd": lambda: api.conv_fwd(plan, graph, xt, ev, ph, Wt, out=out, ws=ws["fwd"], state=state)}
@@ -171,7 +180,10 @@ def sweep(budget_gib, names, dtype="f32"):
             ms, n = time_pass(fns[pname], torch)
             tf = fm["passes"][pname] / (ms * 1e-3) / 1e12
             gbs = bm[pname] / (ms * 1e-3) / 1e9
-            row = dict(workload=name if dtype == "f32" else f"{name} ({dtype})", dtype=dtype, pass_=pname,
+            tag = name if dtype == "f32" else f"{name} ({dtype})"
+            if not retain:
+                tag += f" [no kept state, {budget_gib:g} GiB]"
+            row = dict(workload=tag, dtype=dtype, retain=retain, pass_=pname,
                        N=g.N, E=g.E, ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3),
                        tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS, alg_gbs=gbs, frac_hbm=gbs / PEAK_HBM_GBS,
                        peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9,
@@ -361,6 +373,14 @@ def cpu_baseline(case, plan_sig, target_s=15.0):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
         cores = 1
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:  # pragma: no cover
+        pass
 
     def run(R):
         Es = int(g.rowptr[R])
@@ -382,7 +402,7 @@ def cpu_baseline(case, plan_sig, target_s=15.0):
     return dict(value=Es / dt, unit="edges/s", cores=int(cores), kind="oracle",
                 sample=f"fwd+bwd+dbwd (t_gevec-only) float64 oracle on the in-edges of the first {R} receivers "
                        f"({Es} edges) of the same graph and tensors; {dt:.1f} s",
-                seconds=dt)
+                seconds=dt, cpu_model=cpu_model, affinity_cpus=len(os.sched_getaffinity(0)))
 
 
 def main():
@@ -406,6 +426,9 @@ def main():
     ap.add_argument("--table-profiles", default="", help="tables: comma-separated subset of profiles (default all)")
     ap.add_argument("--retain", action="store_true", help="regimes: keep S and Sbar across passes (default: the "
                     "paper's setting, recompute within the workspace budget)")
+    ap.add_argument("--no-retain", action="store_true",
+                    help="sweep: keep no receiver state across passes (each pass recomputes within its budget, the "
+                    "paper's setting for a fixed scratch budget)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
                     help="only run a plain device copy of this many MiB (traffic-counter calibration)")
     args = ap.parse_args()
@@ -434,7 +457,7 @@ def main():
         return
     if args.sweep:
         names = ["tiny", "small", "medium", "wide", "stress"] if args.sweep == "all" else args.sweep.split(",")
-        sweep(args.budget, names, args.dtype)
+        sweep(args.budget, names, args.dtype, not args.no_retain)
         return
 
     import torch
@@ -444,9 +467,11 @@ def main():
 
     cfg = wl.CONFIGS[args.workload]
     t0 = time.time()
+    log(f"generating the {args.workload} graph ...")
     g = wl.config_graph(args.workload)
     log(f"graph {args.workload}: N={g.N} E={g.E} ({time.time() - t0:.1f}s)")
     torch.cuda.set_device(0)
+    log("creating the plan (kernels from the code-object cache) ...")
     plan = api.Plan(cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"])
     x = wl.node_features(g.N, plan.dim_in, cfg["index"])
     W = wl.weights(plan.K, plan.weight_std(), cfg["index"])
@@ -456,7 +481,11 @@ def main():
     graph = api.Graph(T(g.rowptr), T(g.sender))
     xt, ev, ph, Wt, gt = T(x), T(g.evec), T(g.phi), T(W), T(gout)
     budget = int(args.budget * (1 << 30))
-    ws = {p: graph.workspace(plan, p, budget) for p in ("fwd", "bwd", "dbwd")}
+    # the passes run one after the other on one stream: they share one workspace, sized for the
+    # largest of the three at the budget
+    ws_bytes = {p: graph.workspace_bytes(plan, p, budget) for p in ("fwd", "bwd", "dbwd")}
+    ws_all = torch.empty(max(ws_bytes.values()), dtype=torch.uint8, device=dev)
+    ws = {p: ws_all[:n] for p, n in ws_bytes.items()}
     out = torch.empty(g.N, plan.dim_out, device=dev)
     state = api.new_state(plan, graph)     # receiver state kept from the forward for the backward
     adj = api.new_state(plan, graph)       # adjoint state kept from the backward for the double backward
@@ -473,6 +502,7 @@ def main():
         return api.conv_dbwd(plan, graph, xt, ev, ph, Wt, gt, t_gevec=rdot, ws=ws["dbwd"], adj_state=adj)
 
     # cotangent of L2 = sum |evec_bar|^2
+    log("first forward and backward (the double backward's cotangent) ...")
     fwd()
     _, gev, _, _ = bwd()
     rdot = (2.0 * gev).contiguous()
@@ -483,10 +513,12 @@ def main():
         bwd()
         dbwd()
 
+    log(f"{args.warmup} warm-up steps ...")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats()
+    log(f"{args.steps} timed steps ...")
 
     # timed region: K steps, with per-launch HIP events on the launch stream
     _lib.profile_reset()
@@ -505,6 +537,7 @@ def main():
     ms_step = e0.elapsed_time(e1) / args.steps
     peak_gb = torch.cuda.max_memory_allocated() / 1e9
 
+    log(f"timed: {ms_step:.2f} ms per step; per-pass timing ...")
     # per-pass timing (outside the headline region)
     pass_ms = {}
     for name, fn in (("fwd", fwd), ("bwd", bwd), ("dbwd", dbwd)):
@@ -548,10 +581,13 @@ def main():
                     traffic=None)
 
     passes = {}
+    bm = byte_model(plan, g.N, g.E)
     for name in ("fwd", "bwd", "dbwd"):
         ms = pass_ms[name]
         tf = fm["passes"][name] / (ms * 1e-3) / 1e12
-        passes[name] = dict(ms=ms, edges_per_s=g.E / (ms * 1e-3), tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS)
+        gbs = bm[name] / (ms * 1e-3) / 1e9
+        passes[name] = dict(ms=ms, edges_per_s=g.E / (ms * 1e-3), tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS,
+                            alg_gbs=gbs, frac_hbm=gbs / PEAK_HBM_GBS, flops=fm["passes"][name], bytes=bm[name])
     step_flops = sum(fm["passes"].values())
 
     cpu = None
@@ -583,6 +619,7 @@ def main():
         "passes": passes,
         "peak_mem_gb": peak_gb,
         "workspace_gb": {p: w.numel() / 1e9 for p, w in ws.items()},
+        "workspace_shared_gb": ws_all.numel() / 1e9,
         "retained_state_gb": (state.numel() + adj.numel()) * 4 / 1e9,
         "paper_context": PAPER_CONTEXT,
         "kernels": kernels,
