@@ -26,7 +26,13 @@
  *   thread; the pointer stays valid until the next sobek_* call on that thread.
  * Memory: every device pointer is caller-owned.  conv_* calls never allocate
  *   device memory; their scratch is the caller's workspace (ws, ws_bytes).
- *   Plans own small device tables allocated in sobek_plan_create.
+ *   Plans own small device tables allocated in sobek_plan_create.  The one
+ *   exception is code: a channelwise plan with the state-free kernels loads
+ *   only those at creation, and the first conv_* call that needs its
+ *   receiver-route kernels (a forward that keeps its state, a weight gradient
+ *   or double backward that cannot take the state-free route) compiles them
+ *   (hipRTC, or the on-disk cache) and loads them, which allocates device
+ *   memory for the code and may take seconds.
  * Streams: conv_* calls enqueue work on the given stream and return without
  *   synchronising.  They overwrite their outputs (no accumulation).
  * Determinism: for identical inputs, plan, graph and workspace size the
@@ -167,7 +173,9 @@ int sobek_graph_destroy(sobek_graph graph);
 /* Number of nodes and edges of a prepared graph (either pointer may be NULL). */
 int sobek_graph_info(sobek_graph graph, int64_t *N, int64_t *E);
 
-/* Workspace for one pass: the bytes of a single chunk over every receiver when
+/* Workspace for one pass (Section 4.2: receiver state and chunk buffers stay
+ * within a fixed scratch budget and never scale with the edge count; the
+ * Appendix on the runtime scratch budget).  The bytes of a single chunk over every receiver when
  * that fits in `budget` (budget 0 = the default of 1 GiB), else `budget` itself
  * (or the minimum for chunks of one receiver, if larger), so that a call given
  * exactly the reported bytes chunks as finely as the budget requires and no
