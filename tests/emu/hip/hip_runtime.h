@@ -1,0 +1,61 @@
+// Host-side stand-in for the HIP runtime API (CPU emulation build only).
+#pragma once
+#include <cstddef>
+#include <cstdint>
+#include <cstdio>
+
+typedef enum hipError_t {
+  hipSuccess = 0,
+  hipErrorInvalidValue = 1,
+  hipErrorOutOfMemory = 2,
+  hipErrorNotFound = 500,
+  hipErrorLaunchFailure = 719,
+} hipError_t;
+typedef void* hipStream_t;
+typedef void* hipEvent_t;
+typedef struct EmuModule* hipModule_t;
+typedef struct EmuFunc* hipFunction_t;
+typedef enum hipMemcpyKind {
+  hipMemcpyHostToHost = 0,
+  hipMemcpyHostToDevice = 1,
+  hipMemcpyDeviceToHost = 2,
+  hipMemcpyDeviceToDevice = 3,
+  hipMemcpyDefault = 4
+} hipMemcpyKind;
+typedef enum hipFunction_attribute {
+  HIP_FUNC_ATTRIBUTE_MAX_THREADS_PER_BLOCK,
+  HIP_FUNC_ATTRIBUTE_SHARED_SIZE_BYTES,
+  HIP_FUNC_ATTRIBUTE_CONST_SIZE_BYTES,
+  HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES,
+  HIP_FUNC_ATTRIBUTE_NUM_REGS,
+} hipFunction_attribute;
+
+struct EmuSymbol { void* host; size_t bytes; };
+#define HIP_SYMBOL(x) (&emu_symbol_##x)
+#define __device__
+#define __align__(n) __attribute__((aligned(n)))
+
+extern "C" {
+const char* hipGetErrorString(hipError_t e);
+hipError_t hipMalloc(void** p, size_t n);
+hipError_t hipFree(void* p);
+hipError_t hipMemcpy(void* d, const void* s, size_t n, hipMemcpyKind k);
+hipError_t hipMemcpyAsync(void* d, const void* s, size_t n, hipMemcpyKind k, hipStream_t st);
+hipError_t hipMemsetAsync(void* d, int v, size_t n, hipStream_t st);
+hipError_t hipStreamSynchronize(hipStream_t s);
+hipError_t hipEventCreate(hipEvent_t* e);
+hipError_t hipEventRecord(hipEvent_t e, hipStream_t s);
+hipError_t hipEventSynchronize(hipEvent_t e);
+hipError_t hipEventElapsedTime(float* ms, hipEvent_t a, hipEvent_t b);
+hipError_t hipEventDestroy(hipEvent_t e);
+hipError_t hipModuleLoadData(hipModule_t* m, const void* image);
+hipError_t hipModuleUnload(hipModule_t m);
+hipError_t hipModuleGetFunction(hipFunction_t* f, hipModule_t m, const char* name);
+hipError_t hipModuleLaunchKernel(hipFunction_t f, unsigned gx, unsigned gy, unsigned gz, unsigned bx, unsigned by,
+                                 unsigned bz, unsigned shmem, hipStream_t s, void** params, void** extra);
+hipError_t hipFuncGetAttribute(int* v, hipFunction_attribute a, hipFunction_t f);
+hipError_t hipGetDevice(int* d);
+hipError_t hipGetSymbolAddress(void** p, const EmuSymbol* sym);
+}
+template <class T>
+static inline hipError_t hipMalloc(T** p, size_t n) { return hipMalloc((void**)p, n); }
