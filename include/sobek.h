@@ -226,6 +226,25 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float *x, const flo
  * constant); results agree with the plain calls within rounding (the weight
  * gradient's summation splits differ). */
 int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t *bytes);
+
+/* Materialized forward (Section 2.4 eq. radial_projection_background and the edge
+ * messages of Section 2.5): the conventional evaluation order, kept as a comparison
+ * system for the memory law of Section 2.5 (eq. uvw_width_scaling) and as a second route
+ * to the forward.  It forms the per-edge weights W = phi A (E x N_w floats) and the per-edge
+ * messages M (E x dim_out floats) in the workspace, then sums M over each receiver's edges;
+ * the result equals sobek_conv_fwd's up to rounding.  Fully connected (uvw) plans in the
+ * ir_mul layout with fp32 GEMMs only (else SOBEK_E_UNSUPPORTED).
+ * sobek_materialized_workspace_size: budget 0 gives the bytes of W and M for every edge
+ * (E x (N_w + dim_out) x 4, the materialized memory); a budget gives that much (or one
+ * receiver's edges at the largest in-degree, if more), and the call then processes whole
+ * receivers in edge windows that fit.  sobek_conv_fwd_materialized takes the same inputs as
+ * sobek_conv_fwd (device pointers, 16-byte aligned) and fails with SOBEK_E_WORKSPACE when the
+ * workspace cannot hold the edges of the receiver with the largest in-degree.  The kernels
+ * are compiled (hipRTC or the on-disk cache) and loaded on the plan's first call. */
+int sobek_materialized_workspace_size(sobek_plan plan, sobek_graph graph, size_t budget, size_t *bytes);
+int sobek_conv_fwd_materialized(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                                const float *phi, const float *W, float *out, void *ws, size_t ws_bytes,
+                                hipStream_t stream);
 int sobek_conv_fwd_save(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
                         const float *phi, const float *W, float *out, float *state, void *ws,
                         size_t ws_bytes, hipStream_t stream);

@@ -72,6 +72,8 @@ _SIGNATURES = {
     "sobek_conv_bwd_saved": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "sobek_conv_dbwd_saved": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                      _P]),
+    "sobek_materialized_workspace_size": (_INT, [_P, _P, _SZ, ctypes.POINTER(_SZ)]),
+    "sobek_conv_fwd_materialized": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "sobek_profile_enable": (_INT, [_INT]),
     "sobek_profile_reset": (_INT, []),
     "sobek_profile_query": (_INT, [_INT, ctypes.c_char_p, _SZ, ctypes.POINTER(_I64), ctypes.POINTER(ctypes.c_double)]),

@@ -193,6 +193,32 @@ def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=No
     return out
 
 
+def materialized_bytes(plan, graph, budget=0):
+    """Workspace bytes of the materialized forward: W and the edge messages for every edge (budget 0), or
+    `budget` bytes of edge windows (at least one receiver's edges)."""
+    nb = ctypes.c_size_t()
+    check(lib().sobek_materialized_workspace_size(plan.handle, graph.handle, budget, ctypes.byref(nb)))
+    return int(nb.value)
+
+
+def conv_fwd_materialized(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0):
+    """The materialized forward (W = phi A and the edge messages formed in the workspace, then summed per
+    receiver): the conventional evaluation order the streamed forward avoids, same result."""
+    N, E = graph.N, graph.E
+    _check_tensor(x, "x", (N, plan.dim_in))
+    _check_tensor(evec, "evec", (E, 3))
+    _check_tensor(phi, "phi", (E, plan.K))
+    _check_tensor(W, "W", (plan.K, plan.n_weights))
+    if out is None:
+        out = torch.empty(N, plan.dim_out, dtype=torch.float32, device=x.device)
+    _check_tensor(out, "out", (N, plan.dim_out))
+    if ws is None:
+        ws = torch.empty(max(materialized_bytes(plan, graph, budget), 256), dtype=torch.uint8, device=x.device)
+    check(lib().sobek_conv_fwd_materialized(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W),
+                                            _ptr(out), _ptr(ws), ws.numel(), _stream()))
+    return out
+
+
 def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), ws=None, budget=0, state=None,
              adj_state=None):
     """(gx, gevec, gphi, gW); entries not in `need` are None.

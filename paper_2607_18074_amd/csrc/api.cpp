@@ -780,6 +780,36 @@ int load_uvu(Plan& p, hipModule_t m) {
 std::mutex g_rr_mu;
 
 // the receiver-route kernels of a channelwise plan, compiled and loaded on first use
+// The materialized baseline covers fully connected plans in the ir_mul layout with fp32 GEMMs.
+bool materialized_supported(const Plan& p) {
+  return p.mode == SOBEK_MODE_UVW && p.layout == SOBEK_LAYOUT_IR_MUL && p.dtype == SOBEK_DTYPE_F32;
+}
+
+std::mutex g_mat_mu;
+
+int ensure_materialized(sobek_plan plan) {
+  Plan& p = plan->p;
+  std::lock_guard<std::mutex> lk(g_mat_mu);
+  if (p.k.module_mat) return SOBEK_OK;
+  hipModule_t m = nullptr;
+  int rc;
+  if ((rc = load_module(sobek::generate_materialized_source(p), m))) return rc;
+  if ((rc = get_fn(m, p.k.mat_w, "sobek_mat_w")) || (rc = get_fn(m, p.k.mat_msg, "sobek_mat_msg")) ||
+      (rc = get_fn(m, p.k.mat_reduce, "sobek_mat_reduce"))) {
+    (void)hipModuleUnload(m);
+    return rc;
+  }
+  p.k.module_mat = m;
+  return SOBEK_OK;
+}
+
+// Bytes per edge of the materialized forward's workspace: W (N_w floats) and M (C_out floats).
+size_t materialized_edge_bytes(const Plan& p) { return ((size_t)p.n_w + (size_t)p.dim_out) * 4; }
+
+// Edges per W-kernel block (its grid's second axis counts blocks of them).
+constexpr int64_t kMatEdgeTile = 32;
+constexpr int64_t kMatMaxWindow = 65535 * kMatEdgeTile;
+
 int ensure_receiver_route(sobek_plan plan) {
   Plan& p = plan->p;
   std::lock_guard<std::mutex> lk(g_rr_mu);
@@ -844,6 +874,7 @@ int sobek_jit_compile(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
     // SOBEK_JIT_STATE_FREE_ONLY=1: channelwise plans compile only the part a plan loads at creation
     const char* sf = std::getenv("SOBEK_JIT_STATE_FREE_ONLY");
     if (p.source_u.empty() || !sf || std::strcmp(sf, "1") != 0) sobek::jit_compile(p.source);
+    if (materialized_supported(p)) sobek::jit_compile(sobek::generate_materialized_source(p));
   } catch (const std::exception& ex) {
     return fail(SOBEK_E_COMPILE, "%s", ex.what());
   }
@@ -912,6 +943,7 @@ int sobek_plan_destroy(sobek_plan plan) {
   if (p.d_out_blocks) (void)hipFree(p.d_out_blocks);
   if (p.k.module) (void)hipModuleUnload(p.k.module);
   if (p.k.module_u) (void)hipModuleUnload(p.k.module_u);
+  if (p.k.module_mat) (void)hipModuleUnload(p.k.module_mat);
   delete plan;
   return SOBEK_OK;
 }
@@ -1223,6 +1255,61 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
                    size_t ws_bytes, hipStream_t stream) {
   return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, nullptr, nullptr, gx, gevec, gphi, gW, ws, ws_bytes,
                        stream);
+}
+
+int sobek_materialized_workspace_size(sobek_plan plan, sobek_graph graph, size_t budget, size_t* bytes) {
+  if (!plan || !graph || !bytes) return fail(SOBEK_E_INVALID, "NULL argument");
+  const Plan& p = plan->p;
+  if (!materialized_supported(p))
+    return fail(SOBEK_E_UNSUPPORTED, "the materialized forward covers uvw plans in the ir_mul layout with fp32 GEMMs");
+  const size_t per = materialized_edge_bytes(p);
+  const size_t full = (size_t)std::max<int64_t>(1, graph->E) * per + 256;
+  const size_t least = (size_t)std::max<int64_t>(1, graph->max_deg) * per + 256;
+  *bytes = budget == 0 ? full : std::min(full, std::max(budget, least));
+  return SOBEK_OK;
+}
+
+int sobek_conv_fwd_materialized(sobek_plan plan, sobek_graph graph, const float* x, const float* evec,
+                                const float* phi, const float* W, float* out, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
+  int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
+  if (rc) return rc;
+  const Plan& p = plan->p;
+  const sobek_graph_s& G = *graph;
+  if (!materialized_supported(p))
+    return fail(SOBEK_E_UNSUPPORTED, "the materialized forward covers uvw plans in the ir_mul layout with fp32 GEMMs");
+  if (!out && G.N) return fail(SOBEK_E_INVALID, "out is NULL");
+  if (out && !aligned16(out)) return fail(SOBEK_E_ALIGN, "out is not 16-byte aligned");
+  if (G.N == 0) return SOBEK_OK;
+  // the W block of the window's edges, then its M block (256-byte aligned)
+  auto wbytes = [&](int64_t ne) { return ((size_t)ne * p.n_w * 4 + 255) / 256 * 256; };
+  auto fits = [&](int64_t ne) { return wbytes(ne) + (size_t)ne * p.dim_out * 4 <= ws_bytes; };
+  int64_t ecap = std::min<int64_t>((int64_t)(ws_bytes / materialized_edge_bytes(p)), kMatMaxWindow);
+  while (ecap > 0 && !fits(ecap)) --ecap;
+  if (G.E > 0 && ecap < std::max<int64_t>(1, G.max_deg))
+    return fail(SOBEK_E_WORKSPACE, "workspace of %zu bytes holds %lld edges, fewer than the largest in-degree %lld",
+                ws_bytes, (long long)ecap, (long long)G.max_deg);
+  if ((rc = ensure_materialized(plan))) return rc;
+  float* Wm = (float*)ws;
+  float* Mm = (float*)((char*)ws + wbytes(std::max<int64_t>(0, ecap)));
+  const int32_t* rp = G.h_rowptr.data();
+  const unsigned colb = cdiv(p.dim_out, 256);
+  const long long nw = p.n_w;
+  for (int64_t r = 0; r < G.N;) {
+    // whole receivers while their edges fit the window
+    int64_t r1 = r + 1;
+    while (r1 < G.N && rp[r1 + 1] - rp[r] <= ecap) ++r1;
+    const long long e0 = rp[r];
+    const int ne = (int)(rp[r1] - rp[r]);
+    if (ne > 0) {
+      LAUNCH(p.k.mat_w, cdiv(nw, 256), cdiv(ne, kMatEdgeTile), 1, stream, phi, W, Wm, e0, ne);
+      LAUNCH(p.k.mat_msg, ne, 1, 1, stream, (const int*)G.sender, evec, x, (const float*)Wm, Mm, e0, ne);
+    }
+    const int r0 = (int)r, nr = (int)(r1 - r);
+    LAUNCH(p.k.mat_reduce, nr, colb, 1, stream, (const int*)G.rowptr, (const float*)Mm, out, r0, nr, e0);
+    r = r1;
+  }
+  return zero_dead_out(p, out, G.N, stream);
 }
 
 int sobek_conv_bwd_saved(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,

@@ -1382,6 +1382,110 @@ void emit_uvu_wgrad(std::ostringstream& o, const Plan& P, bool tan) {
   o << "  }\n}\n";
 }
 
+// The materialized baseline (Section 2.4 eq. radial_projection_background, Section 2.5): the
+// conventional evaluation order that forms the per-edge weights W = phi A (E x N_w) and the
+// per-edge messages M (E x C_out) in memory and then reduces M over each receiver's edges.  It is
+// a comparison system for the memory law of Section 2.5 and a second route to the same forward;
+// a module of its own, compiled on first use, so that no streamed kernel's source changes.
+//   sobek_mat_w      W[e][n] = sum_q phi[e][q] A[q][n] for the window's edges (one column per
+//                    thread, A's column in registers, a tile of edges per block)
+//   sobek_mat_msg    one block per edge: the coupling values C_pi[u][m_o] of every path and input
+//                    channel in LDS, then M[e][off_g + m_o C_g + w] = sum_{pi in g} sum_u
+//                    W[e][off_pi + u C_g + w] C_pi[u][m_o] with one thread per output channel w
+//   sobek_mat_reduce out[i][c] = sum of M[e][c] over receiver i's edges
+std::string generate_materialized_source(const Plan& P) {
+  std::ostringstream o;
+  o.precision(17);
+  o << "\n// ---- materialized forward, K=" << P.K << " lmax=" << P.lmax << " N_w=" << P.n_w << "\n";
+  o << "#define K " << P.K << "\n#define NSH " << P.nsh << "\n#define CXI " << P.dim_in << "\n#define CXO " << P.dim_out
+    << "\n#define NWT " << P.n_w << "LL\n#define MAT_ET 32\n";
+  emit_sh(o, P.lmax);
+  for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
+  // W = phi A: blockIdx.x = 256 columns, blockIdx.y = MAT_ET edges of the window
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_mat_w(const float* __restrict__ phi,"
+       " const float* __restrict__ A, float* __restrict__ Wm, sb_i64 e0, int ne) {\n"
+       "  const sb_i64 col = (sb_i64)blockIdx.x * 256 + threadIdx.x;\n"
+       "  if (col >= NWT) return;\n"
+       "  float a[K];\n"
+       "#pragma unroll\n  for (int q = 0; q < K; ++q) a[q] = A[q * NWT + col];\n"
+       "  const int eb = blockIdx.y * MAT_ET, ee = min(ne, eb + MAT_ET);\n"
+       "  for (int e = eb; e < ee; ++e) {\n"
+       "    const float* ph = phi + (e0 + e) * K;\n"
+       "    float s = 0.f;\n"
+       "#pragma unroll\n    for (int q = 0; q < K; ++q) s = fmaf(ph[q], a[q], s);\n"
+       "    Wm[(sb_i64)e * NWT + col] = s;\n"
+       "  }\n}\n";
+  // per-edge messages
+  int ct = 0;
+  std::vector<int> ctoff(P.paths.size());
+  for (size_t t = 0; t < P.paths.size(); ++t) {
+    ctoff[t] = ct;
+    ct += P.paths[t].c_in * (2 * P.paths[t].l_out + 1);
+  }
+  int nch = 0;
+  for (auto& g : P.groups) nch += g.C;
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_mat_msg(const int* __restrict__ sender,"
+       " const float* __restrict__ evec, const float* __restrict__ x, const float* __restrict__ Wm,"
+       " float* __restrict__ Mm, sb_i64 e0, int ne) {\n"
+       "  __shared__ float sC[" << std::max(1, ct) << "];\n"
+       "  const int e = blockIdx.x, tid = threadIdx.x;\n"
+       "  if (e >= ne) return;\n"
+       "  const sb_i64 ge = e0 + e;\n"
+       "  const sb_i64 xrow = (sb_i64)sender[ge] * CXI;\n"
+       "  const float vx = evec[3 * ge], vy = evec[3 * ge + 1], vz = evec[3 * ge + 2];\n"
+       "  const float rinv = __builtin_amdgcn_rsqf(vx * vx + vy * vy + vz * vz);\n"
+       "  float Y[" << (P.lmax + 1) * (P.lmax + 1) << "];\n"
+       "  sb_sh_eval_L" << P.lmax << "(vx * rinv, vy * rinv, vz * rinv, Y);\n";
+  for (size_t t = 0; t < P.paths.size(); ++t) {
+    const Path& q = P.paths[t];
+    const Irrep& ri = P.in[q.i_in];
+    const int DI = 2 * q.l_in + 1, DO = 2 * q.l_out + 1;
+    const int np = (int)path_terms(q).pairs.size();
+    o << "  for (int u = tid; u < " << q.c_in << "; u += 256) {  // path " << t << "\n"
+      << "    float xv[" << DI << "], M[" << std::max(1, np) << "], C[" << DO << "];\n"
+      << "#pragma unroll\n    for (int m = 0; m < " << DI << "; ++m) xv[m] = x[xrow + " << ri.off << " + m * " << ri.mul
+      << " + u];\n"
+      << "    sb_M" << t << "(Y + " << q.l_sh * q.l_sh << ", M);\n"
+      << "    sb_C" << t << "(xv, M, C);\n"
+      << "#pragma unroll\n    for (int m = 0; m < " << DO << "; ++m) sC[" << ctoff[t] << " + u * " << DO << " + m] = C[m];\n"
+      << "  }\n";
+  }
+  o << "  __syncthreads();\n"
+       "  const float* We = Wm + (sb_i64)e * NWT;\n"
+       "  float* Me = Mm + (sb_i64)e * CXO;\n"
+       "  for (int idx = tid; idx < " << nch << "; idx += 256) {\n";
+  int base = 0;
+  for (auto& g : P.groups) {
+    o << "    if (idx >= " << base << " && idx < " << base + g.C << ") {  // output irrep " << g.i_out << "\n"
+      << "      const int w = idx - " << base << ";\n"
+      << "      float acc[" << g.d << "] = {};\n";
+    for (int t : g.paths) {
+      const Path& q = P.paths[t];
+      o << "      for (int u = 0; u < " << q.c_in << "; ++u) {  // path " << t << "\n"
+        << "        const float wv = We[" << q.w_off << "LL + u * " << g.C << " + w];\n"
+        << "#pragma unroll\n        for (int m = 0; m < " << g.d << "; ++m) acc[m] = fmaf(wv, sC[" << ctoff[t] << " + u * "
+        << g.d << " + m], acc[m]);\n"
+        << "      }\n";
+    }
+    o << "#pragma unroll\n      for (int m = 0; m < " << g.d << "; ++m) Me[" << g.off << " + m * " << g.C << " + w] = acc[m];\n"
+      << "    }\n";
+    base += g.C;
+  }
+  o << "  }\n}\n";
+  // segment sum over each receiver's edges (every output column; irreps no path reaches are
+  // cleared by the host afterwards)
+  o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_mat_reduce(const int* __restrict__ rowptr,"
+       " const float* __restrict__ Mm, float* __restrict__ out, int r0, int nr, sb_i64 e0) {\n"
+       "  const int i = blockIdx.x, c = blockIdx.y * 256 + threadIdx.x;\n"
+       "  if (c >= CXO || i >= nr) return;\n"
+       "  const int beg = rowptr[r0 + i], end = rowptr[r0 + i + 1];\n"
+       "  float s = 0.f;\n"
+       "  for (int e = beg; e < end; ++e) s += Mm[(e - e0) * CXO + c];\n"
+       "  out[(sb_i64)(r0 + i) * CXO + c] = s;\n"
+       "}\n";
+  return o.str();
+}
+
 std::string generate_source(const Plan& P, bool receiver_route) {
   std::ostringstream o;
   o.precision(17);

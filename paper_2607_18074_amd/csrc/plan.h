@@ -84,6 +84,8 @@ inline int uvu_wgrad_waves(int K, int64_t n_w) {
 struct Kernels {
   hipModule_t module = nullptr;    // every kernel of the plan (for channelwise plans with the
                                    // state-free kernels: the receiver-route kernels, loaded on first use)
+  hipModule_t module_mat = nullptr;  // the materialized-forward baseline (compiled on first use)
+  hipFunction_t mat_w = nullptr, mat_msg = nullptr, mat_reduce = nullptr;
   hipModule_t module_u = nullptr;  // channelwise plans: the state-free kernels and the common ones
   hipFunction_t fwd_S = nullptr, fwd_dS = nullptr, fwd_dS_r = nullptr;
   hipFunction_t bwd_E = nullptr, dbwd_E = nullptr, dbwd_E_r = nullptr;
@@ -140,5 +142,7 @@ struct Plan {
 void build_plan(Plan& p);
 // Generates the plan-specific HIP source (prepended by the shared prelude at compile time).
 std::string generate_source(const Plan& p, bool receiver_route = true);
+// Source of the materialized-forward baseline module (Section 2.4, eq. radial_projection_background).
+std::string generate_materialized_source(const Plan& p);
 
 }  // namespace sobek

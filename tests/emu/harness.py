@@ -198,6 +198,21 @@ def conv_dbwd(plan, graph, x, evec, phi, W, gout, t_gx=None, t_gevec=None, t_gph
     return tuple(outs)
 
 
+def materialized_bytes(plan, graph, budget=0):
+    nb = ctypes.c_size_t()
+    check(lib().sobek_materialized_workspace_size(plan.handle, graph.handle, budget, ctypes.byref(nb)))
+    return int(nb.value)
+
+
+def conv_fwd_materialized(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0):
+    out = Dev((graph.N, plan.dim_out), np.float32, "out") if out is None else out
+    if ws is None:
+        ws = Dev(max(materialized_bytes(plan, graph, budget), 256), np.uint8, "materialized workspace")
+    check(lib().sobek_conv_fwd_materialized(plan.handle, graph.handle, _p(x), _p(evec), _p(phi), _p(W), _p(out),
+                                            _p(ws), ws.nbytes, None))
+    return out
+
+
 def launches():
     """Kernel launches the emulated runtime has run so far."""
     return int(lib().emu_launch_count())

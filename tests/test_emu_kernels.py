@@ -70,6 +70,26 @@ def test_uvu_on_emulated_kernels(form, monkeypatch):
     _run(make_case("uvu_small", 40, 500, 83, isolated=1, mode="uvu"), mode="uvu")
 
 
+@pytest.mark.parametrize("sig,N,E,seed", [("tiny", 48, 600, 85), ("odd", 40, 500, 86)])
+def test_materialized_forward_on_emulated_kernels(sig, N, E, seed):
+    # W = phi A and the edge messages formed in the workspace: all edges at once, and edge windows
+    # of whole receivers at the smallest workspace the call accepts
+    from tests.emu import harness as H
+    case = make_case(sig, N, E, seed, isolated=2)
+    irr_in, lmax, irr_out, K = case["sig"]
+    plan = H.Plan(irr_in, lmax, irr_out, K)
+    g = case["graph"]
+    graph = H.Graph(g.rowptr, g.sender)
+    args = [H.dev(case["x"], "x"), H.dev(g.evec, "evec"), H.dev(g.phi, "phi"), H.dev(case["W"], "W")]
+    prob = oc.Problem(irr_in, lmax, irr_out, K)
+    ref = oc.fwd(prob, case["x"], g.evec, g.phi, case["W"], g.rowptr, g.sender)
+    full = H.materialized_bytes(plan, graph)
+    assert full >= E * (plan.n_weights + plan.dim_out) * 4
+    for budget in (0, 1):
+        out = H.conv_fwd_materialized(plan, graph, *args, budget=budget)
+        assert max_rel(out.np(), ref) <= FWD_TOL, budget
+
+
 def test_guard_zones_catch_an_out_of_bounds_write(tmp_path):
     """The check itself: an output buffer one receiver short makes the forward's last write land in
     the guard zone, which the emulated runtime reports (in a child process, which it ends)."""
