@@ -313,6 +313,77 @@ def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd")):
             f"{r['edges_per_s'] / 1e6:,.2f} M | {100 * r['frac_fp32']:.1f} | {r['peak_mem_gb']:.2f} |")
 
 
+def materialized(profiles, counts, budget_gib, mem_cap_gb=200.0):
+    """The memory law of Section 2.5 on MI355X: the materialized forward (W = phi A and the edge messages in
+    memory, eq. radial_projection_background) against the streamed forward at the same points of the
+    paper's graph-count regime (B copies of the 128-node degree-32 graph, K = 16), the streamed one at the
+    scratch budget; a point whose materialized W and messages would exceed mem_cap_gb is recorded as not
+    fitting, not run.  Roofline per row: the materialized pass against HBM (its algorithmic bytes: W and M
+    written and read once, x gathered per edge, phi and the output), the streamed pass against fp32."""
+    import torch
+
+    from paper_2607_18074_amd import api
+    from paper_2607_18074_amd import workloads as wl
+    torch.cuda.set_device(0)
+    budget = int(budget_gib * (1 << 30))
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    rows = []
+    for prof in profiles:
+        spec, lmax = wl.profile_irreps(prof)
+        plan = api.Plan(spec, lmax, spec, wl.REGIME_K)
+        W = T(wl.weights(plan.K, plan.weight_std(), 7))
+        for B in counts:
+            g = wl.graph_count_graph(B)
+            log(f"materialized sweep: {prof}, B = {B}, E = {g.E:,} ...")
+            graph = api.Graph(T(g.rowptr), T(g.sender))
+            xt, ev, ph = T(wl.node_features(g.N, plan.dim_in, 7)), T(g.evec), T(g.phi)
+            need = api.materialized_bytes(plan, graph)
+            row = dict(profile=prof, graphs=B, N=g.N, E=g.E, n_w=plan.n_weights,
+                       w_gib=g.E * plan.n_weights * 4 / 2 ** 30, mat_workspace_gb=need / 1e9)
+            fm = flop_model(plan, g.N, g.E)
+            torch.cuda.empty_cache()
+            torch.cuda.synchronize()
+            torch.cuda.reset_peak_memory_stats()
+            ws = graph.workspace(plan, "fwd", budget)
+            ms, _ = time_pass(lambda: api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws), torch)
+            row.update(streamed_ms=ms, streamed_peak_gb=torch.cuda.max_memory_allocated() / 1e9,
+                       streamed_frac_fp32=fm["passes"]["fwd"] / (ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS)
+            del ws
+            graph._ws.clear()
+            torch.cuda.empty_cache()
+            if need / 1e9 > mem_cap_gb:
+                row.update(mat_ms=None, mat_peak_gb=None, fits=False)
+            else:
+                torch.cuda.synchronize()
+                torch.cuda.reset_peak_memory_stats()
+                mws = torch.empty(need, dtype=torch.uint8, device="cuda")
+                out = torch.empty(g.N, plan.dim_out, device="cuda")
+                ms2, _ = time_pass(lambda: api.conv_fwd_materialized(plan, graph, xt, ev, ph, W, out=out, ws=mws),
+                                   torch)
+                alg = 4 * (2 * g.E * plan.n_weights + 2 * g.E * plan.dim_out + g.E * plan.dim_in
+                           + g.E * (plan.K + 3) + g.N * plan.dim_out)
+                row.update(mat_ms=ms2, mat_peak_gb=torch.cuda.max_memory_allocated() / 1e9, fits=True,
+                           mat_alg_gb=alg / 1e9, mat_frac_hbm=alg / (ms2 * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                           speedup=ms2 / ms)
+                del mws, out
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+            del graph, xt, ev, ph
+            torch.cuda.empty_cache()
+        del plan, W
+    log("| profile | B | E | W (GiB) | materialized ms | peak GB | % HBM | streamed ms | peak GB | % fp32 | streamed speedup |")
+    log("|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|")
+    for r in rows:
+        if r["fits"]:
+            m = f"{r['mat_ms']:.2f} | {r['mat_peak_gb']:.1f} | {100 * r['mat_frac_hbm']:.1f}"
+            sp = f"{r['speedup']:.1f}x"
+        else:
+            m = f"does not fit ({r['mat_workspace_gb']:.0f} GB) | — | —"
+            sp = "—"
+        log(f"| {r['profile']} | {r['graphs']} | {r['E']:,} | {r['w_gib']:.1f} | {m} | {r['streamed_ms']:.3f} | "
+            f"{r['streamed_peak_gb']:.2f} | {100 * r['streamed_frac_fp32']:.1f} | {sp} |")
+
+
 PAPER_CONTEXT = {
     "hardware": "NVIDIA RTX 5090 (32 GiB), fp32 throughout, eager, 128 MiB scratch budget (Section 5.1)",
     "workloads": "fixed 128-node degree-32 graph repeated B times, uvw profiles with K = 16 (Section 5.1, Table 3)",
@@ -429,6 +500,8 @@ def main():
     ap.add_argument("--no-retain", action="store_true",
                     help="sweep: keep no receiver state across passes (each pass recomputes within its budget, the "
                     "paper's setting for a fixed scratch budget)")
+    ap.add_argument("--materialized", default="", help="comma-separated graph counts B: the materialized forward "
+                    "against the streamed one on the --profiles at those points of the graph-count regime")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
                     help="only run a plain device copy of this many MiB (traffic-counter calibration)")
     args = ap.parse_args()
@@ -443,8 +516,8 @@ def main():
         print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 3}))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (see DESIGN.md for how it "
-              "would shard); rerun with --gpus 1", file=sys.stderr)
+        print("bench.py runs on one GPU only (the library has no multi-GPU path); rerun with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
 
     if args.tables:
@@ -454,6 +527,9 @@ def main():
     if args.regimes:
         kinds = ("degree", "count") if args.regimes == "all" else tuple(args.regimes.split(","))
         regimes(kinds, args.profiles.split(","), args.budget, args.retain)
+        return
+    if args.materialized:
+        materialized(args.profiles.split(","), [int(b) for b in args.materialized.split(",")], args.budget)
         return
     if args.sweep:
         names = ["tiny", "small", "medium", "wide", "stress"] if args.sweep == "all" else args.sweep.split(",")
