@@ -204,7 +204,8 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float *x, const flo
  * bytes of the state of every receiver of a graph: N * (sum over output groups
  * of (2l+1) * K * sum of C_in of the group's paths) floats, in a library-defined
  * order that callers treat as opaque.  It is bounded by the node count, never
- * by the edge count.
+ * by the edge count.  Plans with SOBEK_DTYPE_BF16_GEMM store S (not Sbar) in
+ * bf16 and use the first half of such a buffer.
  *
  * sobek_conv_fwd_save is sobek_conv_fwd that also leaves S of every receiver in
  * `state` (caller-owned device memory of sobek_state_size bytes, 16-byte

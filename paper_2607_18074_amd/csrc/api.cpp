@@ -493,6 +493,16 @@ float* state_ptr(const WsPlan& w, void* ws, const Plan& p, int which) {
   return (float*)((char*)ws + w.off_state) + (size_t)which * w.ncap * p.srow;
 }
 
+// Bytes per element of the receiver state S (and dS): bf16 for plans whose channel GEMMs run on
+// bf16 MFMA (they round S to bf16 as they read it, so storing it rounded changes nothing but the
+// bytes), fp32 otherwise.  The adjoint state S-bar is fp32 for every plan.
+size_t state_elem(const Plan& p) { return p.dtype == SOBEK_DTYPE_BF16_GEMM ? 2 : 4; }
+
+// Pointer `elems` state elements past S.
+const float* state_at(const Plan& p, const float* S, size_t elems) {
+  return (const float*)((const char*)S + elems * state_elem(p));
+}
+
 // S (or dS) for the chunk
 int run_state(const Plan& p, const sobek_graph_s& G, const Chunk& c, const WsPlan& w, float* S, bool tangent,
               const float* x, const float* evec, const float* phi, const float* xdot, const float* evdot,
@@ -511,7 +521,7 @@ int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const floa
             int acc, hipStream_t s) {
   float* K = (float*)((char*)ws + w.off_K);
   for (auto& g : p.groups) {
-    const float* Sg = S + (size_t)w.ncap * g.s_off;
+    const float* Sg = state_at(p, S, (size_t)w.ncap * g.s_off);
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     if (p.mode == SOBEK_MODE_UVU) {
       LAUNCH(p.k.uvu_mix, cdiv((int64_t)nrows * Cg, 256), 1, 1, s, Sg, nrows, D, Cg, W,
@@ -571,7 +581,7 @@ int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float
            float* gW, bool first_chunk, bool last_chunk, hipStream_t s) {
   float* P = (float*)((char*)ws + w.off_P);
   for (auto& g : p.groups) {
-    const float* Sg = S + (size_t)s_ncap * g.s_off;
+    const float* Sg = state_at(p, S, (size_t)s_ncap * g.s_off);
     int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
     int ns = nsplit_for(g, (int64_t)w.ncap * g.d, p.vec4);
     int rps = (int)(((int64_t)cdiv(nrows, ns) + 31) / 32 * 32);
@@ -1235,6 +1245,8 @@ extern "C" {
 
 int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t* bytes) {
   if (!plan || !graph || !bytes) return fail(SOBEK_E_INVALID, "NULL argument");
+  // fp32 elements for every plan: the same size serves the adjoint state (fp32), and a bf16 state
+  // uses the first half
   *bytes = (size_t)graph->N * plan->p.srow * 4;
   return SOBEK_OK;
 }

@@ -19,6 +19,14 @@
 // register r of lane j + 16g, as for the fp32 instruction.
 
 typedef __bf16 sb_b8 __attribute__((ext_vector_type(8)));
+typedef __bf16 sb_b4 __attribute__((ext_vector_type(4)));
+
+// Four consecutive bf16 values of the receiver state (stored in bf16 by the state kernels of these
+// plans), widened to fp32 for the LDS stage.
+SB_DEV sb_v4 sb_ld4_b(const __bf16* p) {
+  const sb_b4 v = *(const sb_b4*)p;
+  return (sb_v4){(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
 
 // acc += the 32-deep slab product of sA[kk][32 * wave + 0..31] and sB[kk][0..BN-1]
 // (kk = 0..31, the reduction index), rounded to bf16 as it leaves LDS
@@ -43,7 +51,7 @@ SB_DEV void sb_slab_bf16(const float (*sA)[SB_VM + 4], const float (*sB)[BN + 4]
 }
 
 template <int BN>
-SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const float* __restrict__ W,
+SB_DEV void sb_gemm_sa_vb(const __bf16* __restrict__ S, int nrows, int D, const float* __restrict__ W,
                           const int* __restrict__ ktab, float* __restrict__ out, int dg, int Cg, int off, int CX,
                           int r0, int accumulate, float* __restrict__ P, int kper) {
   __shared__ float sA[SB_VK][SB_VM + 4];
@@ -65,7 +73,7 @@ SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const f
     for (int i = 0; i < 4; ++i) {
       const int row = (tid >> 3) + 32 * i, k = k0 + 4 * (tid & 7);
       const int gr = rb + row;
-      ra[i] = (gr < nrows && k < kend) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+      ra[i] = (gr < nrows && k < kend) ? sb_ld4_b(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
@@ -125,7 +133,7 @@ SB_DEV void sb_gemm_sa_vb(const float* __restrict__ S, int nrows, int D, const f
 // (Section 4.3 eq. receiver_adjoint, A_bar = S^T mbar): the blocking of sb_gemm_ga_v (a 128-k x
 // BN-w block walking 32-row slabs of its split), with the slab product on bf16 MFMA.
 template <int BN>
-SB_DEV void sb_gemm_ga_vb(const float* __restrict__ S, int nrows, int D, const float* __restrict__ M,
+SB_DEV void sb_gemm_ga_vb(const __bf16* __restrict__ S, int nrows, int D, const float* __restrict__ M,
                           float* __restrict__ P, int dg, int Cg, int off, int CX, int r0, int rows_per_split,
                           int accumulate) {
   __shared__ float sA[SB_VK][SB_VM + 4];
@@ -146,7 +154,7 @@ SB_DEV void sb_gemm_ga_vb(const float* __restrict__ S, int nrows, int D, const f
     for (int i = 0; i < 4; ++i) {
       const int rr = (tid >> 5) + 8 * i, k = kb + 4 * (tid & 31);
       const int gr = rr0 + rr;
-      ra[i] = (gr < rend && k < D) ? sb_ld4(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+      ra[i] = (gr < rend && k < D) ? sb_ld4_b(S + (sb_i64)gr * D + k) : (sb_v4){0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
@@ -202,12 +210,12 @@ SB_DEV void sb_gemm_ga_vb(const float* __restrict__ S, int nrows, int D, const f
 
 #define SB_GEMM_VB_ENTRY(BN)                                                                         \
   extern "C" __global__ __launch_bounds__(256) void sobek_gemm_sa_vb##BN(                           \
-      const float* S, int nrows, int D, const float* W, const int* ktab, float* out, int dg,       \
+      const __bf16* S, int nrows, int D, const float* W, const int* ktab, float* out, int dg,       \
       int Cg, int off, int CX, int r0, int accumulate, float* P, int kper) {                       \
     sb_gemm_sa_vb<BN>(S, nrows, D, W, ktab, out, dg, Cg, off, CX, r0, accumulate, P, kper);        \
   }                                                                                                \
   extern "C" __global__ __launch_bounds__(256) void sobek_gemm_ga_vb##BN(                           \
-      const float* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \
+      const __bf16* S, int nrows, int D, const float* M, float* P, int dg, int Cg, int off, int CX, \
       int r0, int rows_per_split, int accumulate) {                                                \
     sb_gemm_ga_vb<BN>(S, nrows, D, M, P, dg, Cg, off, CX, r0, rows_per_split, accumulate);         \
   }

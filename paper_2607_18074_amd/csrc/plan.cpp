@@ -418,13 +418,14 @@ int unit_lsh(const Plan& P, const Unit& u) {
 // next block already loaded, and handed to the lanes of an edge by a shuffle.
 void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) {
   const Irrep& ri = P.in[u.a];
+  const char* st = P.dtype == 1 ? "__bf16" : "float";  // the state's storage type (bf16 for bf16-GEMM plans)
   const int DA = 2 * ri.l + 1, L = unit_lsh(P, u), NS = (L + 1) * (L + 1);
   const bool mf = (u.U % 4 == 0) && (P.K % 4 == 0);
   const int KQ = P.K / 4;
   const int NPH = mf ? KQ : P.K;
   o << "template <bool TAN, int FL>\nSB_DEV void sb_fwd_u" << id
     << "(int lane, int il, int beg, int end, const int* __restrict__ sender, const float* __restrict__ evec,"
-       " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, sb_i64 ncap,"
+       " const float* __restrict__ phi, const float* __restrict__ x, " << st << "* __restrict__ S, sb_i64 ncap,"
        " const float* __restrict__ xdot, const float* __restrict__ evdot, const float* __restrict__ phidot, int flags,"
        " int* ids) {\n";
   o << "  const int fl = FL >= 0 ? FL : flags;\n";
@@ -559,7 +560,7 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
     const Path& q = P.paths[t];
     const Group& g = P.groups[q.group];
     const int DO = 2 * q.l_out + 1;
-    o << "    {\n      constexpr int DO = " << DO << ";\n      float* Sg = S + ncap * " << g.s_off
+    o << "    {\n      constexpr int DO = " << DO << ";\n      " << st << "* Sg = S + ncap * " << g.s_off
       << "LL + (sb_i64)il * " << (int64_t)g.d * g.D << "LL + " << q.koff << ";\n";
     if (mf) {
       o << "      const int ub = U0 + 4 * ((lane % U) >> 2), j = lane & 3;\n"
@@ -1529,7 +1530,8 @@ std::string generate_source(const Plan& P, bool receiver_route) {
   // reduced-precision plans: the bf16 variant of the vec4 channel GEMM
   if (P.dtype == 1) o << kGemmBf16;
 
-  // forward S / dS kernels: one wave per (receiver, unit)
+  // forward S / dS kernels: one wave per (receiver, unit); bf16-GEMM plans store the state in bf16
+  const char* st = P.dtype == 1 ? "__bf16" : "float";
   for (int t = 0; t < (int)P.fwd_units.size(); ++t) emit_fwd_unit(o, P, P.fwd_units[t], t);
   const int NU = (int)P.fwd_units.size();
   struct FV { const char* name; bool tan; int fl; };
@@ -1539,7 +1541,7 @@ std::string generate_source(const Plan& P, bool receiver_route) {
     o << "extern \"C\" __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void sobek_fwd_"
       << fv.name
       << "(const int* __restrict__ rowptr, const int* __restrict__ sender, const float* __restrict__ evec,"
-         " const float* __restrict__ phi, const float* __restrict__ x, float* __restrict__ S, int r0, int n_recv,"
+         " const float* __restrict__ phi, const float* __restrict__ x, " << st << "* __restrict__ S, int r0, int n_recv,"
          " sb_i64 ncap, const float* __restrict__ xdot, const float* __restrict__ evdot,"
          " const float* __restrict__ phidot, int flags) {\n"
       << "  __shared__ int sids[4][256];\n"

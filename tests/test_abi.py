@@ -118,13 +118,17 @@ def test_bf16_gemm_option():
     sig = ("32x0e+32x1o+32x2e", 2, "32x0e+32x1o+32x2e", 8)
     s32 = _lib.plan_source(*sig)
     sbf = _lib.plan_source(*sig, "ir_mul", "none", "uvw", "bf16_gemm")
-    # the bf16 GEMM text is added to bf16 plans only: removing it gives the fp32 source exactly
+    # the bf16 GEMM text is added to bf16 plans only, and their state kernels store S in bf16:
+    # removing the one and restoring the fp32 state type gives the fp32 source exactly
     here = os.path.dirname(os.path.abspath(__file__))
     with open(os.path.join(here, "..", "paper_2607_18074_amd", "csrc", "device", "gemm_bf16.hip")) as f:
         block = "\n" + f.read() + "\n"
     assert "__builtin_amdgcn_mfma_f32_16x16x32_bf16" in sbf and "SB_GEMM_VB_ENTRY(64)" in sbf
     assert "bf16" not in s32
-    assert sbf.count(block) == 1 and sbf.replace(block, "") == s32
+    assert sbf.count(block) == 1
+    rest = sbf.replace(block, "")
+    assert rest.count("__bf16* __restrict__ S,") >= 4 and rest.count("__bf16* Sg = S") >= 1   # 3 kernels + the units
+    assert rest.replace("__bf16* __restrict__ S,", "float* __restrict__ S,").replace("__bf16* Sg = S", "float* Sg = S") == s32
     # reduced precision is implemented for uvw plans whose multiplicities are multiples of 4
     for args in (("8x0e+8x1o", 1, "8x0e+8x1o", 4, "ir_mul", "none", "uvu", "bf16_gemm"),
                  ("6x0e+4x1o", 1, "6x0e+4x1o", 4, "ir_mul", "none", "uvw", "bf16_gemm")):

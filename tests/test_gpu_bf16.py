@@ -112,6 +112,35 @@ def test_bf16_double_backward(gpu, sig, N, E, seed, iso):
         assert err <= (BF16_TOL if name in ("g_gout", "g_W") else BWD_TOL), name
 
 
+def test_bf16_retained_states(gpu):
+    """The bf16 plan keeps S in bf16 (the first half of a sobek_state_size buffer) and the adjoint state in
+    fp32 (a whole one): forward, backward and double backward through the kept states match the oracle
+    (bf16-GEMM outputs within the bf16 tolerance) and agree with the plain calls."""
+    case = make_case("small", 300, 4000, 31, isolated=2)
+    api, plan, graph, prob = _setup(case, "bf16_gemm")
+    g = case["graph"]
+    args = (_t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]))
+    oa = (prob, case["x"], g.evec, g.phi, case["W"], g.rowptr, g.sender)
+    state, adj = api.new_state(plan, graph), api.new_state(plan, graph)
+    state.fill_(float("nan"))
+    adj.fill_(float("nan"))
+    m = api.conv_fwd(plan, graph, *args, state=state)
+    assert max_rel(_n(m), oc.fwd(*oa)) <= BF16_TOL
+    assert np.isnan(_n(state)[state.numel() // 2:]).all()      # the bf16 state fills the first half only
+    gout = _t(case["gout"])
+    outs = api.conv_bwd(plan, graph, *args, gout, state=state, adj_state=adj)
+    plain = api.conv_bwd(plan, graph, *args, gout)
+    ref = oc.bwd(*oa, case["gout"])
+    for name, o, q in zip(("gx", "gevec", "gphi", "gW"), outs, plain):
+        assert max_rel(_n(o), ref[name]) <= (BF16_TOL if name == "gW" else BWD_TOL), name
+        assert max_rel(_n(o), _n(q)) <= 1e-4, name
+    tev = _t(case["cot"]["evec"])
+    outs = api.conv_dbwd(plan, graph, *args, gout, None, tev, None, None, adj_state=adj)
+    ref = oc.dbwd(*oa, case["gout"], t_gevec=case["cot"]["evec"])
+    for name, o in zip(("g_gout", "g_x", "g_evec", "g_phi", "g_W"), outs):
+        assert max_rel(_n(o), ref[name]) <= (BF16_TOL if name in ("g_gout", "g_W") else BWD_TOL), name
+
+
 @pytest.mark.timeout(600)
 def test_bf16_full_size_wide(gpu):
     """The Wide workload at full size (50,000 nodes, 2.0M edges) in the benchmark's launch
