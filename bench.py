@@ -128,7 +128,23 @@ def time_pass(fn, torch):
     return float(np.median(samples)), len(samples)
 
 
-def sweep(budget_gib, names, dtype="f32", retain=True):
+def pass_kernels(fn, torch, calls=3):
+    """Mean per-pass time of every kernel of one pass (the library's HIP-event launch timer)."""
+    from paper_2607_18074_amd import _lib
+    torch.cuda.synchronize()
+    _lib.profile_reset()
+    _lib.profile_enable(True)
+    try:
+        for _ in range(calls):
+            fn()
+        torch.cuda.synchronize()
+        prof = _lib.profile_read()
+    finally:
+        _lib.profile_enable(False)
+    return {k: dict(launches=n / calls, ms=t / calls) for k, (n, t) in sorted(prof.items(), key=lambda kv: -kv[1][1])}
+
+
+def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False):
     """Every workload and pass of the benchmark configurations: one JSON line each, then a table.
     dtype "bf16_gemm" runs the plans' channel GEMM m = S A on bf16 MFMA (tensors stay fp32)."""
     import torch
@@ -189,6 +205,8 @@ def sweep(budget_gib, names, dtype="f32", retain=True):
                        peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9,
                        workspace_gb=ws[pname].numel() / 1e9,
                        retained_state_gb=sum(t.numel() * 4 / 1e9 for t in (state, adj) if t is not None))
+            if kernels:
+                row["kernels"] = pass_kernels(fns[pname], torch)
             rows.append(row)
             print(json.dumps({k.rstrip("_"): v for k, v in row.items()}), flush=True)
         del fns, ws, state, adj, out, xt, Wt, gt, ev, ph, graph, plan
@@ -198,6 +216,14 @@ def sweep(budget_gib, names, dtype="f32", retain=True):
     for r in rows:
         log(f"| {r['workload']} | {r['pass_']} | {r['E']:,} | {r['ms']:.3f} | {r['edges_per_s'] / 1e6:,.1f} M | "
             f"{r['tflops']:.1f} | {100 * r['frac_fp32']:.1f} | {r['alg_gbs']:.0f} | {r['peak_mem_gb']:.2f} |")
+    if kernels:
+        log("")
+        log("| workload | pass | kernel | launches | ms per pass |")
+        log("|---|---|---|---:|---:|")
+        for r in rows:
+            for k, v in r["kernels"].items():
+                if v["ms"] >= 0.05:
+                    log(f"| {r['workload']} | {r['pass_']} | `{k}` | {v['launches']:g} | {v['ms']:.3f} |")
 
 
 def time_graph_passes(plan, W, g, passes, budget, retain):
@@ -497,6 +523,7 @@ def main():
     ap.add_argument("--table-profiles", default="", help="tables: comma-separated subset of profiles (default all)")
     ap.add_argument("--retain", action="store_true", help="regimes: keep S and Sbar across passes (default: the "
                     "paper's setting, recompute within the workspace budget)")
+    ap.add_argument("--kernels", action="store_true", help="sweep: also time every kernel of each pass")
     ap.add_argument("--no-retain", action="store_true",
                     help="sweep: keep no receiver state across passes (each pass recomputes within its budget, the "
                     "paper's setting for a fixed scratch budget)")
@@ -533,7 +560,7 @@ def main():
         return
     if args.sweep:
         names = ["tiny", "small", "medium", "wide", "stress"] if args.sweep == "all" else args.sweep.split(",")
-        sweep(args.budget, names, args.dtype, not args.no_retain)
+        sweep(args.budget, names, args.dtype, not args.no_retain, args.kernels)
         return
 
     import torch
