@@ -144,9 +144,10 @@ def pass_kernels(fn, torch, calls=3):
     return {k: dict(launches=n / calls, ms=t / calls) for k, (n, t) in sorted(prof.items(), key=lambda kv: -kv[1][1])}
 
 
-def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False):
+def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False, policy="all"):
     """Every workload and pass of the benchmark configurations: one JSON line each, then a table.
-    dtype "bf16_gemm" runs the plans' channel GEMM m = S A on bf16 MFMA (tensors stay fp32)."""
+    dtype "bf16_gemm" runs the plans' channel GEMM m = S A on bf16 MFMA (tensors stay fp32); policy
+    "groups" builds receiver state one output group at a time (eq. receiver_chunk_budget)."""
     import torch
 
     from paper_2607_18074_amd import api
@@ -157,7 +158,7 @@ def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False):
     for name in names:
         cfg = wl.CONFIGS[name]
         g = wl.config_graph(name)
-        plan = api.Plan(cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"], dtype=dtype)
+        plan = api.Plan(cfg["irreps_in"], cfg["lmax"], cfg["irreps_out"], cfg["K"], dtype=dtype, policy=policy)
         T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
         graph = api.Graph(T(g.rowptr), T(g.sender))
         xt = T(wl.node_features(g.N, plan.dim_in, cfg["index"]))
@@ -199,6 +200,8 @@ def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False):
             tag = name if dtype == "f32" else f"{name} ({dtype})"
             if not retain:
                 tag += f" [no kept state, {budget_gib:g} GiB]"
+            if policy != "all":
+                tag += f" [{policy} policy]"
             row = dict(workload=tag, dtype=dtype, retain=retain, pass_=pname,
                        N=g.N, E=g.E, ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3),
                        tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS, alg_gbs=gbs, frac_hbm=gbs / PEAK_HBM_GBS,
@@ -226,8 +229,10 @@ def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False):
                     log(f"| {r['workload']} | {r['pass_']} | `{k}` | {v['launches']:g} | {v['ms']:.3f} |")
 
 
-def time_graph_passes(plan, W, g, passes, budget, retain):
-    """Time each pass of `passes` on graph g with the paper's protocol; one dict per pass."""
+def time_graph_passes(plan, W, g, passes, budget, retain, keep_groups=False):
+    """Time each pass of `passes` on graph g with the paper's protocol; one dict per pass.  keep_groups:
+    the forward keeps the output groups that sobek_retention_select picks within `budget` and the
+    backward reads them (the rest recomputed one group at a time)."""
     import torch
 
     from paper_2607_18074_amd import api
@@ -238,6 +243,10 @@ def time_graph_passes(plan, W, g, passes, budget, retain):
     gt = T(wl.out_cotangent(g.N, plan.dim_out, 7))
     state = api.new_state(plan, graph) if retain else None
     adj = api.new_state(plan, graph) if retain else None
+    keep = None
+    if keep_groups:
+        mask = api.retention(plan, graph, budget)[0]
+        keep = (mask, api.new_kept(plan, graph, mask))
     fm = flop_model(plan, g.N, g.E)
     out = []
     for pname in passes:
@@ -245,12 +254,12 @@ def time_graph_passes(plan, W, g, passes, budget, retain):
         torch.cuda.empty_cache()
         ws = graph.workspace(plan, pname, budget)
         if pname == "fwd":
-            fn = lambda: api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)  # noqa: E731
+            fn = lambda: api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state, keep=keep)  # noqa: E731
         elif pname == "bwd":
-            if retain:
-                api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state)
+            if retain or keep:
+                api.conv_fwd(plan, graph, xt, ev, ph, W, ws=ws, state=state, keep=keep)
             fn = lambda: api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,  # noqa: E731
-                                      adj_state=adj)
+                                      adj_state=adj, kept=keep)
         else:
             rdot = (2.0 * api.conv_bwd(plan, graph, xt, ev, ph, W, gt, ws=ws, state=state,
                                        adj_state=adj)[1]).contiguous()
@@ -261,6 +270,7 @@ def time_graph_passes(plan, W, g, passes, budget, retain):
         ms, n = time_pass(fn, torch)
         tf = fm["passes"][pname] / (ms * 1e-3) / 1e12
         out.append(dict(N=g.N, E=g.E, mean_degree=g.E / g.N, pass_=pname, ms=ms, samples=n,
+                        kept_groups=hex(keep[0]) if keep else None,
                         edges_per_s=g.E / (ms * 1e-3), tflops=tf, frac_fp32=tf / PEAK_FP32_TFLOPS,
                         peak_mem_gb=torch.cuda.max_memory_allocated() / 1e9, workspace_gb=ws.numel() / 1e9))
         del ws, fn
@@ -308,7 +318,7 @@ def tables(which, budget_gib, retain, only=()):
             f"{r['peak_mem_gb']:.2f} |")
 
 
-def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd")):
+def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd"), policy="all", keep_groups=False):
     """The paper's scaling regimes: degree scaling (2,048 nodes, mean degree 4..1,023) and graph-count
     scaling (B copies of a 128-node degree-32 graph, B = 2..511) on its representative profiles, every
     pass timed with the paper's protocol; one JSON line per point, a table at the end."""
@@ -321,14 +331,14 @@ def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd")):
     rows = []
     for prof in profiles:
         spec, lmax = wl.profile_irreps(prof)
-        plan = api.Plan(spec, lmax, spec, wl.REGIME_K)
+        plan = api.Plan(spec, lmax, spec, wl.REGIME_K, policy=policy)
         W = torch.from_numpy(wl.weights(plan.K, plan.weight_std(), 7)).cuda()
         points = [("degree", d) for d in wl.DEGREE_GRID if "degree" in kinds] + \
                  [("count", b) for b in wl.GRAPH_COUNT_GRID if "count" in kinds]
         for kind, v in points:
             g = wl.degree_graph(v)[0] if kind == "degree" else wl.graph_count_graph(v)
-            for row in time_graph_passes(plan, W, g, passes, budget, retain):
-                row.update(profile=prof, regime=kind, value=v)
+            for row in time_graph_passes(plan, W, g, passes, budget, retain, keep_groups):
+                row.update(profile=prof, regime=kind, value=v, policy=policy)
                 rows.append(row)
                 print(json.dumps({k.rstrip("_"): x for k, x in row.items()}), flush=True)
         del plan, W
@@ -524,6 +534,13 @@ def main():
     ap.add_argument("--retain", action="store_true", help="regimes: keep S and Sbar across passes (default: the "
                     "paper's setting, recompute within the workspace budget)")
     ap.add_argument("--kernels", action="store_true", help="sweep: also time every kernel of each pass")
+    ap.add_argument("--policy", default="all", choices=["all", "groups"],
+                    help="sweep/regimes: scratch policy of the plans (groups: receiver state one output group "
+                         "at a time, eq. receiver_chunk_budget)")
+    ap.add_argument("--keep-groups", action="store_true",
+                    help="regimes: the forward keeps the output groups the retention choice fits in the budget "
+                         "and the backward reads them")
+    ap.add_argument("--passes", default="fwd,bwd,dbwd", help="regimes: passes to time")
     ap.add_argument("--no-retain", action="store_true",
                     help="sweep: keep no receiver state across passes (each pass recomputes within its budget, the "
                     "paper's setting for a fixed scratch budget)")
@@ -553,14 +570,15 @@ def main():
         return
     if args.regimes:
         kinds = ("degree", "count") if args.regimes == "all" else tuple(args.regimes.split(","))
-        regimes(kinds, args.profiles.split(","), args.budget, args.retain)
+        regimes(kinds, args.profiles.split(","), args.budget, args.retain, tuple(args.passes.split(",")),
+                args.policy, args.keep_groups)
         return
     if args.materialized:
         materialized(args.profiles.split(","), [int(b) for b in args.materialized.split(",")], args.budget)
         return
     if args.sweep:
         names = ["tiny", "small", "medium", "wide", "stress"] if args.sweep == "all" else args.sweep.split(",")
-        sweep(args.budget, names, args.dtype, not args.no_retain, args.kernels)
+        sweep(args.budget, names, args.dtype, not args.no_retain, args.kernels, args.policy)
         return
 
     import torch

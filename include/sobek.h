@@ -78,6 +78,7 @@ enum { SOBEK_LAYOUT_IR_MUL = 0, SOBEK_LAYOUT_MUL_IR = 1 };
 enum { SOBEK_DTYPE_F32 = 0, SOBEK_DTYPE_BF16_GEMM = 1 };
 enum { SOBEK_NORM_NONE = 0, SOBEK_NORM_FAN_IN = 1 };
 enum { SOBEK_MODE_UVW = 0, SOBEK_MODE_UVU = 1 };
+enum { SOBEK_POLICY_ALL_GROUPS = 0, SOBEK_POLICY_PER_GROUP = 1 };
 enum { SOBEK_PASS_FWD = 0, SOBEK_PASS_BWD = 1, SOBEK_PASS_DBWD = 2 };
 
 /* One irreducible representation: multiplicity, order l >= 0, parity +1 ('e') or -1 ('o'). */
@@ -136,7 +137,9 @@ int sobek_plan_destroy(sobek_plan plan);
  * Channelwise plans with the state-free kernels load those at creation and the
  * receiver-route kernels on first use (a double backward with cotangents other
  * than the edge vectors', a forward that keeps its state); both are compiled
- * here, or only the first with SOBEK_JIT_STATE_FREE_ONLY=1 in the environment. */
+ * here, or only the first with SOBEK_JIT_STATE_FREE_ONLY=1 in the environment.
+ * SOBEK_JIT_GROUPS=1 also compiles the per-output-group state kernels
+ * (sobek_plan_set_policy, sobek_conv_fwd_keep). */
 int sobek_jit_compile(const sobek_irrep *in, int n_in, int lmax, const sobek_irrep *out, int n_out, int K,
                       int mode, int layout, int dtype, int path_norm);
 /* Full HIP source generated for a signature (prelude + plan code), NUL-terminated
@@ -227,6 +230,50 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float *x, const flo
  * constant); results agree with the plain calls within rounding (the weight
  * gradient's summation splits differ). */
 int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t *bytes);
+
+/* Scratch policy of a plan's receiver-state legs (Appendix B.2, eq. receiver_chunk_budget).
+ * SOBEK_POLICY_ALL_GROUPS (the default): each receiver chunk builds the state of every output
+ * group, in chunks sized by the workspace planner.  SOBEK_POLICY_PER_GROUP: the forward, the
+ * backward's weight gradient and the double backward's state legs (dS and S) take one output
+ * group g at a time, in chunks of n_g = min(N, max(1, floor(B / (4 d_g (D_g + C_g))))) receivers,
+ * with B the bytes of the pass workspace's receiver-state region (d_g = 2l+1, D_g the group's
+ * state width, C_g its output multiplicity); the adjoint edge legs keep all-group receiver chunks.
+ * Workspace sizes do not change.  Results agree with the default within rounding (the channel
+ * GEMMs' split sums follow the chunk sizes) and are deterministic for a given policy and workspace
+ * size.  The per-group kernels are compiled (hipRTC or the on-disk cache) and loaded on first use.
+ * Not thread-safe against calls running on the plan. */
+int sobek_plan_set_policy(sobek_plan plan, int policy);
+
+/* Retention of complete output groups (Section 4.2: forward state is kept only as whole output
+ * groups within the scratch budget, the others recomputed over bounded receiver ranges; Appendix
+ * B.2).  A kept state for `group_mask` (bit g = output group g: the g-th output irrep, in order,
+ * that some path reaches; groups past the 64th cannot be kept) holds, group by group in that order, the N d_g D_g state elements of
+ * each kept group: fp32, or bf16 for SOBEK_DTYPE_BF16_GEMM plans.
+ * sobek_kept_size: its bytes (SOBEK_E_INVALID for mask bits past the plan's groups).
+ * sobek_retention_select: the paper's choice within `budget` bytes (0 = 1 GiB): for uvw plans the
+ * subset of groups whose kept bytes fit and that avoids the most recomputed coupling work (the
+ * sum over the group's paths of the non-zero coefficients times C_in), ties to fewer bytes (exact
+ * over all subsets up to 20 groups, else groups taken greedily by work per byte); for uvu plans
+ * every group when all fit, else none; none for channelwise plans whose weight gradient is
+ * state-free.  *bytes gets the kept bytes of the chosen mask.
+ * sobek_conv_fwd_keep: sobek_conv_fwd that writes the state of the groups of `group_mask` into
+ * `kept` (caller-owned device memory of sobek_kept_size bytes, 16-byte aligned; overwritten) and
+ * streams the other groups one group at a time as SOBEK_POLICY_PER_GROUP does.
+ * sobek_conv_bwd_kept: sobek_conv_bwd whose weight gradient reads those groups from `kept` (written
+ * by sobek_conv_fwd_keep with the same plan, graph, mask, x, evec and phi) and recomputes the others
+ * one group at a time; gW NULL leaves `kept` unread.
+ * Both take the workspace of their pass (sobek_workspace_size); results agree with the plain calls
+ * within rounding.  Channelwise (uvu) plans keep every group or none (else SOBEK_E_INVALID). */
+int sobek_kept_size(sobek_plan plan, sobek_graph graph, uint64_t group_mask, size_t *bytes);
+int sobek_retention_select(sobek_plan plan, sobek_graph graph, size_t budget, uint64_t *group_mask,
+                           size_t *bytes);
+int sobek_conv_fwd_keep(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                        const float *phi, const float *W, float *out, uint64_t group_mask, float *kept,
+                        void *ws, size_t ws_bytes, hipStream_t stream);
+int sobek_conv_bwd_kept(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
+                        const float *phi, const float *W, const float *gout, uint64_t group_mask,
+                        const float *kept, float *gx, float *gevec, float *gphi, float *gW, void *ws,
+                        size_t ws_bytes, hipStream_t stream);
 
 /* Materialized forward (Section 2.4 eq. radial_projection_background and the edge
  * messages of Section 2.5): the conventional evaluation order, kept as a comparison

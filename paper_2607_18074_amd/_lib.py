@@ -72,6 +72,11 @@ _SIGNATURES = {
     "sobek_conv_bwd_saved": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "sobek_conv_dbwd_saved": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                      _P]),
+    "sobek_plan_set_policy": (_INT, [_P, _INT]),
+    "sobek_kept_size": (_INT, [_P, _P, ctypes.c_uint64, ctypes.POINTER(_SZ)]),
+    "sobek_retention_select": (_INT, [_P, _P, _SZ, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(_SZ)]),
+    "sobek_conv_fwd_keep": (_INT, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _SZ, _P]),
+    "sobek_conv_bwd_kept": (_INT, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "sobek_materialized_workspace_size": (_INT, [_P, _P, _SZ, ctypes.POINTER(_SZ)]),
     "sobek_conv_fwd_materialized": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "sobek_profile_enable": (_INT, [_INT]),

@@ -39,13 +39,18 @@ def _check_tensor(t, name, shape, dtype=torch.float32):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
+POLICIES = {"all": 0, "groups": 1}
+
+
 class Plan:
     """Operator signature: irreps, spherical-harmonic order, radial width, channel mode ("uvw" fully
     connected, "uvu" channelwise), dtype ("f32", or "bf16_gemm": the channel GEMMs with the receiver
-    state, m = S A and A_bar = S^T mbar, on bf16 MFMA with fp32 accumulation; tensors stay fp32)."""
+    state, m = S A and A_bar = S^T mbar, on bf16 MFMA with fp32 accumulation; tensors stay fp32), and
+    scratch policy ("all": every output group per receiver chunk; "groups": the receiver-state legs one
+    output group at a time in chunks of n_g receivers, eq. receiver_chunk_budget)."""
 
     def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw",
-                 dtype="f32"):
+                 dtype="f32", policy="all"):
         self.irreps_in = _lib.parse_irreps(irreps_in)
         self.irreps_out = _lib.parse_irreps(irreps_out)
         self.lmax, self.K, self.layout, self.normalization = int(lmax), int(K), layout, normalization
@@ -57,6 +62,12 @@ class Plan:
         vals = [ctypes.c_int64() for _ in range(5)]
         check(lib().sobek_plan_info(h, *[ctypes.byref(v) for v in vals]))
         self.n_paths, self.n_weights, self.dim_in, self.dim_out, self.dim_sh = (v.value for v in vals)
+        self.policy = "all"
+        self.set_policy(policy)
+
+    def set_policy(self, policy):
+        check(lib().sobek_plan_set_policy(self._h, POLICIES[policy]))
+        self.policy = policy
 
     @property
     def handle(self):
@@ -172,8 +183,37 @@ def _check_state(plan, graph, state):
             raise ValueError("state buffer is smaller than sobek_state_size")
 
 
-def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=None):
-    """m = conv(x, evec, phi, W); with `state` (from new_state) S of every receiver is kept in it."""
+def retention(plan, graph, budget=0):
+    """(group mask, kept bytes) of the output groups whose state the forward keeps within `budget` bytes
+    (0 = 1 GiB): the subset that avoids the most recomputed coupling work, ties to fewer bytes."""
+    m, nb = ctypes.c_uint64(), ctypes.c_size_t()
+    check(lib().sobek_retention_select(plan.handle, graph.handle, budget, ctypes.byref(m), ctypes.byref(nb)))
+    return int(m.value), int(nb.value)
+
+
+def kept_bytes(plan, graph, mask):
+    nb = ctypes.c_size_t()
+    check(lib().sobek_kept_size(plan.handle, graph.handle, mask, ctypes.byref(nb)))
+    return int(nb.value)
+
+
+def new_kept(plan, graph, mask, device=None):
+    """An uninitialised buffer for the kept state of the output groups in `mask` (as 4-byte words)."""
+    return torch.empty(max((kept_bytes(plan, graph, mask) + 3) // 4, 4), dtype=torch.float32,
+                       device=device or graph.rowptr.device)
+
+
+def _check_kept(plan, graph, kept):
+    if kept is not None:
+        mask, buf = kept
+        _check_tensor(buf, "kept", (buf.numel(),))
+        if buf.numel() * 4 < kept_bytes(plan, graph, mask):
+            raise ValueError("kept buffer is smaller than sobek_kept_size")
+
+
+def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=None, keep=None):
+    """m = conv(x, evec, phi, W); with `state` (from new_state) S of every receiver is kept in it; with
+    keep = (mask, buffer from new_kept) the state of the output groups in mask is kept there."""
     N, E = graph.N, graph.E
     _check_tensor(x, "x", (N, plan.dim_in))
     _check_tensor(evec, "evec", (E, 3))
@@ -184,7 +224,11 @@ def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=No
         out = torch.empty(N, plan.dim_out, dtype=torch.float32, device=x.device)
     _check_tensor(out, "out", (N, plan.dim_out))
     ws = _ws(plan, graph, "fwd", ws, budget)
-    if state is None:
+    _check_kept(plan, graph, keep)
+    if keep is not None:
+        check(lib().sobek_conv_fwd_keep(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W),
+                                        _ptr(out), keep[0], _ptr(keep[1]), _ptr(ws), ws.numel(), _stream()))
+    elif state is None:
         check(lib().sobek_conv_fwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(out),
                                    _ptr(ws), ws.numel(), _stream()))
     else:
@@ -220,12 +264,14 @@ def conv_fwd_materialized(plan, graph, x, evec, phi, W, out=None, ws=None, budge
 
 
 def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), ws=None, budget=0, state=None,
-             adj_state=None):
+             adj_state=None, kept=None):
     """(gx, gevec, gphi, gW); entries not in `need` are None.
 
     `state`: the retained receiver state of conv_fwd(..., state=...) with the same x, evec and phi; the
     weight gradient then reads it instead of recomputing S.  `adj_state` (from new_state): receives the
-    adjoint state Sbar = gout A^T of every receiver, for conv_dbwd(..., adj_state=...).
+    adjoint state Sbar = gout A^T of every receiver, for conv_dbwd(..., adj_state=...).  `kept`: the
+    (mask, buffer) of conv_fwd(..., keep=...); the weight gradient reads those groups and recomputes the
+    others one group at a time.
     """
     N, E = graph.N, graph.E
     _check_tensor(x, "x", (N, plan.dim_in))
@@ -239,7 +285,14 @@ def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), 
     _check_state(plan, graph, state)
     _check_state(plan, graph, adj_state)
     ws = _ws(plan, graph, "bwd", ws, budget)
-    if state is None and adj_state is None:
+    _check_kept(plan, graph, kept)
+    if kept is not None:
+        if state is not None or adj_state is not None:
+            raise ValueError("kept groups do not combine with state or adj_state")
+        check(lib().sobek_conv_bwd_kept(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W),
+                                        _ptr(gout), kept[0], _ptr(kept[1]), *[_ptr(o) for o in outs], _ptr(ws),
+                                        ws.numel(), _stream()))
+    elif state is None and adj_state is None:
         check(lib().sobek_conv_bwd(plan.handle, graph.handle, _ptr(x), _ptr(evec), _ptr(phi), _ptr(W), _ptr(gout),
                                    *[_ptr(o) for o in outs], _ptr(ws), ws.numel(), _stream()))
     else:

@@ -62,21 +62,30 @@ def _compile_one(sig):
     return sig
 
 
-def prewarm(signatures, jobs=None):
+def prewarm(signatures, jobs=None, groups=False):
     """JIT-compile kernels for (irreps_in, lmax, irreps_out, K[, layout, norm]) signatures.
 
     Each signature compiles in a process of its own (hipRTC holds one compilation per
     process at a time); the code-object cache publishes every result atomically.
+    groups: also the per-output-group state kernels (the per-group scratch policy).
     """
     import multiprocessing as mp
     jobs = jobs or max(1, min(len(signatures), 4, os.cpu_count() or 1))
-    if jobs == 1:
-        for sig in signatures:
-            _compile_one(sig)
-        return
-    with mp.get_context("spawn").Pool(jobs) as pool:
-        for _ in pool.imap_unordered(_compile_one, signatures):
-            pass
+    old = os.environ.get("SOBEK_JIT_GROUPS")
+    os.environ["SOBEK_JIT_GROUPS"] = "1" if groups else "0"
+    try:
+        if jobs == 1:
+            for sig in signatures:
+                _compile_one(sig)
+            return
+        with mp.get_context("spawn").Pool(jobs) as pool:
+            for _ in pool.imap_unordered(_compile_one, signatures):
+                pass
+    finally:
+        if old is None:
+            del os.environ["SOBEK_JIT_GROUPS"]
+        else:
+            os.environ["SOBEK_JIT_GROUPS"] = old
 
 
 def prune_cache(since):

@@ -516,32 +516,81 @@ int run_state(const Plan& p, const sobek_graph_s& G, const Chunk& c, const WsPla
   return SOBEK_OK;
 }
 
+// S_g (or dS_g) of output group gi for receivers [r0, r0 + n), written at the start of Sg
+// (receiver r0 + il at rows il * d_g ...)
+int group_state(const Plan& p, const sobek_graph_s& G, int gi, int r0, int n, float* Sg, bool tangent,
+                const float* x, const float* evec, const float* phi, const float* xdot, const float* evdot,
+                const float* phidot, int flags, hipStream_t s) {
+  const int NU = p.grp_units[gi];
+  long long ncap = n;
+  hipFunction_t f = p.k.fwd_grp[gi][!tangent ? 0 : (flags == 4 ? 1 : 2)];
+  LAUNCH(f, cdiv((int64_t)n * NU, 4), 1, 1, s, (const int*)G.rowptr, (const int*)G.sender, evec, phi, x, Sg, r0, n,
+         ncap, xdot, evdot, phidot, flags);
+  return SOBEK_OK;
+}
+
+// Receivers per chunk of output group g when its state and output rows share `bytes` of fp32
+// scratch (Appendix B.2, eq. receiver_chunk_budget: B / (4 d_g (D_g + C_g)), at least one, at most N).
+// The state alone, n_g d_g D_g elements of at most 4 bytes, then fits those bytes for any n_g >= 1
+// once one receiver's whole state does.
+int64_t group_chunk(const sobek::Group& g, int64_t N, size_t bytes) {
+  const size_t per = (size_t)4 * g.d * ((size_t)g.D + (size_t)g.C);
+  return std::max<int64_t>(1, std::min<int64_t>(std::max<int64_t>(1, N), (int64_t)(bytes / per)));
+}
+
+// Bytes of the receiver-state slots of a planned pass: what the per-group legs have to themselves
+// (every slot, since the legs that use two slots run after them).
+size_t state_region(const Plan& p, const WsPlan& w) { return (size_t)w.nstate * w.ncap * p.srow * 4; }
+
+// Elements before group gi in a kept state of N receivers holding the groups of `mask`
+// (group blocks in group order, group g's block N d_g D_g elements).
+size_t kept_offset(const Plan& p, int64_t N, uint64_t mask, int gi) {
+  size_t o = 0;
+  for (int h = 0; h < gi && h < 64; ++h)
+    if (mask >> h & 1) o += (size_t)N * p.groups[h].d * p.groups[h].D;
+  return o;
+}
+
+bool kept(uint64_t mask, int gi) { return gi < 64 && (mask >> gi & 1); }
+
+// Whether `mask` keeps every output group (never for a plan with more than 64).
+bool keeps_all(const Plan& p, uint64_t mask) {
+  const size_t G = p.groups.size();
+  return mask && G <= 64 && mask == (G == 64 ? ~(uint64_t)0 : (((uint64_t)1 << G) - 1));
+}
+
+// out(i, m_o, w) (+)= S_g A_g for group g; Sg holds the group's rows of receivers [r0, r0 + n)
+int mix_group(const Plan& p, const sobek::Group& g, int r0, int n, const WsPlan& w, void* ws, const float* Sg,
+              const float* W, float* out, int acc, hipStream_t s) {
+  float* K = (float*)((char*)ws + w.off_K);
+  int nrows = n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out;
+  if (p.mode == SOBEK_MODE_UVU) {
+    LAUNCH(p.k.uvu_mix, cdiv((int64_t)nrows * Cg, 256), 1, 1, s, Sg, nrows, D, Cg, W,
+           (const int*)(p.d_ktab + g.ktab_off), out, dg, off, CX, r0, acc);
+    return SOBEK_OK;
+  }
+  int bn = gemm_bn(g.C);
+  if (p.vec4) {
+    int kper = D;
+    const int ns = sa_nsplit(g, nrows, w.kfloats, kper);
+    LAUNCH(p.k.gemm_sa_v[bn_index(bn)], cdiv(nrows, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, W,
+           (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc, K, kper);
+    if (ns > 1)
+      LAUNCH(p.k.sa_reduce, cdiv((int64_t)nrows * (Cg / 4), 256), 1, 1, s, (const float*)K, ns, nrows, Cg, out, dg,
+             off, CX, r0, acc);
+  } else {
+    LAUNCH(p.k.gemm_sa[bn_index(bn)], cdiv(nrows, 64), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
+           (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
+  }
+  return SOBEK_OK;
+}
+
 // out(i, m_o, w) (+)= S_g A_g for every group
 int run_mix(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float* S, const float* W, float* out,
             int acc, hipStream_t s) {
-  float* K = (float*)((char*)ws + w.off_K);
-  for (auto& g : p.groups) {
-    const float* Sg = state_at(p, S, (size_t)w.ncap * g.s_off);
-    int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
-    if (p.mode == SOBEK_MODE_UVU) {
-      LAUNCH(p.k.uvu_mix, cdiv((int64_t)nrows * Cg, 256), 1, 1, s, Sg, nrows, D, Cg, W,
-             (const int*)(p.d_ktab + g.ktab_off), out, dg, off, CX, r0, acc);
-      continue;
-    }
-    int bn = gemm_bn(g.C);
-    if (p.vec4) {
-      int kper = D;
-      const int ns = sa_nsplit(g, nrows, w.kfloats, kper);
-      LAUNCH(p.k.gemm_sa_v[bn_index(bn)], cdiv(nrows, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, W,
-             (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc, K, kper);
-      if (ns > 1)
-        LAUNCH(p.k.sa_reduce, cdiv((int64_t)nrows * (Cg / 4), 256), 1, 1, s, (const float*)K, ns, nrows, Cg, out, dg,
-               off, CX, r0, acc);
-    } else {
-      LAUNCH(p.k.gemm_sa[bn_index(bn)], cdiv(nrows, 64), cdiv(Cg, bn), 1, s, Sg, nrows, D, W,
-             (const int*)(p.d_ktab + g.ktab_off), out, dg, Cg, off, CX, r0, acc);
-    }
-  }
+  for (auto& g : p.groups)
+    if (int rc = mix_group(p, g, c.r0, c.n, w, ws, state_at(p, S, (size_t)w.ncap * g.s_off), W, out, acc, s))
+      return rc;
   return SOBEK_OK;
 }
 
@@ -572,44 +621,144 @@ int run_sbar(const Plan& p, const Chunk& c, int64_t s_ncap, const float* M, cons
   return SOBEK_OK;
 }
 
-// gW = sum over the pass's chunks of S_g^T mbar_g, deterministic: each chunk adds
-// its rows into fixed split partials (chunk 0 overwrites them), and after the
-// last chunk the splits are summed in fixed order into W's layout
-// S holds the state of receivers [c.r0, c.r0 + c.n) at row 0 of each group block,
-// group blocks s_ncap receivers apart (the chunk slot, or a retained full state).
-int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float* S, int64_t s_ncap, const float* M,
-           float* gW, bool first_chunk, bool last_chunk, hipStream_t s) {
+// Weight-gradient split partials of group gi: a region of nsplit_for(g, ncap d_g) * D_g * C_g
+// floats per group, the groups' regions in group order (ncap = the pass's receiver capacity).
+float* ga_partials(const Plan& p, const WsPlan& w, void* ws, int gi) {
   float* P = (float*)((char*)ws + w.off_P);
-  for (auto& g : p.groups) {
-    const float* Sg = state_at(p, S, (size_t)s_ncap * g.s_off);
-    int nrows = c.n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out, r0 = c.r0;
-    int ns = nsplit_for(g, (int64_t)w.ncap * g.d, p.vec4);
-    int rps = (int)(((int64_t)cdiv(nrows, ns) + 31) / 32 * 32);
-    int bn = gemm_bn(g.C);
-    int acc = first_chunk ? 0 : 1;
-    if (p.mode == SOBEK_MODE_UVU) {
-      // channelwise: one weight per column k of S (P[split][k]); the region holds ns * D * C floats
-      LAUNCH(p.k.uvu_ga, cdiv(D, 256), 1, ns, s, Sg, nrows, D, Cg, M, P, dg, off, CX, r0, rps, acc);
-      if (last_chunk) {
-        int one = 1, ncol = 1;
-        LAUNCH(p.k.ga_reduce, cdiv((int64_t)D, 256), 1, 1, s, (const float*)P, ns, D, ncol,
-               (const int*)(p.d_ktab + g.ktab_off), gW, one);
-      }
-      P += (size_t)ns * g.D * g.C;
-      continue;
-    }
-    if (p.vec4)
-      LAUNCH(p.k.gemm_ga_v[bn_index(bn)], cdiv(D, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
-             rps, acc);
-    else
-      LAUNCH(p.k.gemm_ga[bn_index(bn)], cdiv(D, 64), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
-             rps, acc);
+  for (int h = 0; h < gi; ++h) {
+    const sobek::Group& g = p.groups[h];
+    P += (size_t)nsplit_for(g, (int64_t)w.ncap * g.d, p.vec4) * g.D * g.C;
+  }
+  return P;
+}
+
+// gW += S_g^T mbar_g over the rows of receivers [r0, r0 + n), deterministic: each call adds its
+// rows into fixed split partials (the group's first call overwrites them), and its last call sums
+// the splits in fixed order into W's layout.  The split count follows the pass's receiver
+// capacity, so every call of a group, whatever its receiver count, uses the same partials.
+int ga_group(const Plan& p, int gi, int r0, int n, const WsPlan& w, void* ws, const float* Sg, const float* M,
+             float* gW, bool first_chunk, bool last_chunk, hipStream_t s) {
+  const sobek::Group& g = p.groups[gi];
+  float* P = ga_partials(p, w, ws, gi);
+  int nrows = n * g.d, D = (int)g.D, dg = g.d, Cg = g.C, off = g.off, CX = p.dim_out;
+  int ns = nsplit_for(g, (int64_t)w.ncap * g.d, p.vec4);
+  int rps = (int)(((int64_t)cdiv(nrows, ns) + 31) / 32 * 32);
+  int bn = gemm_bn(g.C);
+  int acc = first_chunk ? 0 : 1;
+  if (p.mode == SOBEK_MODE_UVU) {
+    // channelwise: one weight per column k of S (P[split][k]); the region holds ns * D * C floats
+    LAUNCH(p.k.uvu_ga, cdiv(D, 256), 1, ns, s, Sg, nrows, D, Cg, M, P, dg, off, CX, r0, rps, acc);
     if (last_chunk) {
-      int one = 1;
-      LAUNCH(p.k.ga_reduce, cdiv((int64_t)D * Cg, 256), 1, 1, s, (const float*)P, ns, D, Cg,
+      int one = 1, ncol = 1;
+      LAUNCH(p.k.ga_reduce, cdiv((int64_t)D, 256), 1, 1, s, (const float*)P, ns, D, ncol,
              (const int*)(p.d_ktab + g.ktab_off), gW, one);
     }
-    P += (size_t)ns * g.D * g.C;
+    return SOBEK_OK;
+  }
+  if (p.vec4)
+    LAUNCH(p.k.gemm_ga_v[bn_index(bn)], cdiv(D, 128), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
+           rps, acc);
+  else
+    LAUNCH(p.k.gemm_ga[bn_index(bn)], cdiv(D, 64), cdiv(Cg, bn), ns, s, Sg, nrows, D, M, P, dg, Cg, off, CX, r0,
+           rps, acc);
+  if (last_chunk) {
+    int one = 1;
+    LAUNCH(p.k.ga_reduce, cdiv((int64_t)D * Cg, 256), 1, 1, s, (const float*)P, ns, D, Cg,
+           (const int*)(p.d_ktab + g.ktab_off), gW, one);
+  }
+  return SOBEK_OK;
+}
+
+// gW over every group; S holds the state of receivers [c.r0, c.r0 + c.n) at row 0 of each group
+// block, group blocks s_ncap receivers apart (the chunk slot, or a retained full state).
+int run_ga(const Plan& p, const Chunk& c, const WsPlan& w, void* ws, const float* S, int64_t s_ncap, const float* M,
+           float* gW, bool first_chunk, bool last_chunk, hipStream_t s) {
+  for (int gi = 0; gi < (int)p.groups.size(); ++gi)
+    if (int rc = ga_group(p, gi, c.r0, c.n, w, ws, state_at(p, S, (size_t)s_ncap * p.groups[gi].s_off), M, gW,
+                          first_chunk, last_chunk, s))
+      return rc;
+  return SOBEK_OK;
+}
+
+// out (+)= S A, one output group at a time: kept groups from `keep` (one pass over every
+// receiver, written there by the forward when `write_kept`), the others recomputed in chunks of
+// group_chunk receivers in the state slot.
+int fwd_by_group(const Plan& p, const sobek_graph_s& G, const WsPlan& w, void* ws, uint64_t mask, float* keep,
+                 bool write_kept, const float* x, const float* evec, const float* phi, const float* W, float* out,
+                 hipStream_t s) {
+  int rc;
+  float* slot = state_ptr(w, ws, p, 0);
+  for (int gi = 0; gi < (int)p.groups.size(); ++gi) {
+    const sobek::Group& g = p.groups[gi];
+    if (kept(mask, gi)) {
+      float* Sg = (float*)state_at(p, keep, kept_offset(p, G.N, mask, gi));
+      if (write_kept && (rc = group_state(p, G, gi, 0, (int)G.N, Sg, false, x, evec, phi, nullptr, nullptr, nullptr,
+                                          0, s)))
+        return rc;
+      if ((rc = mix_group(p, g, 0, (int)G.N, w, ws, Sg, W, out, 0, s))) return rc;
+      continue;
+    }
+    const int64_t ng = group_chunk(g, G.N, state_region(p, w));
+    for (int64_t r = 0; r < G.N; r += ng) {
+      const int n = (int)std::min<int64_t>(ng, G.N - r);
+      if ((rc = group_state(p, G, gi, (int)r, n, slot, false, x, evec, phi, nullptr, nullptr, nullptr, 0, s)) ||
+          (rc = mix_group(p, g, (int)r, n, w, ws, slot, W, out, 0, s)))
+        return rc;
+    }
+  }
+  return SOBEK_OK;
+}
+
+// gW = S^T mbar, one output group at a time: kept groups read from `keep` in one pass, the others
+// recomputed in chunks of group_chunk receivers in the state slot.
+int ga_by_group(const Plan& p, const sobek_graph_s& G, const WsPlan& w, void* ws, uint64_t mask, const float* keep,
+                const float* x, const float* evec, const float* phi, const float* M, float* gW, hipStream_t s) {
+  int rc;
+  float* slot = state_ptr(w, ws, p, 0);
+  for (int gi = 0; gi < (int)p.groups.size(); ++gi) {
+    if (kept(mask, gi)) {
+      if ((rc = ga_group(p, gi, 0, (int)G.N, w, ws, state_at(p, keep, kept_offset(p, G.N, mask, gi)), M, gW, true,
+                         true, s)))
+        return rc;
+      continue;
+    }
+    const int64_t ng = group_chunk(p.groups[gi], G.N, state_region(p, w));
+    for (int64_t r = 0; r < G.N; r += ng) {
+      const int n = (int)std::min<int64_t>(ng, G.N - r);
+      if ((rc = group_state(p, G, gi, (int)r, n, slot, false, x, evec, phi, nullptr, nullptr, nullptr, 0, s)) ||
+          (rc = ga_group(p, gi, (int)r, n, w, ws, slot, M, gW, r == 0, r + n >= G.N, s)))
+        return rc;
+    }
+  }
+  return SOBEK_OK;
+}
+
+// The double backward's receiver-state legs, one output group at a time in chunks of group_chunk
+// receivers: dS_g for the output tangent (ggk) and the weight gradient (g_W), then S_g for the
+// output tangent's S dA term (t_gW), in the state slot.
+int dbwd_state_by_group(const Plan& p, const sobek_graph_s& G, const WsPlan& w, void* ws, const float* x,
+                        const float* evec, const float* phi, const float* xdot, const float* evdot,
+                        const float* phidot, int flags, const float* W, const float* t_gW, const float* gk,
+                        float* ggk, float* g_W, hipStream_t s) {
+  int rc;
+  const bool tan = flags & 7;
+  float* slot = state_ptr(w, ws, p, 0);
+  for (int gi = 0; gi < (int)p.groups.size(); ++gi) {
+    const sobek::Group& g = p.groups[gi];
+    const int64_t ng = group_chunk(g, G.N, state_region(p, w));
+    for (int64_t r = 0; r < G.N; r += ng) {
+      const int r0 = (int)r, n = (int)std::min<int64_t>(ng, G.N - r);
+      if (tan && (ggk || g_W)) {
+        if ((rc = group_state(p, G, gi, r0, n, slot, true, x, evec, phi, xdot, evdot, phidot, flags & 7, s))) return rc;
+        if (ggk && (rc = mix_group(p, g, r0, n, w, ws, slot, W, ggk, 0, s))) return rc;
+        if (g_W && (rc = ga_group(p, gi, r0, n, w, ws, slot, gk, g_W, r == 0, r + n >= G.N, s))) return rc;
+      }
+      if (t_gW && ggk) {  // S_g reuses the slot once dS_g has been consumed
+        if ((rc = group_state(p, G, gi, r0, n, slot, false, x, evec, phi, nullptr, nullptr, nullptr, 0, s)) ||
+            (rc = mix_group(p, g, r0, n, w, ws, slot, t_gW, ggk, tan ? 1 : 0, s)))
+          return rc;
+      }
+    }
   }
   return SOBEK_OK;
 }
@@ -831,6 +980,40 @@ int ensure_receiver_route(sobek_plan plan) {
   return SOBEK_OK;
 }
 
+std::mutex g_grp_mu;
+
+// The state kernels of one output group at a time (the per-group scratch policy and group
+// retention), a module of their own compiled and loaded on first use.
+int ensure_groups(sobek_plan plan) {
+  Plan& p = plan->p;
+  std::lock_guard<std::mutex> lk(g_grp_mu);
+  if (p.k.module_grp) return SOBEK_OK;
+  hipModule_t m = nullptr;
+  int rc;
+  if ((rc = load_module(sobek::generate_group_source(p), m))) return rc;
+  std::vector<std::array<hipFunction_t, 3>> fns(p.groups.size());
+  std::vector<int> units;
+  const char* kinds[3] = {"S", "dS_r", "dS"};
+  for (int gi = 0; gi < (int)p.groups.size(); ++gi) {
+    for (int k = 0; k < 3; ++k) {
+      const std::string nm = "sobek_fwdg" + std::to_string(gi) + "_" + kinds[k];
+      if ((rc = get_fn(m, fns[gi][k], nm.c_str()))) {
+        (void)hipModuleUnload(m);
+        return rc;
+      }
+    }
+    units.push_back((int)sobek::pack_fwd_units(p, gi, nullptr).size());
+    if (!units.back()) {
+      (void)hipModuleUnload(m);
+      return fail(SOBEK_E_INTERNAL, "output group %d has no forward units", gi);
+    }
+  }
+  p.grp_units = units;
+  p.k.fwd_grp = fns;
+  p.k.module_grp = m;
+  return SOBEK_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -885,6 +1068,8 @@ int sobek_jit_compile(const sobek_irrep* in, int n_in, int lmax, const sobek_irr
     const char* sf = std::getenv("SOBEK_JIT_STATE_FREE_ONLY");
     if (p.source_u.empty() || !sf || std::strcmp(sf, "1") != 0) sobek::jit_compile(p.source);
     if (materialized_supported(p)) sobek::jit_compile(sobek::generate_materialized_source(p));
+    const char* gs = std::getenv("SOBEK_JIT_GROUPS");
+    if (gs && std::strcmp(gs, "1") == 0) sobek::jit_compile(sobek::generate_group_source(p));
   } catch (const std::exception& ex) {
     return fail(SOBEK_E_COMPILE, "%s", ex.what());
   }
@@ -954,6 +1139,7 @@ int sobek_plan_destroy(sobek_plan plan) {
   if (p.k.module) (void)hipModuleUnload(p.k.module);
   if (p.k.module_u) (void)hipModuleUnload(p.k.module_u);
   if (p.k.module_mat) (void)hipModuleUnload(p.k.module_mat);
+  if (p.k.module_grp) (void)hipModuleUnload(p.k.module_grp);
   delete plan;
   return SOBEK_OK;
 }
@@ -1101,8 +1287,11 @@ namespace {
 
 // Forward; with `state` non-NULL the receiver state of every receiver is
 // computed into it in one pass (and kept), otherwise chunk by chunk in the workspace.
+// With keep_mask non-zero, the state of the output groups in it is computed into `keep` (every
+// receiver, group by group) and the other groups are streamed one group at a time.
 int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
-                  const float* W, float* out, float* state, void* ws, size_t ws_bytes, hipStream_t stream) {
+                  const float* W, float* out, float* state, void* ws, size_t ws_bytes, hipStream_t stream,
+                  uint64_t keep_mask = 0, float* keep = nullptr, bool per_group = false) {
   int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
   if (rc) return rc;
   if (!out && graph->N) return fail(SOBEK_E_INVALID, "out is NULL");
@@ -1110,8 +1299,13 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   const Plan& p = plan->p;
   const sobek_graph_s& G = *graph;
   if (state && !aligned16(state)) return fail(SOBEK_E_ALIGN, "state is not 16-byte aligned");
+  // the channelwise single-multiplicity forward keeps no receiver state unless asked to
+  const bool state_free = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && !state && !keep_mask;
+  const bool by_group = !state && !state_free && (per_group || keep_mask || p.policy == SOBEK_POLICY_PER_GROUP);
   WsPlan w;
-  if ((rc = plan_workspace(p, G, SOBEK_PASS_FWD, ws_bytes, w, false, state ? 0 : -1))) return rc;
+  if ((rc = plan_workspace(p, G, SOBEK_PASS_FWD, ws_bytes, w, false,
+                           state || keeps_all(p, keep_mask) ? 0 : (by_group ? 1 : -1))))
+    return rc;
   if (G.N == 0) return SOBEK_OK;
   const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
   const float* xk = x;
@@ -1121,8 +1315,16 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
     ok = (float*)((char*)ws + w.off_out);
     if ((rc = transpose(p, x, (float*)xk, G.N, true, 0, stream))) return rc;
   }
-  if (!(p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && !state) && (rc = ensure_receiver_route(plan))) return rc;
-  if (p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && !state) {
+  if (!state_free && (rc = ensure_receiver_route(plan))) return rc;
+  if (by_group) {
+    if ((rc = ensure_groups(plan)) ||
+        (rc = fwd_by_group(p, G, w, ws, keep_mask, keep, true, xk, evec, phi, W, ok, stream)) ||
+        (rc = zero_dead_out(p, ok, G.N, stream)))
+      return rc;
+    if (mulir && (rc = transpose(p, ok, out, G.N, false, 1, stream))) return rc;
+    return SOBEK_OK;
+  }
+  if (state_free) {
     // channelwise, one multiplicity: every receiver at once, no receiver state
     int r0 = 0, n = (int)G.N;
     LAUNCH(p.k.uvu_fwd, cdiv(G.N, 4), cdiv(p.uvu_C, 64), 1, stream, (const int*)G.rowptr, (const int*)G.sender, evec,
@@ -1146,9 +1348,12 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
 // With `adj_state` non-NULL the adjoint state Sbar = mbar A^T of every receiver is
 // computed into it in one pass (and kept for a double backward); the edge kernel
 // then reads each chunk's rows from it.
+// With keep_mask non-zero the weight gradient reads the state of those output groups from `keep`
+// (as sobek_conv_fwd_keep left it) and recomputes the others one group at a time.
 int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
                   const float* W, const float* gout, const float* state, float* adj_state, float* gx, float* gevec,
-                  float* gphi, float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
+                  float* gphi, float* gW, void* ws, size_t ws_bytes, hipStream_t stream, uint64_t keep_mask = 0,
+                  const float* keep = nullptr) {
   int rc = check_common(plan, graph, x, evec, phi, W, ws, ws_bytes);
   if (rc) return rc;
   if (!gout && graph->N) return fail(SOBEK_E_INVALID, "gout is NULL");
@@ -1163,7 +1368,10 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   const bool uvu_direct = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct;
   // with it, A_bar comes from the edges directly (no receiver state; a kept S is not needed)
   const bool uvu_wg = uvu_direct && p.uvu_wgrad_direct;
-  const bool need_slot = (gW && !state && !uvu_wg) || (!uvu_direct && !adj_state && (gx || gevec || gphi));
+  // the weight gradient one output group at a time: kept groups, or the per-group policy
+  const bool ga_groups = gW && !state && !uvu_wg && (keep_mask || p.policy == SOBEK_POLICY_PER_GROUP);
+  const bool ga_recompute = gW && !state && !uvu_wg && !keeps_all(p, keep_mask);
+  const bool need_slot = ga_recompute || (!uvu_direct && !adj_state && (gx || gevec || gphi));
   if ((!uvu_direct || (gW && !uvu_wg)) && (rc = ensure_receiver_route(plan))) return rc;
   if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false, need_slot ? 1 : 0))) return rc;
   if (gW) { if ((rc = fill_zero(p, gW, (int64_t)p.K * p.n_w, stream))) return rc; }
@@ -1199,11 +1407,14 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
            evec, phi, xk, gk, P, n, (const float*)nullptr, rows);
     LAUNCH(p.k.uvu_wreduce, cdiv(nw, 256), 1, 1, stream, (const float*)P, rows, nw, gW);
   }
+  if (ga_groups && ((rc = ensure_groups(plan)) ||
+                    (rc = ga_by_group(p, G, w, ws, keep_mask, keep, xk, evec, phi, gk, gW, stream))))
+    return rc;
   if (adj_state && (rc = run_sbar(p, all, G.N, gk, W, adj_state, stream))) return rc;
   bool first_win = true;  // the first edge window overall initialises the sender cursors and x-gradient rows
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
-    if (gW && !state && !uvu_wg) {
+    if (gW && !state && !uvu_wg && !ga_groups) {
       if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
       if ((rc = run_ga(p, c, w, ws, S, w.ncap, gk, gW, ci == 0, ci + 1 == w.chunks.size(), stream))) return rc;
     }
@@ -1267,6 +1478,100 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
                    size_t ws_bytes, hipStream_t stream) {
   return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, nullptr, nullptr, gx, gevec, gphi, gW, ws, ws_bytes,
                        stream);
+}
+
+int sobek_plan_set_policy(sobek_plan plan, int policy) {
+  if (!plan) return fail(SOBEK_E_INVALID, "NULL plan");
+  if (policy != SOBEK_POLICY_ALL_GROUPS && policy != SOBEK_POLICY_PER_GROUP)
+    return fail(SOBEK_E_INVALID, "unknown scratch policy %d", policy);
+  plan->p.policy = policy;
+  return SOBEK_OK;
+}
+
+int sobek_kept_size(sobek_plan plan, sobek_graph graph, uint64_t group_mask, size_t* bytes) {
+  if (!plan || !graph || !bytes) return fail(SOBEK_E_INVALID, "NULL argument");
+  const Plan& p = plan->p;
+  if (p.groups.size() < 64 && (group_mask >> p.groups.size()))
+    return fail(SOBEK_E_INVALID, "group mask has bits past the plan's %zu output groups", p.groups.size());
+  *bytes = kept_offset(p, graph->N, group_mask, (int)p.groups.size()) * state_elem(p);
+  return SOBEK_OK;
+}
+
+int sobek_retention_select(sobek_plan plan, sobek_graph graph, size_t budget, uint64_t* group_mask, size_t* bytes) {
+  if (!plan || !graph || !group_mask || !bytes) return fail(SOBEK_E_INVALID, "NULL argument");
+  const Plan& p = plan->p;
+  const size_t B = budget ? budget : default_budget();
+  const int G = (int)std::min<size_t>(64, p.groups.size());
+  std::vector<size_t> cost(G);
+  std::vector<double> work(G, 0.0);
+  for (int g = 0; g < G; ++g) {
+    cost[g] = (size_t)graph->N * p.groups[g].d * p.groups[g].D * state_elem(p);
+    for (int t : p.groups[g].paths) {
+      size_t nz = 0;
+      for (double c : p.paths[t].cg) nz += c != 0.0;
+      work[g] += (double)nz * p.paths[t].c_in;
+    }
+  }
+  uint64_t best = 0;
+  const bool free_wgrad = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && p.uvu_bwd_direct && p.uvu_wgrad_direct;
+  if (free_wgrad) {
+    best = 0;
+  } else if (p.mode == SOBEK_MODE_UVU) {
+    size_t all = 0;
+    for (int g = 0; g < G; ++g) all += cost[g];
+    if (G == (int)p.groups.size() && all <= B) best = G == 64 ? ~(uint64_t)0 : (((uint64_t)1 << G) - 1);
+  } else if (G <= 20) {
+    double bw = 0.0;
+    size_t bb = 0;
+    for (uint64_t m = 1; m < ((uint64_t)1 << G); ++m) {
+      double v = 0.0;
+      size_t b = 0;
+      for (int g = 0; g < G; ++g)
+        if (m >> g & 1) { v += work[g]; b += cost[g]; }
+      if (b > B) continue;
+      if (v > bw || (v == bw && b < bb)) { best = m; bw = v; bb = b; }
+    }
+  } else {
+    std::vector<int> order(G);
+    for (int g = 0; g < G; ++g) order[g] = g;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+      return work[a] * (double)cost[b] > work[b] * (double)cost[a];
+    });
+    size_t used = 0;
+    for (int g : order)
+      if (used + cost[g] <= B) { best |= (uint64_t)1 << g; used += cost[g]; }
+  }
+  *group_mask = best;
+  *bytes = kept_offset(p, graph->N, best, (int)p.groups.size()) * state_elem(p);
+  return SOBEK_OK;
+}
+
+int sobek_conv_fwd_keep(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                        const float* W, float* out, uint64_t group_mask, float* kept, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+  if (!plan || !graph) return fail(SOBEK_E_INVALID, "NULL plan or graph");
+  size_t kb = 0;
+  if (int rc = sobek_kept_size(plan, graph, group_mask, &kb)) return rc;
+  if (group_mask && graph->N && !kept) return fail(SOBEK_E_INVALID, "kept is NULL");
+  if (kept && !aligned16(kept)) return fail(SOBEK_E_ALIGN, "kept is not 16-byte aligned");
+  if (plan->p.mode == SOBEK_MODE_UVU && group_mask && !keeps_all(plan->p, group_mask))
+    return fail(SOBEK_E_INVALID, "a channelwise plan keeps every output group or none");
+  return conv_fwd_impl(plan, graph, x, evec, phi, W, out, nullptr, ws, ws_bytes, stream, group_mask, kept, true);
+}
+
+int sobek_conv_bwd_kept(sobek_plan plan, sobek_graph graph, const float* x, const float* evec, const float* phi,
+                        const float* W, const float* gout, uint64_t group_mask, const float* kept, float* gx,
+                        float* gevec, float* gphi, float* gW, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!plan || !graph) return fail(SOBEK_E_INVALID, "NULL plan or graph");
+  size_t kb = 0;
+  if (int rc = sobek_kept_size(plan, graph, group_mask, &kb)) return rc;
+  if (group_mask && graph->N && gW && !kept) return fail(SOBEK_E_INVALID, "kept is NULL");
+  if (kept && !aligned16(kept)) return fail(SOBEK_E_ALIGN, "kept is not 16-byte aligned");
+  if (plan->p.mode == SOBEK_MODE_UVU && group_mask && !keeps_all(plan->p, group_mask))
+    return fail(SOBEK_E_INVALID, "a channelwise plan keeps every output group or none");
+  if (!gW) group_mask = 0;
+  return conv_bwd_impl(plan, graph, x, evec, phi, W, gout, nullptr, nullptr, gx, gevec, gphi, gW, ws, ws_bytes,
+                       stream, group_mask, group_mask ? kept : nullptr);
 }
 
 int sobek_materialized_workspace_size(sobek_plan plan, sobek_graph graph, size_t budget, size_t* bytes) {
@@ -1430,16 +1735,23 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
   float* Sb2 = state_ptr(w, ws, p, 1);
   float* contrib = g_x ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = g_x || g_evec || g_phi;
+  // the state legs one output group at a time (per-group policy), then the edge legs by receiver chunk
+  const bool by_group = p.policy == SOBEK_POLICY_PER_GROUP;
+  if (by_group && ((tan && (g_gout || g_W)) || (t_gW && g_gout)) &&
+      ((rc = ensure_groups(plan)) ||
+       (rc = dbwd_state_by_group(p, G, w, ws, xk, evec, phi, txk, t_gevec, t_gphi, flags, W, t_gW, gk,
+                                 g_gout ? ggk : nullptr, g_W, stream))))
+    return rc;
   bool first_win = true;  // the first edge window overall initialises the sender cursors and x-gradient rows
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
-    if (tan && (g_gout || g_W)) {
+    if (tan && (g_gout || g_W) && !by_group) {
       if ((rc = run_state(p, G, c, w, dS, true, xk, evec, phi, txk, t_gevec, t_gphi, flags & 7, stream))) return rc;
       if (g_gout && (rc = run_mix(p, c, w, ws, dS, W, ggk, 0, stream))) return rc;
       if (g_W && (rc = run_ga(p, c, w, ws, dS, w.ncap, gk, g_W, ci == 0, ci + 1 == w.chunks.size(), stream)))
         return rc;
     }
-    if (t_gW && g_gout) {  // S reuses the slot once dS has been consumed
+    if (t_gW && g_gout && !by_group) {  // S reuses the slot once dS has been consumed
       if ((rc = run_state(p, G, c, w, S, false, xk, evec, phi, nullptr, nullptr, nullptr, 0, stream))) return rc;
       if ((rc = run_mix(p, c, w, ws, S, t_gW, ggk, tan ? 1 : 0, stream))) return rc;
     }

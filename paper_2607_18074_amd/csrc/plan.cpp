@@ -42,6 +42,38 @@ std::vector<std::array<int, 3>> channel_blocks(int C) {
 }
 }  // namespace
 
+// Forward wave units: per input irrep and channel block, the paths (all of them, or those into
+// output group `group` only) packed while K * sum(d_out) accumulators fit the register budget.
+std::vector<Unit> pack_fwd_units(const Plan& p, int group, std::vector<int>* dead_in) {
+  std::vector<Unit> units;
+  for (int a = 0; a < (int)p.in.size(); ++a) {
+    std::vector<int> ps;
+    for (int t = 0; t < (int)p.paths.size(); ++t)
+      if (p.paths[t].i_in == a && (group < 0 || p.paths[t].group == group)) ps.push_back(t);
+    if (ps.empty()) {
+      if (dead_in) dead_in->push_back(a);
+      continue;
+    }
+    for (auto blk : channel_blocks(p.in[a].mul)) {
+      Unit cur;
+      cur.a = a; cur.U = blk[0]; cur.U0 = blk[1]; cur.ES = blk[2];
+      int acc = 0;
+      for (int t : ps) {
+        int need = p.K * (2 * p.paths[t].l_out + 1);
+        if (!cur.paths.empty() && acc + need > kAccMax) {
+          units.push_back(cur);
+          cur.paths.clear();
+          acc = 0;
+        }
+        cur.paths.push_back(t);
+        acc += need;
+      }
+      units.push_back(cur);
+    }
+  }
+  return units;
+}
+
 void build_plan(Plan& p) {
   int off = 0;
   for (auto& r : p.in) { r.off = off; off += r.dim(); }
@@ -137,29 +169,7 @@ void build_plan(Plan& p) {
 
   // forward wave units: per input irrep and channel block, paths packed while
   // K * sum(d_out) accumulators fit the register budget
-  p.fwd_units.clear();
-  for (int a = 0; a < (int)p.in.size(); ++a) {
-    std::vector<int> ps;
-    for (int t = 0; t < (int)p.paths.size(); ++t)
-      if (p.paths[t].i_in == a) ps.push_back(t);
-    if (ps.empty()) { p.dead_in.push_back(a); continue; }
-    for (auto blk : channel_blocks(p.in[a].mul)) {
-      Unit cur;
-      cur.a = a; cur.U = blk[0]; cur.U0 = blk[1]; cur.ES = blk[2];
-      int acc = 0;
-      for (int t : ps) {
-        int need = p.K * (2 * p.paths[t].l_out + 1);
-        if (!cur.paths.empty() && acc + need > kAccMax) {
-          p.fwd_units.push_back(cur);
-          cur.paths.clear();
-          acc = 0;
-        }
-        cur.paths.push_back(t);
-        acc += need;
-      }
-      p.fwd_units.push_back(cur);
-    }
-  }
+  p.fwd_units = pack_fwd_units(p, -1, &p.dead_in);
 
   // adjoint tiles: 16 channels per item, radial index padded to a multiple of 4
   p.adj_U = 16;
@@ -416,7 +426,7 @@ int unit_lsh(const Plan& P, const Unit& u) {
 // one iteration is computed, the loads of the next two are in flight.  The
 // receiver's sender ids are held 64 at a time in one register per lane, the
 // next block already loaded, and handed to the lanes of an edge by a shuffle.
-void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) {
+void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id, bool group_only = false) {
   const Irrep& ri = P.in[u.a];
   const char* st = P.dtype == 1 ? "__bf16" : "float";  // the state's storage type (bf16 for bf16-GEMM plans)
   const int DA = 2 * ri.l + 1, L = unit_lsh(P, u), NS = (L + 1) * (L + 1);
@@ -560,7 +570,7 @@ void emit_fwd_unit(std::ostringstream& o, const Plan& P, const Unit& u, int id) 
     const Path& q = P.paths[t];
     const Group& g = P.groups[q.group];
     const int DO = 2 * q.l_out + 1;
-    o << "    {\n      constexpr int DO = " << DO << ";\n      " << st << "* Sg = S + ncap * " << g.s_off
+    o << "    {\n      constexpr int DO = " << DO << ";\n      " << st << "* Sg = S + ncap * " << (group_only ? 0 : g.s_off)
       << "LL + (sb_i64)il * " << (int64_t)g.d * g.D << "LL + " << q.koff << ";\n";
     if (mf) {
       o << "      const int ub = U0 + 4 * ((lane % U) >> 2), j = lane & 3;\n"
@@ -1484,6 +1494,50 @@ std::string generate_materialized_source(const Plan& P) {
        "  for (int e = beg; e < end; ++e) s += Mm[(e - e0) * CXO + c];\n"
        "  out[(sb_i64)(r0 + i) * CXO + c] = s;\n"
        "}\n";
+  return o.str();
+}
+
+// State kernels of one output group at a time (the per-group scratch policy, Appendix B.2 eq.
+// receiver_chunk_budget): for every output group g, the forward units of g's paths alone and
+// sobek_fwdg<g>_{S,dS_r,dS}, the same kernels as sobek_fwd_* restricted to g, writing S_g at the
+// start of S (receiver il at il * d_g * D_g).  A module of its own, compiled on first use, so that
+// the plan's main source does not change.
+std::string generate_group_source(const Plan& P) {
+  std::ostringstream o;
+  o.precision(17);
+  o << "\n// ---- per-group state kernels, K=" << P.K << " lmax=" << P.lmax << "\n";
+  o << "#define K " << P.K << "\n#define NSH " << P.nsh << "\n#define CXI " << P.dim_in << "\n#define CXO " << P.dim_out
+    << "\n#define EB " << P.bwd_eb << "\n#define KP " << P.adj_KP << "\n#define ADJ_W " << P.adj_waves << "\n";
+  emit_sh(o, P.lmax);
+  for (int t = 0; t < (int)P.paths.size(); ++t) emit_path(o, P, t);
+  const char* st = P.dtype == 1 ? "__bf16" : "float";
+  struct FV { const char* name; bool tan; int fl; };
+  const FV fvs[] = {{"S", false, 0}, {"dS_r", true, 4}, {"dS", true, -1}};
+  int id = 0;
+  for (int gi = 0; gi < (int)P.groups.size(); ++gi) {
+    const std::vector<Unit> units = pack_fwd_units(P, gi, nullptr);
+    const int id0 = id;
+    for (const Unit& u : units) emit_fwd_unit(o, P, u, id++, true);
+    const int NU = (int)units.size();
+    for (const FV& fv : fvs) {
+      o << "extern \"C\" __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void sobek_fwdg" << gi
+        << "_" << fv.name
+        << "(const int* __restrict__ rowptr, const int* __restrict__ sender, const float* __restrict__ evec,"
+           " const float* __restrict__ phi, const float* __restrict__ x, " << st << "* __restrict__ S, int r0, int n_recv,"
+           " sb_i64 ncap, const float* __restrict__ xdot, const float* __restrict__ evdot,"
+           " const float* __restrict__ phidot, int flags) {\n"
+        << "  __shared__ int sids[4][256];\n"
+        << "  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;\n"
+        << "  const int il = gw / " << NU << ", t = gw % " << NU << ";\n"
+        << "  if (il >= n_recv) return;\n"
+           "  const int beg = rowptr[r0 + il], end = rowptr[r0 + il + 1];\n"
+           "  switch (t) {\n";
+      for (int t = 0; t < NU; ++t)
+        o << "    case " << t << ": sb_fwd_u" << id0 + t << "<" << (fv.tan ? "true" : "false") << ", " << fv.fl
+          << ">(lane, il, beg, end, sender, evec, phi, x, S, ncap, xdot, evdot, phidot, flags, sids[threadIdx.x >> 6]); break;\n";
+      o << "  }\n}\n";
+    }
+  }
   return o.str();
 }
 

@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <array>
 #include <cstdint>
 #include <map>
 #include <string>
@@ -84,6 +85,8 @@ inline int uvu_wgrad_waves(int K, int64_t n_w) {
 struct Kernels {
   hipModule_t module = nullptr;    // every kernel of the plan (for channelwise plans with the
                                    // state-free kernels: the receiver-route kernels, loaded on first use)
+  hipModule_t module_grp = nullptr;  // per-output-group state kernels (compiled on first use)
+  std::vector<std::array<hipFunction_t, 3>> fwd_grp;  // per group: S, dS_r, dS
   hipModule_t module_mat = nullptr;  // the materialized-forward baseline (compiled on first use)
   hipFunction_t mat_w = nullptr, mat_msg = nullptr, mat_reduce = nullptr;
   hipModule_t module_u = nullptr;  // channelwise plans: the state-free kernels and the common ones
@@ -104,6 +107,8 @@ struct Plan {
   std::vector<Irrep> in, out;
   int lmax = 0, K = 0, layout = 0, dtype = 0, norm = 0;
   int mode = 0;                 // 0: uvw (fully connected mixing), 1: uvu (channelwise)
+  int policy = 0;               // scratch policy: 0 all groups per receiver chunk, 1 one output group at a time
+  std::vector<int> grp_units;   // forward wave units of each output group's own state kernels
   int dim_in = 0, dim_out = 0, nsh = 0;
   int64_t n_w = 0;
   std::vector<Path> paths;
@@ -144,5 +149,9 @@ void build_plan(Plan& p);
 std::string generate_source(const Plan& p, bool receiver_route = true);
 // Source of the materialized-forward baseline module (Section 2.4, eq. radial_projection_background).
 std::string generate_materialized_source(const Plan& p);
+// Source of the per-output-group state kernels (Appendix B.2, eq. receiver_chunk_budget).
+std::string generate_group_source(const Plan& p);
+// Forward wave units over every path (group < 0) or over the paths into one output group.
+std::vector<Unit> pack_fwd_units(const Plan& p, int group, std::vector<int>* dead_in);
 
 }  // namespace sobek

@@ -98,15 +98,36 @@ def _p(d):
 
 class Plan:
     def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw",
-                 dtype="f32"):
+                 dtype="f32", policy="all"):
         args = _lib._sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode, dtype)
         h = ctypes.c_void_p()
         check(lib().sobek_plan_create(*args, ctypes.byref(h)))
         self.handle = h
         self.K = int(K)
+        self.irreps_in = _lib.parse_irreps(irreps_in)
+        self.irreps_out = _lib.parse_irreps(irreps_out)
         vals = [ctypes.c_int64() for _ in range(5)]
         check(lib().sobek_plan_info(h, *[ctypes.byref(v) for v in vals]))
         self.n_paths, self.n_weights, self.dim_in, self.dim_out, self.dim_sh = (v.value for v in vals)
+        self.set_policy(policy)
+
+    def set_policy(self, policy):
+        check(lib().sobek_plan_set_policy(self.handle, {"all": 0, "groups": 1}[policy]))
+        self.policy = policy
+
+    def paths(self):
+        n = self.n_paths
+        a, b, c = ((ctypes.c_int32 * n)() for _ in range(3))
+        w = (ctypes.c_int64 * n)()
+        check(lib().sobek_plan_paths(self.handle, a, b, c, w))
+        return [(a[t], b[t], c[t], w[t]) for t in range(n)]
+
+    def cg(self, path):
+        i_in, i_sh, i_out, _ = self.paths()[path]
+        li, ls, lo = self.irreps_in[i_in][1], i_sh, self.irreps_out[i_out][1]
+        buf = (ctypes.c_double * ((2 * li + 1) * (2 * ls + 1) * (2 * lo + 1)))()
+        check(lib().sobek_plan_cg(self.handle, path, buf))
+        return np.array(buf).reshape(2 * li + 1, 2 * ls + 1, 2 * lo + 1)
 
 
 class Graph:
@@ -151,11 +172,30 @@ def _ws(plan, graph, p, ws, budget):
     return graph.workspace(plan, p, budget) if ws is None else ws
 
 
-def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=None):
+def retention(plan, graph, budget=0):
+    m, nb = ctypes.c_uint64(), ctypes.c_size_t()
+    check(lib().sobek_retention_select(plan.handle, graph.handle, budget, ctypes.byref(m), ctypes.byref(nb)))
+    return int(m.value), int(nb.value)
+
+
+def kept_bytes(plan, graph, mask):
+    nb = ctypes.c_size_t()
+    check(lib().sobek_kept_size(plan.handle, graph.handle, mask, ctypes.byref(nb)))
+    return int(nb.value)
+
+
+def new_kept(plan, graph, mask, device=None):
+    return Dev(max((kept_bytes(plan, graph, mask) + 3) // 4, 4), np.float32, "kept")
+
+
+def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=None, keep=None):
     out = Dev((graph.N, plan.dim_out), np.float32, "out") if out is None else out
     ws = _ws(plan, graph, "fwd", ws, budget)
     L = lib()
-    if state is None:
+    if keep is not None:
+        check(L.sobek_conv_fwd_keep(plan.handle, graph.handle, _p(x), _p(evec), _p(phi), _p(W), _p(out), keep[0],
+                                    _p(keep[1]), _p(ws), ws.nbytes, None))
+    elif state is None:
         check(L.sobek_conv_fwd(plan.handle, graph.handle, _p(x), _p(evec), _p(phi), _p(W), _p(out), _p(ws),
                                ws.nbytes, None))
     else:
@@ -165,13 +205,16 @@ def conv_fwd(plan, graph, x, evec, phi, W, out=None, ws=None, budget=0, state=No
 
 
 def conv_bwd(plan, graph, x, evec, phi, W, gout, need=(True, True, True, True), ws=None, budget=0, state=None,
-             adj_state=None):
+             adj_state=None, kept=None):
     N, E = graph.N, graph.E
     shapes = [(N, plan.dim_in), (E, 3), (E, plan.K), (plan.K, plan.n_weights)]
     outs = [Dev(s, np.float32, nm) if n else None for s, n, nm in zip(shapes, need, ("gx", "gevec", "gphi", "gW"))]
     ws = _ws(plan, graph, "bwd", ws, budget)
     L = lib()
-    if state is None and adj_state is None:
+    if kept is not None:
+        check(L.sobek_conv_bwd_kept(plan.handle, graph.handle, _p(x), _p(evec), _p(phi), _p(W), _p(gout), kept[0],
+                                    _p(kept[1]), *[_p(o) for o in outs], _p(ws), ws.nbytes, None))
+    elif state is None and adj_state is None:
         check(L.sobek_conv_bwd(plan.handle, graph.handle, _p(x), _p(evec), _p(phi), _p(W), _p(gout),
                                *[_p(o) for o in outs], _p(ws), ws.nbytes, None))
     else:
