@@ -78,7 +78,7 @@ enum { SOBEK_LAYOUT_IR_MUL = 0, SOBEK_LAYOUT_MUL_IR = 1 };
 enum { SOBEK_DTYPE_F32 = 0, SOBEK_DTYPE_BF16_GEMM = 1 };
 enum { SOBEK_NORM_NONE = 0, SOBEK_NORM_FAN_IN = 1 };
 enum { SOBEK_MODE_UVW = 0, SOBEK_MODE_UVU = 1 };
-enum { SOBEK_POLICY_ALL_GROUPS = 0, SOBEK_POLICY_PER_GROUP = 1 };
+enum { SOBEK_POLICY_ALL_GROUPS = 0, SOBEK_POLICY_PER_GROUP = 1, SOBEK_POLICY_AUTO = 2 };
 enum { SOBEK_PASS_FWD = 0, SOBEK_PASS_BWD = 1, SOBEK_PASS_DBWD = 2 };
 
 /* One irreducible representation: multiplicity, order l >= 0, parity +1 ('e') or -1 ('o'). */
@@ -232,8 +232,11 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float *x, const flo
 int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t *bytes);
 
 /* Scratch policy of a plan's receiver-state legs (Appendix B.2, eq. receiver_chunk_budget).
- * SOBEK_POLICY_ALL_GROUPS (the default): each receiver chunk builds the state of every output
- * group, in chunks sized by the workspace planner.  SOBEK_POLICY_PER_GROUP: the forward, the
+ * SOBEK_POLICY_ALL_GROUPS: each receiver chunk builds the state of every output group, in chunks
+ * sized by the workspace planner.  SOBEK_POLICY_AUTO (the default): per pass, the per-group route
+ * below when the all-group plan of the pass needs three or more receiver chunks (Appendix B.2 takes
+ * a chunked route only when it gives at least three chunks), else all groups.
+ * SOBEK_POLICY_PER_GROUP: the forward, the
  * backward's weight gradient and the double backward's state legs (dS and S) take one output
  * group g at a time, in chunks of n_g = min(N, max(1, floor(B / (4 d_g (D_g + C_g))))) receivers,
  * with B the bytes of the pass workspace's receiver-state region (d_g = 2l+1, D_g the group's

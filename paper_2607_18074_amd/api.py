@@ -39,7 +39,7 @@ def _check_tensor(t, name, shape, dtype=torch.float32):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
-POLICIES = {"all": 0, "groups": 1}
+POLICIES = {"all": 0, "groups": 1, "auto": 2}
 
 
 class Plan:
@@ -47,10 +47,11 @@ class Plan:
     connected, "uvu" channelwise), dtype ("f32", or "bf16_gemm": the channel GEMMs with the receiver
     state, m = S A and A_bar = S^T mbar, on bf16 MFMA with fp32 accumulation; tensors stay fp32), and
     scratch policy ("all": every output group per receiver chunk; "groups": the receiver-state legs one
-    output group at a time in chunks of n_g receivers, eq. receiver_chunk_budget)."""
+    output group at a time in chunks of n_g receivers, eq. receiver_chunk_budget; "auto", the default:
+    "groups" for a pass whose all-group plan needs three or more receiver chunks)."""
 
     def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw",
-                 dtype="f32", policy="all"):
+                 dtype="f32", policy="auto"):
         self.irreps_in = _lib.parse_irreps(irreps_in)
         self.irreps_out = _lib.parse_irreps(irreps_out)
         self.lmax, self.K, self.layout, self.normalization = int(lmax), int(K), layout, normalization
@@ -62,7 +63,7 @@ class Plan:
         vals = [ctypes.c_int64() for _ in range(5)]
         check(lib().sobek_plan_info(h, *[ctypes.byref(v) for v in vals]))
         self.n_paths, self.n_weights, self.dim_in, self.dim_out, self.dim_sh = (v.value for v in vals)
-        self.policy = "all"
+        self.policy = "auto"
         self.set_policy(policy)
 
     def set_policy(self, policy):

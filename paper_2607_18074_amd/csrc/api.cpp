@@ -553,6 +553,12 @@ size_t kept_offset(const Plan& p, int64_t N, uint64_t mask, int gi) {
 
 bool kept(uint64_t mask, int gi) { return gi < 64 && (mask >> gi & 1); }
 
+// SOBEK_POLICY_AUTO: the per-group route when the all-group plan of a pass needs at least three
+// receiver chunks (Appendix B.2 takes a chunked route only when it gives at least three chunks).
+bool group_route_pays(const Plan& p, const WsPlan& w) {
+  return p.policy == SOBEK_POLICY_AUTO && w.chunks.size() >= 3;
+}
+
 // Whether `mask` keeps every output group (never for a plan with more than 64).
 bool keeps_all(const Plan& p, uint64_t mask) {
   const size_t G = p.groups.size();
@@ -1301,11 +1307,12 @@ int conv_fwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   if (state && !aligned16(state)) return fail(SOBEK_E_ALIGN, "state is not 16-byte aligned");
   // the channelwise single-multiplicity forward keeps no receiver state unless asked to
   const bool state_free = p.mode == SOBEK_MODE_UVU && p.uvu_C > 0 && !state && !keep_mask;
-  const bool by_group = !state && !state_free && (per_group || keep_mask || p.policy == SOBEK_POLICY_PER_GROUP);
+  const bool groups_asked = per_group || keep_mask || p.policy == SOBEK_POLICY_PER_GROUP;
   WsPlan w;
   if ((rc = plan_workspace(p, G, SOBEK_PASS_FWD, ws_bytes, w, false,
-                           state || keeps_all(p, keep_mask) ? 0 : (by_group ? 1 : -1))))
+                           state || keeps_all(p, keep_mask) ? 0 : (groups_asked && !state_free ? 1 : -1))))
     return rc;
+  const bool by_group = !state && !state_free && (groups_asked || group_route_pays(p, w));
   if (G.N == 0) return SOBEK_OK;
   const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
   const float* xk = x;
@@ -1369,11 +1376,12 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   // with it, A_bar comes from the edges directly (no receiver state; a kept S is not needed)
   const bool uvu_wg = uvu_direct && p.uvu_wgrad_direct;
   // the weight gradient one output group at a time: kept groups, or the per-group policy
-  const bool ga_groups = gW && !state && !uvu_wg && (keep_mask || p.policy == SOBEK_POLICY_PER_GROUP);
+  bool ga_groups = gW && !state && !uvu_wg && (keep_mask || p.policy == SOBEK_POLICY_PER_GROUP);
   const bool ga_recompute = gW && !state && !uvu_wg && !keeps_all(p, keep_mask);
   const bool need_slot = ga_recompute || (!uvu_direct && !adj_state && (gx || gevec || gphi));
   if ((!uvu_direct || (gW && !uvu_wg)) && (rc = ensure_receiver_route(plan))) return rc;
   if ((rc = plan_workspace(p, G, SOBEK_PASS_BWD, ws_bytes, w, false, need_slot ? 1 : 0))) return rc;
+  if (gW && !state && !uvu_wg && group_route_pays(p, w)) ga_groups = true;
   if (gW) { if ((rc = fill_zero(p, gW, (int64_t)p.K * p.n_w, stream))) return rc; }
   if (G.N == 0) return SOBEK_OK;
   const bool mulir = p.layout == SOBEK_LAYOUT_MUL_IR;
@@ -1482,7 +1490,7 @@ int sobek_conv_bwd(sobek_plan plan, sobek_graph graph, const float* x, const flo
 
 int sobek_plan_set_policy(sobek_plan plan, int policy) {
   if (!plan) return fail(SOBEK_E_INVALID, "NULL plan");
-  if (policy != SOBEK_POLICY_ALL_GROUPS && policy != SOBEK_POLICY_PER_GROUP)
+  if (policy != SOBEK_POLICY_ALL_GROUPS && policy != SOBEK_POLICY_PER_GROUP && policy != SOBEK_POLICY_AUTO)
     return fail(SOBEK_E_INVALID, "unknown scratch policy %d", policy);
   plan->p.policy = policy;
   return SOBEK_OK;
@@ -1736,7 +1744,7 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
   float* contrib = g_x ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = g_x || g_evec || g_phi;
   // the state legs one output group at a time (per-group policy), then the edge legs by receiver chunk
-  const bool by_group = p.policy == SOBEK_POLICY_PER_GROUP;
+  const bool by_group = p.policy == SOBEK_POLICY_PER_GROUP || group_route_pays(p, w);
   if (by_group && ((tan && (g_gout || g_W)) || (t_gW && g_gout)) &&
       ((rc = ensure_groups(plan)) ||
        (rc = dbwd_state_by_group(p, G, w, ws, xk, evec, phi, txk, t_gevec, t_gphi, flags, W, t_gW, gk,

@@ -98,7 +98,7 @@ def _p(d):
 
 class Plan:
     def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw",
-                 dtype="f32", policy="all"):
+                 dtype="f32", policy="auto"):
         args = _lib._sig_args(irreps_in, lmax, irreps_out, K, layout, normalization, mode, dtype)
         h = ctypes.c_void_p()
         check(lib().sobek_plan_create(*args, ctypes.byref(h)))
@@ -112,7 +112,7 @@ class Plan:
         self.set_policy(policy)
 
     def set_policy(self, policy):
-        check(lib().sobek_plan_set_policy(self.handle, {"all": 0, "groups": 1}[policy]))
+        check(lib().sobek_plan_set_policy(self.handle, {"all": 0, "groups": 1, "auto": 2}[policy]))
         self.policy = policy
 
     def paths(self):

@@ -2,7 +2,8 @@
 receiver_chunk_budget) and retention of complete output groups (Section 4.2: forward state is kept
 only as whole output groups that fit the budget, the rest recomputed over bounded receiver ranges).
 
-* Per-group policy: forward, backward and double backward (the edge-vector cotangent alone and all
+* Per-group policy (and the default, which takes it when the all-group plan of a pass needs three or
+  more receiver chunks): forward, backward and double backward (the edge-vector cotangent alone and all
   four cotangents) against the float64 oracle, at the default workspace and at one small enough to
   split every pass into several chunks, on fully connected signatures (one and several output groups
   of different orders, a dead input and a dead output irrep, the mul_ir layout, the bf16 channel-GEMM
@@ -82,7 +83,8 @@ def test_per_group_policy(gpu, sig, mode, layout, dtype, N, E, seed):
     case = make_case(sig, N, E, seed, isolated=2, mode=mode)
     g = case["graph"]
     plan = api.Plan(irr_in, lmax, irr_out, K, layout=layout, mode=mode, dtype=dtype, policy="groups")
-    ref_plan = api.Plan(irr_in, lmax, irr_out, K, layout=layout, mode=mode, dtype=dtype)
+    ref_plan = api.Plan(irr_in, lmax, irr_out, K, layout=layout, mode=mode, dtype=dtype, policy="all")
+    auto_plan = api.Plan(irr_in, lmax, irr_out, K, layout=layout, mode=mode, dtype=dtype)   # the default
     prob = oc.Problem(irr_in, lmax, irr_out, K, layout=layout, mode=mode)
     graph = api.Graph(_t(g.rowptr), _t(g.sender))
     args = (_t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]))
@@ -123,6 +125,17 @@ def test_per_group_policy(gpu, sig, mode, layout, dtype, N, E, seed):
             finally:
                 _lib.profile_enable(False)
             print(f"{tag}: per-group chunks {launches}, all-group chunks {chunks_all}")
+            # the default policy takes the per-group route exactly when the all-group plan has >= 3 chunks
+            _lib.profile_reset()
+            _lib.profile_enable(True)
+            try:
+                m_auto = api.conv_fwd(auto_plan, graph, *args, budget=budget)
+                torch.cuda.synchronize()
+                auto = _lib.profile_read()
+            finally:
+                _lib.profile_enable(False)
+            assert ("sobek_fwdg0_S" in auto) == (chunks_all >= 3) and ("sobek_fwd_S" in auto) == (chunks_all < 3)
+            _check([m_auto], {"m": ref_f}, ["m"], FWD_TOL, tag + " fwd (auto)", loose=("m",) if bf else ())
             per = [4 * d * (D + C) for (d, D, C) in groups]
             for L, b in zip(launches, per):
                 assert 1 <= L <= chunks_all

@@ -32,7 +32,7 @@ def test_workspace_independent_of_edge_count(gpu):
     import torch
     from paper_2607_18074_amd import _lib, api
     irr_in, lmax, irr_out, K = SIGS["small"]
-    plan = api.Plan(irr_in, lmax, irr_out, K)
+    plan = api.Plan(irr_in, lmax, irr_out, K, policy="all")   # all-group receiver chunks throughout
     N = 300
     small_g = wl.random_graph(N, 2000, 51, K=K)
     big_g = wl.random_graph(N, 12000, 52, K=K)
