@@ -144,7 +144,7 @@ def pass_kernels(fn, torch, calls=3):
     return {k: dict(launches=n / calls, ms=t / calls) for k, (n, t) in sorted(prof.items(), key=lambda kv: -kv[1][1])}
 
 
-def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False, policy="all"):
+def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False, policy="auto"):
     """Every workload and pass of the benchmark configurations: one JSON line each, then a table.
     dtype "bf16_gemm" runs the plans' channel GEMM m = S A on bf16 MFMA (tensors stay fp32); policy
     "groups" builds receiver state one output group at a time (eq. receiver_chunk_budget)."""
@@ -200,7 +200,7 @@ def sweep(budget_gib, names, dtype="f32", retain=True, kernels=False, policy="al
             tag = name if dtype == "f32" else f"{name} ({dtype})"
             if not retain:
                 tag += f" [no kept state, {budget_gib:g} GiB]"
-            if policy != "all":
+            if policy != "auto":
                 tag += f" [{policy} policy]"
             row = dict(workload=tag, dtype=dtype, retain=retain, pass_=pname,
                        N=g.N, E=g.E, ms=ms, samples=n, edges_per_s=g.E / (ms * 1e-3),
@@ -318,7 +318,7 @@ def tables(which, budget_gib, retain, only=()):
             f"{r['peak_mem_gb']:.2f} |")
 
 
-def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd"), policy="all", keep_groups=False):
+def regimes(kinds, profiles, budget_gib, retain, passes=("fwd", "bwd", "dbwd"), policy="auto", keep_groups=False):
     """The paper's scaling regimes: degree scaling (2,048 nodes, mean degree 4..1,023) and graph-count
     scaling (B copies of a 128-node degree-32 graph, B = 2..511) on its representative profiles, every
     pass timed with the paper's protocol; one JSON line per point, a table at the end."""
@@ -534,9 +534,10 @@ def main():
     ap.add_argument("--retain", action="store_true", help="regimes: keep S and Sbar across passes (default: the "
                     "paper's setting, recompute within the workspace budget)")
     ap.add_argument("--kernels", action="store_true", help="sweep: also time every kernel of each pass")
-    ap.add_argument("--policy", default="all", choices=["all", "groups"],
+    ap.add_argument("--policy", default="auto", choices=["all", "groups", "auto"],
                     help="sweep/regimes: scratch policy of the plans (groups: receiver state one output group "
-                         "at a time, eq. receiver_chunk_budget)")
+                         "at a time, eq. receiver_chunk_budget; auto, the library's default: groups for a pass "
+                         "whose all-group plan needs three or more receiver chunks)")
     ap.add_argument("--keep-groups", action="store_true",
                     help="regimes: the forward keeps the output groups the retention choice fits in the budget "
                          "and the backward reads them")
