@@ -105,13 +105,15 @@ int sobek_version(void);
  *   dtype: SOBEK_DTYPE_F32, fp32 throughout (the paper's precision, Section 5.1);
  *          SOBEK_DTYPE_BF16_GEMM, a reduced-precision option for uvw plans whose
  *          multiplicities are all multiples of 4 (else SOBEK_E_UNSUPPORTED): the
- *          channel GEMMs with the receiver state, m = S A (Section 4.2 eq.
- *          receiver_matrix_product; the forward, and the double backward's
- *          products with S and dS) and A_bar = S^T mbar (Section 4.3 eq.
- *          receiver_adjoint; the weight gradients), round both operands to bf16
+ *          channel GEMMs, m = S A (Section 4.2 eq. receiver_matrix_product; the
+ *          forward, and the double backward's products with S and dS), A_bar =
+ *          S^T mbar (Section 4.3 eq. receiver_adjoint; the weight gradients) and,
+ *          for output groups whose multiplicity is a multiple of 32 (up to 256),
+ *          the adjoint state Sbar = mbar A^T (same equation; the backward's and
+ *          double backward's edge terms read it), round both operands to bf16
  *          (nearest even) and accumulate in fp32 on bf16 MFMA.  Every tensor at
- *          this boundary stays fp32; the edge stage, Sbar = mbar A^T and every
- *          reduction stay fp32.
+ *          this boundary stays fp32; S is stored in bf16, Sbar in fp32; the edge
+ *          stage and every reduction stay fp32.
  *   (uvu plans whose paths share one multiplicity run a forward and backward
  *   without receiver state; the environment variable SOBEK_UVU_ROUTE=receiver,
  *   read at plan creation, keeps them on the receiver-state route instead.

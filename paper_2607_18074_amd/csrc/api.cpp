@@ -886,7 +886,7 @@ int load_receiver_route(Plan& p, hipModule_t m) {
   if (p.vec4)
     for (auto& g : p.groups)
       if (sobek::sbar_streams(p.vec4, g.C) && !p.k.gemm_sbar_c.count(g.C)) {
-        std::string nm = "sobek_gemm_sbar_c" + std::to_string(g.C);
+        std::string nm = (sobek::sbar_bf16(p, g.C) ? "sobek_gemm_sbar_cb" : "sobek_gemm_sbar_c") + std::to_string(g.C);
         hipFunction_t f = nullptr;
         if ((rc = get_fn(m, f, nm.c_str()))) return rc;
         p.k.gemm_sbar_c[g.C] = f;

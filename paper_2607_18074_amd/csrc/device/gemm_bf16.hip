@@ -1,7 +1,7 @@
-// The channel GEMMs with the receiver state S on bf16 MFMA, for plans built with
-// the dtype SOBEK_DTYPE_BF16_GEMM: m_g = S_g A_g (Section 4.2 eq.
-// receiver_matrix_product) and the weight gradient A_bar = S^T mbar (Section 4.3
-// eq. receiver_adjoint), which the paper runs as fp32 GEMMs.  The generator appends this file to the
+// The channel GEMMs on bf16 MFMA, for plans built with the dtype
+// SOBEK_DTYPE_BF16_GEMM: m_g = S_g A_g (Section 4.2 eq. receiver_matrix_product),
+// the weight gradient A_bar = S^T mbar and the adjoint state Sbar = mbar A^T
+// (Section 4.3 eq. receiver_adjoint), which the paper runs as fp32 GEMMs.  The generator appends this file to the
 // plan's source only for such plans; it relies on the fp32 device code that
 // precedes every plan (sb_gemm_sa_v's tiling constants, loads and row mapping).
 //
@@ -223,3 +223,91 @@ SB_DEV void sb_gemm_ga_vb(const __bf16* __restrict__ S, int nrows, int D, const 
 SB_GEMM_VB_ENTRY(16)
 SB_GEMM_VB_ENTRY(32)
 SB_GEMM_VB_ENTRY(64)
+
+// Adjoint state Sbar_g = mbar_g A_g^T (Section 4.3 eq. receiver_adjoint) on bf16 MFMA: the blocking
+// of sb_gemm_sbar_s (64 rows of mbar per block, kept in LDS; 64-wide column tiles of Sbar walked in
+// 32-deep slices of w with A's slice double-buffered), one v_mfma_f32_16x16x32_bf16 per slice and
+// 16x16 tile instead of eight fp32 ones.  Rows of the transposed tile are k (A^T rows), columns are
+// receiver rows; the lane's eight w values of A and of mbar are rounded to bf16 as they leave LDS
+// and products accumulate in fp32.  Sbar is written in fp32.  CG (the group's multiplicity) is a
+// multiple of 32.
+template <int CG>
+SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
+                            const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int off, int CX,
+                            int r0) {
+  static_assert(CG % 32 == 0, "32-deep slices of w");
+  constexpr int PAD = 68;                       // row pitch of the transposed LDS tiles (floats)
+  constexpr int NV = CG / 4;                    // float4 per row of mbar
+  constexpr int WC = 32;                        // w per slice
+  constexpr int NS = CG / WC;                   // slices per column tile
+  constexpr int NBL = (64 * (WC / 4) + 255) / 256;  // float4 loads of a slice per thread
+  __shared__ float sM[CG][PAD];
+  __shared__ float sB[2][WC][PAD];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int j = lane & 15, g = lane >> 4, kg = 8 * g;
+  const int rb = blockIdx.x * 64;
+  for (int idx = tid; idx < 64 * NV; idx += 256) {
+    const int row = idx / NV, w4 = 4 * (idx % NV);
+    const int gr = rb + row;
+    const sb_v4 v = gr < nrows ? sb_ld4(M + sb_row_addr(gr, dg, CG, off, CX, r0) + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sM[w4 + c][row] = v[c];
+  }
+  sb_v4 rbv[NBL];
+  auto loadB = [&](int sl) {  // slice sl = (column tile, w chunk)
+    const int k0 = (sl / NS) * 64, w0 = (sl % NS) * WC;
+#pragma unroll
+    for (int i = 0; i < NBL; ++i) {
+      const int idx = tid + 256 * i;
+      const int kc = idx / (WC / 4), w4 = 4 * (idx % (WC / 4)), gk = k0 + kc;
+      rbv[i] = (idx < 64 * (WC / 4) && gk < D) ? sb_ld4(W + (sb_i64)ktab[gk] + w0 + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto storeB = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NBL; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < 64 * (WC / 4)) {
+        const int kc = idx / (WC / 4), w4 = 4 * (idx % (WC / 4));
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sB[buf][w4 + c][kc] = rbv[i][c];
+      }
+    }
+  };
+  // blockIdx.y takes a contiguous range of 64-wide column tiles
+  const int ntile = (D + 63) / 64, tpb = (ntile + gridDim.y - 1) / gridDim.y;
+  const int sl0 = blockIdx.y * tpb * NS, nsl = min(ntile, (int)(blockIdx.y + 1) * tpb) * NS;
+  loadB(sl0);
+  storeB(0);
+  __syncthreads();
+  const int row = rb + 16 * wave + j;
+  float* out = Sbar + (sb_i64)row * D;
+  sb_f4 acc[4];
+  for (int sl = sl0; sl < nsl; ++sl) {
+    const int buf = (sl - sl0) & 1, w0 = (sl % NS) * WC;
+    if (sl + 1 < nsl) loadB(sl + 1);
+    if (w0 == 0) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+    }
+    sb_b8 b;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) b[q] = (__bf16)sM[w0 + kg + q][16 * wave + j];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      sb_b8 a;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) a[q] = (__bf16)sB[buf][kg + q][16 * t + j];
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[t], 0, 0, 0);
+    }
+    if (w0 + WC >= CG && row < nrows) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int k = (sl / NS) * 64 + 16 * t + 4 * g;
+        if (k < D) *(sb_v4*)(out + k) = acc[t];
+      }
+    }
+    if (sl + 1 < nsl) storeB(buf ^ 1);
+    __syncthreads();
+  }
+}

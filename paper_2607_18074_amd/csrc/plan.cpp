@@ -1581,8 +1581,18 @@ std::string generate_source(const Plan& P, bool receiver_route) {
        "  sb_sender_reduce<CXI>(send_rowptr, send_perm, contrib, gx, cursor, N, e0, e1, first);\n"
        "}\n";
   if (!receiver_route) return o.str();
-  // reduced-precision plans: the bf16 variant of the vec4 channel GEMM
-  if (P.dtype == 1) o << kGemmBf16;
+  // reduced-precision plans: the bf16 variants of the vec4 channel GEMMs, and of the streaming
+  // adjoint-state GEMM for output multiplicities in multiples of 32
+  if (P.dtype == 1) {
+    o << kGemmBf16;
+    std::vector<int> cgs;
+    for (auto& g : P.groups)
+      if (sbar_bf16(P, g.C) && std::find(cgs.begin(), cgs.end(), g.C) == cgs.end()) cgs.push_back(g.C);
+    for (int C : cgs)
+      o << "extern \"C\" __global__ __launch_bounds__(256) void sobek_gemm_sbar_cb" << C
+        << "(const float* M, int nrows, int D, const float* W, const int* ktab, float* Sbar, int dg, int off, int CX,"
+           " int r0) {\n  sb_gemm_sbar_sb<" << C << ">(M, nrows, D, W, ktab, Sbar, dg, off, CX, r0);\n}\n";
+  }
 
   // forward S / dS kernels: one wave per (receiver, unit); bf16-GEMM plans store the state in bf16
   const char* st = P.dtype == 1 ? "__bf16" : "float";

@@ -148,6 +148,10 @@ struct Plan {
 void build_plan(Plan& p);
 // Generates the plan-specific HIP source (prepended by the shared prelude at compile time).
 std::string generate_source(const Plan& p, bool receiver_route = true);
+// bf16-GEMM plans run the streaming adjoint-state GEMM on bf16 MFMA for output multiplicities in
+// multiples of 32 (sobek_gemm_sbar_cb<C>); other widths keep the fp32 kernels.
+inline bool sbar_bf16(const Plan& p, int C) { return p.dtype == 1 && sbar_streams(p.vec4, C) && C % 32 == 0; }
+
 // Source of the materialized-forward baseline module (Section 2.4, eq. radial_projection_background).
 std::string generate_materialized_source(const Plan& p);
 // Source of the per-output-group state kernels (Appendix B.2, eq. receiver_chunk_budget).

@@ -127,6 +127,12 @@ def test_bf16_gemm_option():
     assert "bf16" not in s32
     assert sbf.count(block) == 1
     rest = sbf.replace(block, "")
+    # with it, one bf16 adjoint-state GEMM entry per output multiplicity that is a multiple of 32
+    entries = re.findall(r'extern "C" __global__ __launch_bounds__\(256\) void sobek_gemm_sbar_cb(\d+)\(.*?\n}\n',
+                         rest, re.S)
+    assert entries == ["32"]
+    rest = re.sub(r'extern "C" __global__ __launch_bounds__\(256\) void sobek_gemm_sbar_cb\d+\(.*?\n}\n', "", rest,
+                  flags=re.S)
     assert rest.count("__bf16* __restrict__ S,") >= 4 and rest.count("__bf16* Sg = S") >= 1   # 3 kernels + the units
     assert rest.replace("__bf16* __restrict__ S,", "float* __restrict__ S,").replace("__bf16* Sg = S", "float* Sg = S") == s32
     # reduced precision is implemented for uvw plans whose multiplicities are multiples of 4

@@ -1,20 +1,22 @@
-"""GPU parity of the reduced-precision channel GEMM (plan dtype "bf16_gemm").
+"""GPU parity of the reduced-precision channel GEMMs (plan dtype "bf16_gemm").
 
 Such a plan rounds both operands to bf16 inside the GEMMs with the receiver
 state, m = S A (Section 4.2 eq. receiver_matrix_product) and A_bar = S^T mbar
-(Section 4.3 eq. receiver_adjoint), and accumulates in fp32; every tensor at the
-boundary and every other stage stays fp32.  Checked through the C ABI against
-the float64 oracle on fp32 inputs:
+(Section 4.3 eq. receiver_adjoint), and, for output multiplicities in multiples
+of 32, inside the adjoint-state GEMM Sbar = mbar A^T (same equation); products
+accumulate in fp32, S is stored in bf16, every tensor at the boundary and every
+edge stage stays fp32.  Checked through the C ABI against the float64 oracle on
+fp32 inputs:
 
-* the outputs those GEMMs produce (forward m, the weight gradients, the double
-  backward's g_gout) within the reduced-precision bound 1e-2 (max-norm
-  relative): bf16 keeps 8 mantissa bits, so each rounded operand is off by at
-  most 2^-9 relative, and the accumulated sum stays well inside 1e-2 of the
-  largest output;
-* the forward really took the bf16 kernel: it differs from the fp32 plan's
-  forward by more than fp32 rounding could explain;
-* every other output (x_bar, phi_bar, evec_bar and their double-backward
-  counterparts, built from the fp32 adjoint state) keeps the fp32 tolerance.
+* every output within the reduced-precision bound 1e-2 (max-norm relative):
+  bf16 keeps 8 mantissa bits, so each rounded operand is off by at most 2^-9
+  relative, and the accumulated sums stay well inside 1e-2 of the largest
+  output (the edge-stage outputs x_bar, phi_bar, evec_bar inherit Sbar's
+  rounding);
+* the bf16 kernels really ran: the forward, the weight gradient and (where the
+  multiplicities are multiples of 32) the x-gradient differ from the fp32
+  plan's by more than fp32 rounding could explain; where they are not, the
+  x-gradient keeps the fp32 tolerance.
 """
 
 import numpy as np
@@ -84,14 +86,20 @@ def test_bf16_backward(gpu, sig, N, E, seed, iso):
     for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
         err = max_rel(_n(o), ref[name])
         print(f"bf16-plan bwd {sig} {name}: {err:.2e}")
-        assert err <= (BF16_TOL if name == "gW" else BWD_TOL), name
-    # the weight gradient came from the bf16 kernel: the fp32 plan's differs by more than rounding
+        assert err <= BF16_TOL, name
+    # the weight gradient came from the bf16 kernel, and so did Sbar when every multiplicity is a
+    # multiple of 32: the fp32 plan's gradients differ by more than rounding
     _, plan32, graph32, _ = _setup(case, "f32")
-    gW32 = api.conv_bwd(plan32, graph32, _t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]), _t(case["gout"]),
-                        need=(False, False, False, True))[3]
+    gx32, _, _, gW32 = api.conv_bwd(plan32, graph32, _t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]),
+                                    _t(case["gout"]), need=(True, False, False, True))
     gap = max_rel(_n(outs[3]), _n(gW32))
-    print(f"bf16-plan bwd {sig} gW vs fp32 plan: {gap:.2e}")
+    gapx = max_rel(_n(outs[0]), _n(gx32))
+    print(f"bf16-plan bwd {sig} vs fp32 plan: gW {gap:.2e}, gx {gapx:.2e}")
     assert gap > 1e-5
+    if all(m % 32 == 0 for (m, _l, _p) in plan.irreps_out):
+        assert gapx > 1e-5
+    else:
+        assert max_rel(_n(outs[0]), ref["gx"]) <= BWD_TOL
 
 
 @pytest.mark.parametrize("sig,N,E,seed,iso", CASES[1:3])
@@ -108,14 +116,13 @@ def test_bf16_double_backward(gpu, sig, N, E, seed, iso):
     for name, o in zip(names, outs):
         err = max_rel(_n(o), ref[name])
         print(f"bf16 dbwd {sig} {name}: {err:.2e}")
-        # g_gout and g_W come from the bf16 GEMMs; the rest from the fp32 adjoint kernels
-        assert err <= (BF16_TOL if name in ("g_gout", "g_W") else BWD_TOL), name
+        assert err <= BF16_TOL, name
 
 
 def test_bf16_retained_states(gpu):
     """The bf16 plan keeps S in bf16 (the first half of a sobek_state_size buffer) and the adjoint state in
     fp32 (a whole one): forward, backward and double backward through the kept states match the oracle
-    (bf16-GEMM outputs within the bf16 tolerance) and agree with the plain calls."""
+    within the bf16 tolerance and agree with the plain calls."""
     case = make_case("small", 300, 4000, 31, isolated=2)
     api, plan, graph, prob = _setup(case, "bf16_gemm")
     g = case["graph"]
@@ -132,13 +139,13 @@ def test_bf16_retained_states(gpu):
     plain = api.conv_bwd(plan, graph, *args, gout)
     ref = oc.bwd(*oa, case["gout"])
     for name, o, q in zip(("gx", "gevec", "gphi", "gW"), outs, plain):
-        assert max_rel(_n(o), ref[name]) <= (BF16_TOL if name == "gW" else BWD_TOL), name
+        assert max_rel(_n(o), ref[name]) <= BF16_TOL, name
         assert max_rel(_n(o), _n(q)) <= 1e-4, name
     tev = _t(case["cot"]["evec"])
     outs = api.conv_dbwd(plan, graph, *args, gout, None, tev, None, None, adj_state=adj)
     ref = oc.dbwd(*oa, case["gout"], t_gevec=case["cot"]["evec"])
     for name, o in zip(("g_gout", "g_x", "g_evec", "g_phi", "g_W"), outs):
-        assert max_rel(_n(o), ref[name]) <= (BF16_TOL if name in ("g_gout", "g_W") else BWD_TOL), name
+        assert max_rel(_n(o), ref[name]) <= BF16_TOL, name
 
 
 @pytest.mark.timeout(600)

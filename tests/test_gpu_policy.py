@@ -144,15 +144,16 @@ def test_per_group_policy(gpu, sig, mode, layout, dtype, N, E, seed):
                 if per[i] > per[j]:
                     assert launches[i] >= launches[j]
         outs = api.conv_bwd(plan, graph, *args, gout, budget=budget)
-        _check(outs, ref_b, ("gx", "gevec", "gphi", "gW"), BWD_TOL, tag + " bwd", loose=("gW",) if bf else ())
+        _check(outs, ref_b, ("gx", "gevec", "gphi", "gW"), BWD_TOL, tag + " bwd",
+               loose=("gx", "gevec", "gphi", "gW") if bf else ())
         outs = api.conv_dbwd(plan, graph, *args, gout, None, _t(c["evec"]), None, None, budget=budget)
         _check(outs, ref_de, ("g_gout", "g_x", "g_evec", "g_phi", "g_W"), BWD_TOL, tag + " dbwd[evec]",
-               loose=("g_gout", "g_W") if bf else ())
+               loose=("g_gout", "g_x", "g_evec", "g_phi", "g_W") if bf else ())
         full = lambda: api.conv_dbwd(plan, graph, *args, gout, _t(c["x"]), _t(c["evec"]), _t(c["phi"]),
                                      _t(c["W"]), budget=budget)
         outs = full()
         _check(outs, ref_da, ("g_gout", "g_x", "g_evec", "g_phi", "g_W"), BWD_TOL, tag + " dbwd[all]",
-               loose=("g_gout", "g_W") if bf else ())
+               loose=("g_gout", "g_x", "g_evec", "g_phi", "g_W") if bf else ())
         for a, b in zip(outs, full()):
             assert np.array_equal(_n(a), _n(b)), tag
 
