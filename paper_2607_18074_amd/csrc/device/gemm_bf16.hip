@@ -225,33 +225,31 @@ SB_GEMM_VB_ENTRY(32)
 SB_GEMM_VB_ENTRY(64)
 
 // Adjoint state Sbar_g = mbar_g A_g^T (Section 4.3 eq. receiver_adjoint) on bf16 MFMA: the blocking
-// of sb_gemm_sbar_s (64 rows of mbar per block, kept in LDS; 64-wide column tiles of Sbar walked in
-// 32-deep slices of w with A's slice double-buffered), one v_mfma_f32_16x16x32_bf16 per slice and
-// 16x16 tile instead of eight fp32 ones.  Rows of the transposed tile are k (A^T rows), columns are
-// receiver rows; the lane's eight w values of A and of mbar are rounded to bf16 as they leave LDS
-// and products accumulate in fp32.  Sbar is written in fp32.  CG (the group's multiplicity) is a
-// multiple of 32.
+// and w-contiguous LDS rows of sb_gemm_sbar_w (64 rows of mbar per block; 64-wide column tiles of
+// Sbar walked in 32-deep slices of w with A's slice double-buffered), one v_mfma_f32_16x16x32_bf16
+// per slice and 16x16 tile: lane group g takes w = 8g .. 8g + 7 of its A row and its mbar row (two
+// 16-byte LDS reads each), rounded to bf16 as they leave LDS; products accumulate in fp32 and Sbar
+// is written in fp32.  CG (the group's multiplicity) is a multiple of 32.
 template <int CG>
 SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
                             const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int off, int CX,
                             int r0) {
   static_assert(CG % 32 == 0, "32-deep slices of w");
-  constexpr int PAD = 68;                       // row pitch of the transposed LDS tiles (floats)
-  constexpr int NV = CG / 4;                    // float4 per row of mbar
   constexpr int WC = 32;                        // w per slice
   constexpr int NS = CG / WC;                   // slices per column tile
+  constexpr int PM = CG + 4, PB = WC + 4;       // LDS row pitches (floats)
+  constexpr int NV = CG / 4;                    // float4 per row of mbar
   constexpr int NBL = (64 * (WC / 4) + 255) / 256;  // float4 loads of a slice per thread
-  __shared__ float sM[CG][PAD];
-  __shared__ float sB[2][WC][PAD];
+  __shared__ __attribute__((aligned(16))) float sM[64 * PM];
+  __shared__ __attribute__((aligned(16))) float sB[2][64 * PB];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int j = lane & 15, g = lane >> 4, kg = 8 * g;
+  const int j = lane & 15, g = lane >> 4;
   const int rb = blockIdx.x * 64;
   for (int idx = tid; idx < 64 * NV; idx += 256) {
     const int row = idx / NV, w4 = 4 * (idx % NV);
     const int gr = rb + row;
-    const sb_v4 v = gr < nrows ? sb_ld4(M + sb_row_addr(gr, dg, CG, off, CX, r0) + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < 4; ++c) sM[w4 + c][row] = v[c];
+    *(sb_v4*)&sM[row * PM + w4] =
+        gr < nrows ? sb_ld4(M + sb_row_addr(gr, dg, CG, off, CX, r0) + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
   }
   sb_v4 rbv[NBL];
   auto loadB = [&](int sl) {  // slice sl = (column tile, w chunk)
@@ -267,12 +265,13 @@ SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const
 #pragma unroll
     for (int i = 0; i < NBL; ++i) {
       const int idx = tid + 256 * i;
-      if (idx < 64 * (WC / 4)) {
-        const int kc = idx / (WC / 4), w4 = 4 * (idx % (WC / 4));
-#pragma unroll
-        for (int c = 0; c < 4; ++c) sB[buf][w4 + c][kc] = rbv[i][c];
-      }
+      if (idx < 64 * (WC / 4)) *(sb_v4*)&sB[buf][(idx / (WC / 4)) * PB + 4 * (idx % (WC / 4))] = rbv[i];
     }
+  };
+  auto bf8 = [](const float* p) -> sb_b8 {
+    const sb_v4 u = *(const sb_v4*)p, v = *(const sb_v4*)(p + 4);
+    return (sb_b8){(__bf16)u[0], (__bf16)u[1], (__bf16)u[2], (__bf16)u[3],
+                   (__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
   };
   // blockIdx.y takes a contiguous range of 64-wide column tiles
   const int ntile = (D + 63) / 64, tpb = (ntile + gridDim.y - 1) / gridDim.y;
@@ -282,6 +281,7 @@ SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const
   __syncthreads();
   const int row = rb + 16 * wave + j;
   float* out = Sbar + (sb_i64)row * D;
+  const float* mrow = &sM[(16 * wave + j) * PM + 8 * g];
   sb_f4 acc[4];
   for (int sl = sl0; sl < nsl; ++sl) {
     const int buf = (sl - sl0) & 1, w0 = (sl % NS) * WC;
@@ -290,16 +290,10 @@ SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
     }
-    sb_b8 b;
+    const sb_b8 b = bf8(mrow + w0);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) b[q] = (__bf16)sM[w0 + kg + q][16 * wave + j];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      sb_b8 a;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) a[q] = (__bf16)sB[buf][kg + q][16 * t + j];
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[t], 0, 0, 0);
-    }
+    for (int t = 0; t < 4; ++t)
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf8(&sB[buf][(16 * t + j) * PB + 8 * g]), b, acc[t], 0, 0, 0);
     if (w0 + WC >= CG && row < nrows) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {

@@ -399,10 +399,18 @@ SB_DEV void sb_gemm_sbar_v(const float* __restrict__ M, int nrows, int D, const 
 // taken transposed, Sbar^T tile = A_g tile x mbar^T (16x16x4 MFMA, A rows = k,
 // B columns = rows), which leaves lane (j + 16 g) with columns 4g .. 4g + 3 of row
 // j: one float4 store per 16x16 tile and lane.  CG (the group's multiplicity) is a
-// multiple of 4.
+// multiple of 4; multiples of 16 take sb_gemm_sbar_w below.
+template <int CG>
+SB_DEV void sb_gemm_sbar_w(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
+                           const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int off, int CX, int r0);
+
 template <int CG>
 SB_DEV void sb_gemm_sbar_s(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
                            const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int off, int CX, int r0) {
+  if constexpr (CG % 16 == 0) {
+    sb_gemm_sbar_w<CG>(M, nrows, D, W, ktab, Sbar, dg, off, CX, r0);
+    return;
+  }
   constexpr int PAD = 68;                       // row pitch of the transposed LDS tiles (floats)
   constexpr int NV = CG / 4;                    // float4 per row of mbar
   constexpr int WC = CG < 32 ? CG : 32;         // w per slice
@@ -463,6 +471,89 @@ SB_DEV void sb_gemm_sbar_s(const float* __restrict__ M, int nrows, int D, const 
       const float b = sM[w0 + w + g][16 * wave + j];
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = sb_mfma(sB[buf][w + g][16 * t + j], b, acc[t]);
+    }
+    if (w0 + WC >= CG && row < nrows) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int k = (sl / NS) * 64 + 16 * t + 4 * g;
+        if (k < D) *(sb_v4*)(out + k) = acc[t];
+      }
+    }
+    if (sl + 1 < nsl) storeB(buf ^ 1);
+    __syncthreads();
+  }
+}
+
+// The streaming Sbar GEMM for multiplicities in multiples of 16, with w-contiguous LDS rows: the
+// block's mbar rows as stored ([row][w], pitch CG + 4 floats) and A's slice as [k][w] (pitch WC + 4),
+// so a lane takes four consecutive w of its A row and of its mbar row with one 16-byte LDS read each
+// (the row pitches keep eight lanes' reads on distinct banks).  The 16x16x4 MFMA sums over its four
+// lane groups; in step s of a 16-wide block of w, lane group g supplies w = 4g + s for both operands,
+// so four steps cover the block.  Blocking, slices, the column-tile split and the stores are those of
+// sb_gemm_sbar_s.
+template <int CG>
+SB_DEV void sb_gemm_sbar_w(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
+                           const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int off, int CX, int r0) {
+  static_assert(CG % 16 == 0, "16-wide blocks of w");
+  constexpr int WC = CG < 32 ? CG : 32;         // w per slice (16 or 32; divides CG)
+  constexpr int NS = CG / WC;                   // slices per column tile
+  constexpr int PM = CG + 4, PB = WC + 4;       // LDS row pitches (floats)
+  constexpr int NV = CG / 4;                    // float4 per row of mbar
+  constexpr int NBL = (64 * (WC / 4) + 255) / 256;  // float4 loads of a slice per thread
+  __shared__ __attribute__((aligned(16))) float sM[64 * PM];
+  __shared__ __attribute__((aligned(16))) float sB[2][64 * PB];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int j = lane & 15, g = lane >> 4;
+  const int rb = blockIdx.x * 64;
+  for (int idx = tid; idx < 64 * NV; idx += 256) {
+    const int row = idx / NV, w4 = 4 * (idx % NV);
+    const int gr = rb + row;
+    *(sb_v4*)&sM[row * PM + w4] =
+        gr < nrows ? sb_ld4(M + sb_row_addr(gr, dg, CG, off, CX, r0) + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+  }
+  sb_v4 rbv[NBL];
+  auto loadB = [&](int sl) {  // slice sl = (column tile, w chunk)
+    const int k0 = (sl / NS) * 64, w0 = (sl % NS) * WC;
+#pragma unroll
+    for (int i = 0; i < NBL; ++i) {
+      const int idx = tid + 256 * i;
+      const int kc = idx / (WC / 4), w4 = 4 * (idx % (WC / 4)), gk = k0 + kc;
+      rbv[i] = (idx < 64 * (WC / 4) && gk < D) ? sb_ld4(W + (sb_i64)ktab[gk] + w0 + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto storeB = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NBL; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < 64 * (WC / 4)) *(sb_v4*)&sB[buf][(idx / (WC / 4)) * PB + 4 * (idx % (WC / 4))] = rbv[i];
+    }
+  };
+  // blockIdx.y takes a contiguous range of 64-wide column tiles
+  const int ntile = (D + 63) / 64, tpb = (ntile + gridDim.y - 1) / gridDim.y;
+  const int sl0 = blockIdx.y * tpb * NS, nsl = min(ntile, (int)(blockIdx.y + 1) * tpb) * NS;
+  loadB(sl0);
+  storeB(0);
+  __syncthreads();
+  const int row = rb + 16 * wave + j;
+  float* out = Sbar + (sb_i64)row * D;
+  const float* mrow = &sM[(16 * wave + j) * PM + 4 * g];
+  sb_f4 acc[4];
+  for (int sl = sl0; sl < nsl; ++sl) {
+    const int buf = (sl - sl0) & 1, w0 = (sl % NS) * WC;
+    if (sl + 1 < nsl) loadB(sl + 1);
+    if (w0 == 0) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int wb = 0; wb < WC; wb += 16) {
+      const sb_v4 b = *(const sb_v4*)(mrow + w0 + wb);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const sb_v4 a = *(const sb_v4*)&sB[buf][(16 * t + j) * PB + wb + 4 * g];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) acc[t] = sb_mfma(a[s], b[s], acc[t]);
+      }
     }
     if (w0 + WC >= CG && row < nrows) {
 #pragma unroll
