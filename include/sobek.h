@@ -237,7 +237,9 @@ int sobek_state_size(sobek_plan plan, sobek_graph graph, size_t *bytes);
  * SOBEK_POLICY_ALL_GROUPS: each receiver chunk builds the state of every output group, in chunks
  * sized by the workspace planner.  SOBEK_POLICY_AUTO (the default): per pass, the per-group route
  * below when the all-group plan of the pass needs three or more receiver chunks (Appendix B.2 takes
- * a chunked route only when it gives at least three chunks), else all groups.
+ * a chunked route only when it gives at least three chunks) and each chunk holds fewer than 8192
+ * forward-state waves (receivers x wave units: too few to fill the GPU), else all groups; the
+ * per-group route walks every edge once per output group.
  * SOBEK_POLICY_PER_GROUP: the forward, the
  * backward's weight gradient and the double backward's state legs (dS and S) take one output
  * group g at a time, in chunks of n_g = min(N, max(1, floor(B / (4 d_g (D_g + C_g))))) receivers,

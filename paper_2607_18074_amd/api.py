@@ -49,7 +49,8 @@ class Plan:
     accumulation; tensors stay fp32), and
     scratch policy ("all": every output group per receiver chunk; "groups": the receiver-state legs one
     output group at a time in chunks of n_g receivers, eq. receiver_chunk_budget; "auto", the default:
-    "groups" for a pass whose all-group plan needs three or more receiver chunks)."""
+    "groups" for a pass whose all-group plan needs three or more receiver chunks, each too small to fill
+    the GPU)."""
 
     def __init__(self, irreps_in, lmax, irreps_out, K, layout="ir_mul", normalization="none", mode="uvw",
                  dtype="f32", policy="auto"):

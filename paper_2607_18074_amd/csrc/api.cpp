@@ -553,10 +553,17 @@ size_t kept_offset(const Plan& p, int64_t N, uint64_t mask, int gi) {
 
 bool kept(uint64_t mask, int gi) { return gi < 64 && (mask >> gi & 1); }
 
+// Forward-state waves (receivers x wave units) below which an all-group receiver chunk leaves the
+// GPU underfilled: eight waves on each of its 1024 SIMDs.
+constexpr int64_t kFillWaves = 8 * 1024;
+
 // SOBEK_POLICY_AUTO: the per-group route when the all-group plan of a pass needs at least three
-// receiver chunks (Appendix B.2 takes a chunked route only when it gives at least three chunks).
+// receiver chunks (Appendix B.2 takes a chunked route only when it gives at least three chunks) and
+// each of them is too small to fill the GPU.  The per-group route walks every edge once per output
+// group, so with all-group chunks that already fill the GPU it only adds edge traffic.
 bool group_route_pays(const Plan& p, const WsPlan& w) {
-  return p.policy == SOBEK_POLICY_AUTO && w.chunks.size() >= 3;
+  return p.policy == SOBEK_POLICY_AUTO && w.chunks.size() >= 3 &&
+         w.ncap * (int64_t)p.fwd_units.size() < kFillWaves;
 }
 
 // Whether `mask` keeps every output group (never for a plan with more than 64).

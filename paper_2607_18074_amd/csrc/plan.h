@@ -108,7 +108,8 @@ struct Plan {
   int lmax = 0, K = 0, layout = 0, dtype = 0, norm = 0;
   int mode = 0;                 // 0: uvw (fully connected mixing), 1: uvu (channelwise)
   int policy = 2;               // scratch policy: 0 all groups per receiver chunk, 1 one output group at a
-                                // time, 2 (default) the second when the first needs three or more chunks
+                                // time, 2 (default) the second when the first gives three or more chunks
+                                // too small to fill the GPU
   std::vector<int> grp_units;   // forward wave units of each output group's own state kernels
   int dim_in = 0, dim_out = 0, nsh = 0;
   int64_t n_w = 0;

@@ -3,9 +3,9 @@ receiver_chunk_budget) and retention of complete output groups (Section 4.2: for
 only as whole output groups that fit the budget, the rest recomputed over bounded receiver ranges).
 
 * Per-group policy (and the default, which takes it when the all-group plan of a pass needs three or
-  more receiver chunks): forward, backward and double backward (the edge-vector cotangent alone and all
-  four cotangents) against the float64 oracle, at the default workspace and at one small enough to
-  split every pass into several chunks, on fully connected signatures (one and several output groups
+  more receiver chunks, each too small to fill the GPU): forward, backward and double backward (the
+  edge-vector cotangent alone and all four cotangents) against the float64 oracle, at the default
+  workspace and at one small enough to split every pass into several chunks, on fully connected signatures (one and several output groups
   of different orders, a dead input and a dead output irrep, the mul_ir layout, the bf16 channel-GEMM
   plan) and a channelwise one.  From the launch profile: the per-group state kernels ran and the
   all-group one did not, each group's chunks fit the workspace under eq. receiver_chunk_budget
@@ -125,7 +125,8 @@ def test_per_group_policy(gpu, sig, mode, layout, dtype, N, E, seed):
             finally:
                 _lib.profile_enable(False)
             print(f"{tag}: per-group chunks {launches}, all-group chunks {chunks_all}")
-            # the default policy takes the per-group route exactly when the all-group plan has >= 3 chunks
+            # the default policy takes the per-group route only when the all-group plan has >= 3 chunks
+            # (and these small graphs' chunks never fill the GPU, so then always)
             _lib.profile_reset()
             _lib.profile_enable(True)
             try:
