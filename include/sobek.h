@@ -108,7 +108,7 @@ int sobek_version(void);
  *          channel GEMMs, m = S A (Section 4.2 eq. receiver_matrix_product; the
  *          forward, and the double backward's products with S and dS), A_bar =
  *          S^T mbar (Section 4.3 eq. receiver_adjoint; the weight gradients) and,
- *          for output groups whose multiplicity is a multiple of 32 (up to 256),
+ *          for output groups whose multiplicity is a multiple of 32 (up to 128),
  *          the adjoint state Sbar = mbar A^T (same equation; the backward's and
  *          double backward's edge terms read it), round both operands to bf16
  *          (nearest even) and accumulate in fp32 on bf16 MFMA.  Every tensor at

@@ -45,7 +45,7 @@ POLICIES = {"all": 0, "groups": 1, "auto": 2}
 class Plan:
     """Operator signature: irreps, spherical-harmonic order, radial width, channel mode ("uvw" fully
     connected, "uvu" channelwise), dtype ("f32", or "bf16_gemm": the channel GEMMs m = S A, A_bar =
-    S^T mbar and, for multiplicities in multiples of 32, Sbar = mbar A^T on bf16 MFMA with fp32
+    S^T mbar and, for multiplicities in multiples of 32 up to 128, Sbar = mbar A^T on bf16 MFMA with fp32
     accumulation; tensors stay fp32), and
     scratch policy ("all": every output group per receiver chunk; "groups": the receiver-state legs one
     output group at a time in chunks of n_g receivers, eq. receiver_chunk_budget; "auto", the default:

@@ -622,7 +622,7 @@ int run_sbar(const Plan& p, const Chunk& c, int64_t s_ncap, const float* M, cons
     {
       // spread the 64-wide column tiles over blockIdx.y until about kSaTarget blocks run,
       // keeping at least four tiles per block
-      const int rows = cdiv(nrows, 64), ntile = cdiv(D, 64);
+      const int rows = cdiv(nrows, sobek::sbar_block_rows(p, g.C)), ntile = cdiv(D, 64);
       const int gy = std::max(1, std::min((int)cdiv(kSaTarget, rows), ntile / 4));
       LAUNCH(p.k.gemm_sbar_c.at(g.C), rows, gy, 1, s, M, nrows, D, W, (const int*)(p.d_ktab + g.ktab_off), Sg, dg,
              off, CX, r0);

@@ -224,32 +224,42 @@ SB_GEMM_VB_ENTRY(16)
 SB_GEMM_VB_ENTRY(32)
 SB_GEMM_VB_ENTRY(64)
 
-// Adjoint state Sbar_g = mbar_g A_g^T (Section 4.3 eq. receiver_adjoint) on bf16 MFMA: the blocking
-// and w-contiguous LDS rows of sb_gemm_sbar_w (64 rows of mbar per block; 64-wide column tiles of
-// Sbar walked in 32-deep slices of w with A's slice double-buffered), one v_mfma_f32_16x16x32_bf16
-// per slice and 16x16 tile: lane group g takes w = 8g .. 8g + 7 of its A row and its mbar row (two
-// 16-byte LDS reads each), rounded to bf16 as they leave LDS; products accumulate in fp32 and Sbar
-// is written in fp32.  CG (the group's multiplicity) is a multiple of 32.
+// Adjoint state Sbar_g = mbar_g A_g^T (Section 4.3 eq. receiver_adjoint) on bf16 MFMA, streaming:
+// a block owns SB_SBR rows of mbar (kept in LDS in bf16, w contiguous) and walks its range of 64-wide
+// column tiles of Sbar in 32-deep slices of w, A's slice double-buffered in LDS (bf16, w contiguous).
+// Wave v owns rows 64v .. 64v + 63 of the block (four 16-row tiles), so each slice costs sixteen
+// v_mfma_f32_16x16x32_bf16 per wave, and A_g is read once per SB_SBR rows: the group's A (several MB
+// for 128-channel groups, beyond one XCD's L2) would otherwise be streamed again for every 64 rows.
+// Operands are rounded to bf16 (nearest even) as they enter LDS; products accumulate in fp32 and Sbar
+// is written in fp32.  Lane (j + 16 g) supplies w = 8g .. 8g + 7 of its A row and mbar row, one 16-byte
+// LDS read each; the product is taken transposed (rows of the tile = k), which leaves the lane with
+// columns 4g .. 4g + 3 of row j: one float4 store per tile.  CG (the group's multiplicity) is a multiple
+// of 32, at most 128 (the mbar rows then take at most 68 KB of LDS).
+#define SB_SBR 256
+
 template <int CG>
 SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const float* __restrict__ W,
                             const int* __restrict__ ktab, float* __restrict__ Sbar, int dg, int off, int CX,
                             int r0) {
-  static_assert(CG % 32 == 0, "32-deep slices of w");
+  static_assert(CG % 32 == 0 && CG <= 128, "32-deep slices of w, mbar rows within LDS");
   constexpr int WC = 32;                        // w per slice
   constexpr int NS = CG / WC;                   // slices per column tile
-  constexpr int PM = CG + 4, PB = WC + 4;       // LDS row pitches (floats)
+  constexpr int PM = CG + 8, PB = WC + 8;       // LDS row pitches (bf16)
   constexpr int NV = CG / 4;                    // float4 per row of mbar
   constexpr int NBL = (64 * (WC / 4) + 255) / 256;  // float4 loads of a slice per thread
-  __shared__ __attribute__((aligned(16))) float sM[64 * PM];
-  __shared__ __attribute__((aligned(16))) float sB[2][64 * PB];
+  __shared__ __attribute__((aligned(16))) __bf16 sM[SB_SBR * PM];
+  __shared__ __attribute__((aligned(16))) __bf16 sB[2][64 * PB];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int j = lane & 15, g = lane >> 4;
-  const int rb = blockIdx.x * 64;
-  for (int idx = tid; idx < 64 * NV; idx += 256) {
+  const int rb = blockIdx.x * SB_SBR;
+  auto put4 = [](__bf16* p, sb_v4 v) {  // four values rounded to bf16, one 8-byte LDS store
+    *(sb_b4*)p = (sb_b4){(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+  };
+  for (int idx = tid; idx < SB_SBR * NV; idx += 256) {
     const int row = idx / NV, w4 = 4 * (idx % NV);
     const int gr = rb + row;
-    *(sb_v4*)&sM[row * PM + w4] =
-        gr < nrows ? sb_ld4(M + sb_row_addr(gr, dg, CG, off, CX, r0) + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f};
+    put4(&sM[row * PM + w4],
+         gr < nrows ? sb_ld4(M + sb_row_addr(gr, dg, CG, off, CX, r0) + w4) : (sb_v4){0.f, 0.f, 0.f, 0.f});
   }
   sb_v4 rbv[NBL];
   auto loadB = [&](int sl) {  // slice sl = (column tile, w chunk)
@@ -265,13 +275,8 @@ SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const
 #pragma unroll
     for (int i = 0; i < NBL; ++i) {
       const int idx = tid + 256 * i;
-      if (idx < 64 * (WC / 4)) *(sb_v4*)&sB[buf][(idx / (WC / 4)) * PB + 4 * (idx % (WC / 4))] = rbv[i];
+      if (idx < 64 * (WC / 4)) put4(&sB[buf][(idx / (WC / 4)) * PB + 4 * (idx % (WC / 4))], rbv[i]);
     }
-  };
-  auto bf8 = [](const float* p) -> sb_b8 {
-    const sb_v4 u = *(const sb_v4*)p, v = *(const sb_v4*)(p + 4);
-    return (sb_b8){(__bf16)u[0], (__bf16)u[1], (__bf16)u[2], (__bf16)u[3],
-                   (__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
   };
   // blockIdx.y takes a contiguous range of 64-wide column tiles
   const int ntile = (D + 63) / 64, tpb = (ntile + gridDim.y - 1) / gridDim.y;
@@ -279,26 +284,37 @@ SB_DEV void sb_gemm_sbar_sb(const float* __restrict__ M, int nrows, int D, const
   loadB(sl0);
   storeB(0);
   __syncthreads();
-  const int row = rb + 16 * wave + j;
-  float* out = Sbar + (sb_i64)row * D;
-  const float* mrow = &sM[(16 * wave + j) * PM + 8 * g];
-  sb_f4 acc[4];
+  sb_f4 acc[4][4];  // [row tile][column tile]
   for (int sl = sl0; sl < nsl; ++sl) {
     const int buf = (sl - sl0) & 1, w0 = (sl % NS) * WC;
     if (sl + 1 < nsl) loadB(sl + 1);
     if (w0 == 0) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) acc[t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
+      for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[rt][t] = (sb_f4){0.f, 0.f, 0.f, 0.f};
     }
-    const sb_b8 b = bf8(mrow + w0);
+    sb_b8 a[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf8(&sB[buf][(16 * t + j) * PB + 8 * g]), b, acc[t], 0, 0, 0);
-    if (w0 + WC >= CG && row < nrows) {
+    for (int t = 0; t < 4; ++t) a[t] = *(const sb_b8*)&sB[buf][(16 * t + j) * PB + 8 * g];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int k = (sl / NS) * 64 + 16 * t + 4 * g;
-        if (k < D) *(sb_v4*)(out + k) = acc[t];
+    for (int rt = 0; rt < 4; ++rt) {
+      const sb_b8 b = *(const sb_b8*)&sM[(64 * wave + 16 * rt + j) * PM + w0 + 8 * g];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[rt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t], b, acc[rt][t], 0, 0, 0);
+    }
+    if (w0 + WC >= CG) {
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        const int row = rb + 64 * wave + 16 * rt + j;
+        if (row < nrows) {
+          float* out = Sbar + (sb_i64)row * D;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int k = (sl / NS) * 64 + 16 * t + 4 * g;
+            if (k < D) *(sb_v4*)(out + k) = acc[rt][t];
+          }
+        }
       }
     }
     if (sl + 1 < nsl) storeB(buf ^ 1);

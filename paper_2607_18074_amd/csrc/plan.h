@@ -150,8 +150,10 @@ void build_plan(Plan& p);
 // Generates the plan-specific HIP source (prepended by the shared prelude at compile time).
 std::string generate_source(const Plan& p, bool receiver_route = true);
 // bf16-GEMM plans run the streaming adjoint-state GEMM on bf16 MFMA for output multiplicities in
-// multiples of 32 (sobek_gemm_sbar_cb<C>); other widths keep the fp32 kernels.
-inline bool sbar_bf16(const Plan& p, int C) { return p.dtype == 1 && sbar_streams(p.vec4, C) && C % 32 == 0; }
+// multiples of 32 up to 128 (sobek_gemm_sbar_cb<C>, 256 rows of mbar per block); other widths keep
+// the fp32 kernels (64 rows per block).
+inline bool sbar_bf16(const Plan& p, int C) { return p.dtype == 1 && sbar_streams(p.vec4, C) && C % 32 == 0 && C <= 128; }
+inline int sbar_block_rows(const Plan& p, int C) { return sbar_bf16(p, C) ? 256 : 64; }
 
 // Source of the materialized-forward baseline module (Section 2.4, eq. radial_projection_background).
 std::string generate_materialized_source(const Plan& p);

@@ -3,7 +3,7 @@
 Such a plan rounds both operands to bf16 inside the GEMMs with the receiver
 state, m = S A (Section 4.2 eq. receiver_matrix_product) and A_bar = S^T mbar
 (Section 4.3 eq. receiver_adjoint), and, for output multiplicities in multiples
-of 32, inside the adjoint-state GEMM Sbar = mbar A^T (same equation); products
+of 32 up to 128, inside the adjoint-state GEMM Sbar = mbar A^T (same equation); products
 accumulate in fp32, S is stored in bf16, every tensor at the boundary and every
 edge stage stays fp32.  Checked through the C ABI against the float64 oracle on
 fp32 inputs:
@@ -96,7 +96,7 @@ def test_bf16_backward(gpu, sig, N, E, seed, iso):
     gapx = max_rel(_n(outs[0]), _n(gx32))
     print(f"bf16-plan bwd {sig} vs fp32 plan: gW {gap:.2e}, gx {gapx:.2e}")
     assert gap > 1e-5
-    if all(m % 32 == 0 for (m, _l, _p) in plan.irreps_out):
+    if all(m % 32 == 0 and m <= 128 for (m, _l, _p) in plan.irreps_out):
         assert gapx > 1e-5
     else:
         assert max_rel(_n(outs[0]), ref["gx"]) <= BWD_TOL
