@@ -223,6 +223,7 @@ SB_DEV void sb_gemm_ga_vb(const __bf16* __restrict__ S, int nrows, int D, const 
 SB_GEMM_VB_ENTRY(16)
 SB_GEMM_VB_ENTRY(32)
 SB_GEMM_VB_ENTRY(64)
+SB_GEMM_VB_ENTRY(128)  // groups over 64 channels: each block reads its rows of S once
 
 // Adjoint state Sbar_g = mbar_g A_g^T (Section 4.3 eq. receiver_adjoint) on bf16 MFMA, streaming:
 // a block owns SB_SBR rows of mbar (kept in LDS in bf16, w contiguous) and walks its range of 64-wide

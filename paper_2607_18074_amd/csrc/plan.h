@@ -94,6 +94,7 @@ struct Kernels {
   hipFunction_t bwd_E = nullptr, dbwd_E = nullptr, dbwd_E_r = nullptr;
   hipFunction_t gemm_sa[3] = {}, gemm_sbar[3] = {}, gemm_ga[3] = {};  // BN = 16, 32, 64
   hipFunction_t gemm_sa_v[3] = {}, gemm_ga_v[3] = {}, gemm_sbar_v = nullptr;  // 16-byte aligned operands
+  hipFunction_t gemm_sa_vb128 = nullptr;  // bf16-GEMM plans: m = S A for groups over 64 channels
   std::map<int, hipFunction_t> gemm_sbar_c;  // streaming adjoint-state GEMM per output multiplicity
   hipFunction_t ga_reduce = nullptr, sender_reduce = nullptr, transpose = nullptr, fill_cols = nullptr,
                 zero = nullptr, sa_reduce = nullptr;
