@@ -254,3 +254,45 @@ def test_kept_groups(gpu, sig, N, E, seed):
     err = float(np.abs(a - b).max() / np.abs(b).max())
     print(f"{sig}: kept vs full state {err:.2e}")
     assert err <= 1e-6
+
+
+def test_kept_groups_channelwise_and_errors(gpu):
+    """Channelwise plans keep every output group or none (Appendix B.2): the retention choice of a plan
+    whose weight gradient is state-free is none; a full mask still keeps the state and the backward
+    reading it matches the oracle; a partial mask, a mask past the plan's groups and a NULL kept buffer
+    are rejected with SOBEK_E_INVALID."""
+    import ctypes
+    from paper_2607_18074_amd import api
+    from paper_2607_18074_amd._lib import SobekError, lib
+    sig = "uvu_small"
+    irr_in, lmax, irr_out, K = SIGS[sig]
+    case = make_case(sig, 90, 1000, 69, isolated=1, mode="uvu")
+    g = case["graph"]
+    plan = api.Plan(irr_in, lmax, irr_out, K, mode="uvu")
+    prob = oc.Problem(irr_in, lmax, irr_out, K, mode="uvu")
+    graph = api.Graph(_t(g.rowptr), _t(g.sender))
+    args = (_t(case["x"]), _t(g.evec), _t(g.phi), _t(case["W"]))
+    oa = (prob, case["x"], g.evec, g.phi, case["W"], g.rowptr, g.sender)
+    G = len(_groups(plan))
+    full = (1 << G) - 1
+    assert api.retention(plan, graph, 0) == (0, 0)          # state-free weight gradient: nothing to keep
+    assert api.kept_bytes(plan, graph, full) == api.state_floats(plan, graph) * 4
+    kept = api.new_kept(plan, graph, full)
+    out = api.conv_fwd(plan, graph, *args, keep=(full, kept))
+    assert max_rel(_n(out), oc.fwd(*oa)) <= FWD_TOL
+    outs = api.conv_bwd(plan, graph, *args, _t(case["gout"]), kept=(full, kept))
+    ref = oc.bwd(*oa, case["gout"])
+    for name, o in zip(("gx", "gevec", "gphi", "gW"), outs):
+        assert max_rel(_n(o), ref[name]) <= BWD_TOL, name
+    with pytest.raises(SobekError) as e:
+        api.conv_fwd(plan, graph, *args, keep=(1, kept))       # a partial mask
+    assert e.value.code == -1
+    with pytest.raises(SobekError) as e:
+        api.kept_bytes(plan, graph, 1 << G)                     # a group the plan does not have
+    assert e.value.code == -1
+    ws = graph.workspace(plan, "fwd")
+    o = api.conv_fwd(plan, graph, *args)
+    rc = lib().sobek_conv_fwd_keep(plan.handle, graph.handle, *[ctypes.c_void_p(t.data_ptr()) for t in args],
+                                   ctypes.c_void_p(o.data_ptr()), full, None, ctypes.c_void_p(ws.data_ptr()),
+                                   ws.numel(), None)
+    assert rc == -1                                             # kept buffer missing
