@@ -192,6 +192,12 @@ int sobek_graph_info(sobek_graph graph, int64_t *N, int64_t *E);
  * an edge-vector cotangent alone). */
 int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t budget, size_t *bytes);
 
+/* Streams: every conv_* call queues its work on `stream` and returns without synchronising.  Some
+ * calls run part of it on a second stream of the plan (the backward's weight gradient from a kept
+ * state, the double backward's dS GEMMs when the adjoint state is kept), forked from `stream` and
+ * joined back into it with events, so everything the call writes is ready for later work on
+ * `stream`; calls on one plan from several threads serialise that part. */
+
 /* Forward (Section 4.2): out[N][dim_out] = conv(x, evec, phi, W). */
 int sobek_conv_fwd(sobek_plan plan, sobek_graph graph, const float *x, const float *evec,
                    const float *phi, const float *W, float *out, void *ws, size_t ws_bytes,

@@ -40,6 +40,11 @@ using sobek::Plan;
 
 struct sobek_plan_s {
   Plan p;
+  // A second stream for channel GEMMs that overlap the edge stage of the same call, forked from and
+  // joined back into the caller's stream with events (created on first use, default priority).
+  std::mutex side_mu;
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
 };
 
 struct sobek_graph_s {
@@ -1164,6 +1169,9 @@ int sobek_plan_destroy(sobek_plan plan) {
   if (p.k.module_u) (void)hipModuleUnload(p.k.module_u);
   if (p.k.module_mat) (void)hipModuleUnload(p.k.module_mat);
   if (p.k.module_grp) (void)hipModuleUnload(p.k.module_grp);
+  if (plan->side) (void)hipStreamDestroy(plan->side);
+  if (plan->fork) (void)hipEventDestroy(plan->fork);
+  if (plan->join) (void)hipEventDestroy(plan->join);
   delete plan;
   return SOBEK_OK;
 }
@@ -1309,6 +1317,29 @@ int sobek_workspace_size(sobek_plan plan, sobek_graph graph, int pass, size_t bu
 
 namespace {
 
+// Fork: work queued on the returned side stream after this call runs after everything queued on
+// `main` so far.  The side stream is the plan's own; calls on one plan serialise their side work.
+int side_fork(sobek_plan plan, hipStream_t main, hipStream_t& side) {
+  std::lock_guard<std::mutex> lk(plan->side_mu);
+  if (!plan->side) {
+    HIPCHK(hipStreamCreateWithFlags(&plan->side, hipStreamNonBlocking));
+    HIPCHK(hipEventCreateWithFlags(&plan->fork, hipEventDisableTiming));
+    HIPCHK(hipEventCreateWithFlags(&plan->join, hipEventDisableTiming));
+  }
+  HIPCHK(hipEventRecord(plan->fork, main));
+  HIPCHK(hipStreamWaitEvent(plan->side, plan->fork, 0));
+  side = plan->side;
+  return SOBEK_OK;
+}
+
+// Join: work queued on `main` after this call runs after everything queued on the side stream so far.
+int side_join(sobek_plan plan, hipStream_t main) {
+  std::lock_guard<std::mutex> lk(plan->side_mu);
+  HIPCHK(hipEventRecord(plan->join, plan->side));
+  HIPCHK(hipStreamWaitEvent(main, plan->join, 0));
+  return SOBEK_OK;
+}
+
 // Forward; with `state` non-NULL the receiver state of every receiver is
 // computed into it in one pass (and kept), otherwise chunk by chunk in the workspace.
 // With keep_mask non-zero, the state of the output groups in it is computed into `keep` (every
@@ -1418,8 +1449,14 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   float* contrib = gx ? (float*)((char*)ws + w.off_contrib) : nullptr;
   const bool edge = gx || gevec || gphi;
   const Chunk all{0, (int)G.N, 0, G.E};
+  // the weight gradient from a kept state shares nothing with the adjoint-state GEMM and the edge
+  // windows that follow (its split partials have a region of their own): it runs beside them
+  bool side_open = false;
   if (gW && state && !uvu_wg) {
-    if ((rc = run_ga(p, all, w, ws, state, G.N, gk, gW, true, true, stream))) return rc;
+    hipStream_t side = stream;
+    if ((rc = side_fork(plan, stream, side))) return rc;
+    side_open = true;
+    if ((rc = run_ga(p, all, w, ws, state, G.N, gk, gW, true, true, side))) return rc;
   }
   if (gW && uvu_wg) {
     int na = 0, n = (int)G.N;
@@ -1473,6 +1510,7 @@ int conv_bwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const floa
   }
   if (gx && first_win && (rc = fill_zero(p, gxk, G.N * p.dim_in, stream))) return rc;  // no edges at all
   if (mulir && gx && (rc = transpose(p, gxk, gx, G.N, true, 1, stream))) return rc;
+  if (side_open && (rc = side_join(plan, stream))) return rc;
   return SOBEK_OK;
 }
 
@@ -1769,12 +1807,23 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
                                  g_gout ? ggk : nullptr, g_W, stream))))
     return rc;
   bool first_win = true;  // the first edge window overall initialises the sender cursors and x-gradient rows
+  // With the adjoint state kept and no dA cotangent, a chunk's dS GEMMs (m_dot = dS A, g_W += dS^T mbar)
+  // share nothing with its edge windows (they read the kept adjoint state, not the slot): they run
+  // beside them, and the next chunk's dS waits for them before it overwrites the slot.
+  const bool overlap = adj_state && !t_gW && !by_group;
+  bool side_open = false;
   for (size_t ci = 0; ci < w.chunks.size(); ++ci) {
     const Chunk& c = w.chunks[ci];
     if (tan && (g_gout || g_W) && !by_group) {
+      if (side_open && (rc = side_join(plan, stream))) return rc;   // the slot's previous dS is consumed
       if ((rc = run_state(p, G, c, w, dS, true, xk, evec, phi, txk, t_gevec, t_gphi, flags & 7, stream))) return rc;
-      if (g_gout && (rc = run_mix(p, c, w, ws, dS, W, ggk, 0, stream))) return rc;
-      if (g_W && (rc = run_ga(p, c, w, ws, dS, w.ncap, gk, g_W, ci == 0, ci + 1 == w.chunks.size(), stream)))
+      hipStream_t gs = stream;
+      if (overlap) {
+        if ((rc = side_fork(plan, stream, gs))) return rc;
+        side_open = true;
+      }
+      if (g_gout && (rc = run_mix(p, c, w, ws, dS, W, ggk, 0, gs))) return rc;
+      if (g_W && (rc = run_ga(p, c, w, ws, dS, w.ncap, gk, g_W, ci == 0, ci + 1 == w.chunks.size(), gs)))
         return rc;
     }
     if (t_gW && g_gout && !by_group) {  // S reuses the slot once dS has been consumed
@@ -1800,6 +1849,7 @@ int conv_dbwd_impl(sobek_plan plan, sobek_graph graph, const float* x, const flo
     }
   }
   if (g_x && first_win && (rc = fill_zero(p, gxk, G.N * p.dim_in, stream))) return rc;  // no edges at all
+  if (side_open && (rc = side_join(plan, stream))) return rc;
   if (g_gout && (rc = zero_dead_out(p, ggk, G.N, stream))) return rc;
   if (mulir) {
     if (g_gout && (rc = transpose(p, ggk, g_gout, G.N, false, 1, stream))) return rc;

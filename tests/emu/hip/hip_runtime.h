@@ -31,6 +31,8 @@ typedef enum hipFunction_attribute {
 } hipFunction_attribute;
 
 struct EmuSymbol { void* host; size_t bytes; };
+#define hipStreamNonBlocking 0x1
+#define hipEventDisableTiming 0x2
 #define HIP_SYMBOL(x) (&emu_symbol_##x)
 #define __device__
 #define __align__(n) __attribute__((aligned(n)))
@@ -43,6 +45,10 @@ hipError_t hipMemcpy(void* d, const void* s, size_t n, hipMemcpyKind k);
 hipError_t hipMemcpyAsync(void* d, const void* s, size_t n, hipMemcpyKind k, hipStream_t st);
 hipError_t hipMemsetAsync(void* d, int v, size_t n, hipStream_t st);
 hipError_t hipStreamSynchronize(hipStream_t s);
+hipError_t hipStreamCreateWithFlags(hipStream_t* s, unsigned flags);
+hipError_t hipStreamDestroy(hipStream_t s);
+hipError_t hipStreamWaitEvent(hipStream_t s, hipEvent_t e, unsigned flags);
+hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned flags);
 hipError_t hipEventCreate(hipEvent_t* e);
 hipError_t hipEventRecord(hipEvent_t e, hipStream_t s);
 hipError_t hipEventSynchronize(hipEvent_t e);

@@ -435,6 +435,16 @@ hipError_t hipMemsetAsync(void* d, int v, size_t n, hipStream_t) {
   return hipSuccess;
 }
 hipError_t hipStreamSynchronize(hipStream_t) { return hipSuccess; }
+// Launches run to completion in call order, so every stream is one stream and events order nothing
+// further; a created stream is a distinct non-null handle.
+hipError_t hipStreamCreateWithFlags(hipStream_t* s, unsigned) {
+  static int side;
+  *s = &side;
+  return hipSuccess;
+}
+hipError_t hipStreamDestroy(hipStream_t) { return hipSuccess; }
+hipError_t hipStreamWaitEvent(hipStream_t, hipEvent_t, unsigned) { return hipSuccess; }
+hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned) { return hipEventCreate(e); }
 hipError_t hipEventCreate(hipEvent_t* e) {
   static int dummy;
   *e = &dummy;
