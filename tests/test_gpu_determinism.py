@@ -7,7 +7,9 @@ atomics).  Two identical calls per route, every output compared with np.array_eq
 * channelwise backward and edge-vector double backward on the state-free kernels (per-wave weight-gradient
   partial rows and their fixed-order reduction; the per-slice edge partials of the multi-block form), in
   both backward forms, and the receiver route taken by general cotangents;
-* the bf16 channel-GEMM plan's forward, backward and double backward.
+* the bf16 channel-GEMM plan's forward, backward and double backward;
+* the passes that run part of their work on the plan's second stream, on a non-default caller stream
+  synchronised alone, against the default stream.
 """
 
 import numpy as np
@@ -86,3 +88,36 @@ def test_bf16_gemm_bitwise(gpu):
     _twice(lambda: [api.conv_fwd(plan, graph, *args)])
     _twice(lambda: api.conv_bwd(plan, graph, *args, gout))
     _twice(lambda: api.conv_dbwd(plan, graph, *args, gout, c["x"], c["evec"], c["phi"], c["W"]))
+
+
+def test_second_stream_joins_caller_stream(gpu):
+    """The backward's weight gradient from a kept state and the double backward's dS GEMMs run on a
+    second stream of the plan, joined back into the caller's stream: on a non-default caller stream,
+    synchronising that stream alone must leave every output complete, bitwise equal to a run on the
+    default stream (kept states, a workspace small enough for several double-backward chunks)."""
+    import torch
+    case = make_case("small", 300, 4000, 44, isolated=2)
+    api, plan, graph, args = _setup(case)
+    gout = _t(case["gout"])
+    tev = _t(case["cot"]["evec"])
+
+    def run():
+        state, adj = api.new_state(plan, graph), api.new_state(plan, graph)
+        m = api.conv_fwd(plan, graph, *args, state=state)
+        b = api.conv_bwd(plan, graph, *args, gout, state=state, adj_state=adj)
+        d = api.conv_dbwd(plan, graph, *args, gout, None, tev, None, None, adj_state=adj, budget=1 << 20)
+        return [m, *b, *d]
+
+    ref = [_n(o) for o in run()]
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        outs = run()
+    s.synchronize()
+    got = [o.cpu().numpy() if o is not None else None for o in outs]   # copies on the current stream
+    for i, (a, b) in enumerate(zip(ref, got)):
+        if a is None:
+            assert b is None
+            continue
+        assert np.array_equal(a, b), f"output {i} differs on a non-default caller stream"
